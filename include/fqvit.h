@@ -1,0 +1,141 @@
+/*
+ * fqvit.h -- C ABI of the MI355X (gfx950) library for the integer hot path of
+ * FQ-ViT (Lin et al., "FQ-ViT: Post-Training Quantization for Fully Quantized
+ * Vision Transformer", IJCAI 2022): Power-of-Two-Factor LayerNorm and
+ * Log-Int-Softmax attention.
+ *
+ * Conventions shared by every entry point
+ *   - Tensor arguments are DEVICE pointers into memory the caller owns (for
+ *     example allocated through torch).  The library allocates nothing, keeps
+ *     no state between calls, never synchronises, and enqueues its kernels on
+ *     `stream` (a hipStream_t; NULL is the default stream).  It is re-entrant.
+ *   - Scalars are passed by value.  Tensors are dense and row-major with the
+ *     shapes given below; a tensor is read or written only inside the extent
+ *     its shape gives.
+ *   - Every argument is validated on the host before anything is enqueued.  A
+ *     failing check returns its status code and enqueues nothing.  Empty
+ *     tensors (T, G or Lq equal to 0) return FQ_OK and enqueue nothing.
+ *   - Integer outputs are a pure function of the arguments (no atomics, no
+ *     order dependence): the same call gives the same bits every time.
+ *   - Quantized activations live on the paper's unsigned b-bit grid
+ *     {0 .. 2^b - 1} (Sec. 3.1, eq. 2).  The int8 containers used here hold
+ *     (paper value - 2^(b-1)); zero points are shifted the same way.  Every
+ *     formula uses only X_Q - zp, so results are identical on either grid.
+ */
+#ifndef FQVIT_H
+#define FQVIT_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum fq_status {
+    FQ_OK = 0,
+    FQ_ERR_NULL = 1,      /* a required pointer is NULL                              */
+    FQ_ERR_SHAPE = 2,     /* a size is out of the supported range                    */
+    FQ_ERR_PARAM = 3,     /* a scalar parameter is out of range                      */
+    FQ_ERR_HEADROOM = 4,  /* the exact integer sums could overflow 64 bits           */
+    FQ_ERR_HIP = 5        /* the HIP runtime rejected a launch                       */
+} fq_status;
+
+/* Static, human-readable name of a status code (never NULL). */
+const char* fq_status_str(int status);
+
+/* Library version as major * 10000 + minor * 100 + patch. */
+int32_t fq_version(void);
+
+/*
+ * PTF LayerNorm, integer-only (Sec. 3.2, eq. 12 for the shift; Supplement A.1
+ * for the statistics M1, M2, the factors A and B, their dyadic form N2 / 2^N1
+ * and the output Y_Q).
+ *
+ *   x_q     [T, C] int8 container of the PTF-quantized input X_Q.
+ *   zp_in   layer-wise zero point, container form, in [-2^(b-1), 2^(b-1) - 1].
+ *   alpha   [C] uint8 power-of-two factors; values above K are clamped to K.
+ *   K       0..7 (the paper uses 3).
+ *   gamma, beta  [C] float affine parameters.
+ *   s_out   output scale (> 0, finite); zp_out output zero point (container).
+ *   bits    b in [2, 8]; the output is clipped to the b-bit grid.
+ *   y_q     [T, C] int8 container output.
+ * The input scale cancels from A and B and is therefore not an argument.
+ * Per row: X^ = (X_Q - zp) << alpha, M1 = sum X^, M2 = sum X^^2,
+ * V = C M2 - M1^2; in IEEE double, D = sqrt(V), r = C / D, m = M1 / D,
+ * A = (gamma/s_out) r, B = beta/s_out - (gamma/s_out) m (each operation
+ * rounded on its own; A = 0 and B = beta/s_out when V = 0);
+ * N1 = clamp(b - 1 - floor(log2|A|), 0, 30), N2 = min(floor(|A| 2^N1), 2^31 - 1)
+ * (both 0 when A = 0); Y = clip(floor((sign(A) N2 X^ + rint(B 2^N1)
+ * + 2^(N1-1)) / 2^N1) + zp_out) (no half term when N1 = 0).
+ * Errors: FQ_ERR_NULL (x_q, alpha, gamma, beta or y_q NULL with T > 0),
+ * FQ_ERR_SHAPE (T < 0, C outside [1, 8192]), FQ_ERR_PARAM (bits, K, s_out or a
+ * zero point out of range).
+ */
+fq_status ptf_layernorm_int8(const int8_t* x_q, int64_t T, int32_t C, int32_t zp_in,
+                             const uint8_t* alpha, int32_t K, const float* gamma,
+                             const float* beta, float s_out, int32_t zp_out, int32_t bits,
+                             int8_t* y_q, void* stream);
+
+/*
+ * Log-Int-Softmax codes (Supplement A.2: Algorithm 1, I-Exp; Algorithm 2,
+ * I-Log2 and Log-Int-Softmax; the clip of the LIS equation in the same
+ * section).
+ *
+ *   logits  [G, Lq, Lk] int32 attention logits with scale s_logit
+ *           (G = attention units, e.g. batch x windows x heads).
+ *   bias    NULL or [Hb, Lq, Lk] int32 added to the logits of unit g from
+ *           head g % Hb before the row maximum (Swin relative-position bias).
+ *   s_logit in [1e-4, 0.5].
+ *   bits    code width b in [1, 4]; codes are Attn_Q in [0, 2^b - 1] and the
+ *           LIS output of the paper is N - Attn_Q with N = 2^b - 1, scale 2^-N.
+ *   exp_n   I-Exp clamp depth n in [1, 30]: inputs below n q_ln2 are clamped.
+ *   codes   [G, Lq, ld_codes] uint8 output, two codes per byte, the even key
+ *           in the low nibble; an odd row's last high nibble is 0; bytes at
+ *           and beyond ceil(Lk/2) in each row are not written.
+ * Per row: t_j = v_j - max v, e_j = I-Exp(t_j) with q_ln2 = floor(-ln2/s),
+ * q_b = floor(1.353/s), q_c = floor(0.344/((0.3585 s) s)) in IEEE double,
+ * S = sum e_j, Attn_Q_j = min(I-Log2(floor((2S + e_j) / (2 e_j))), 2^b - 1).
+ * Errors: FQ_ERR_NULL (logits or codes NULL with G Lq > 0), FQ_ERR_SHAPE
+ * (G or Lq < 0, Lk outside [1, 4096], ld_codes < ceil(Lk/2), Hb < 1 with a
+ * bias), FQ_ERR_PARAM (bits, exp_n or s_logit out of range), FQ_ERR_HEADROOM
+ * ((2 Lk + 1) (q_b^2 + q_c) 2^n >= 2^63).
+ * Precondition (not checked): |logit + bias| < 2^30.
+ */
+fq_status lis_softmax_log4(const int32_t* logits, int64_t G, int32_t Lq, int32_t Lk,
+                           const int32_t* bias, int32_t Hb, float s_logit, int32_t bits,
+                           int32_t exp_n, uint8_t* codes, int32_t ld_codes, void* stream);
+
+/*
+ * BitShift Attn x V (Sec. 3.3, eq. 16-17, and its zero-point form in
+ * Supplement A.2):
+ *   out[g, i, c] = sum_j (v[g, j, c] - zp_v) << ((2^b - 1) - code[g, i, j]).
+ *
+ *   codes   [G, Lq, ld_codes] packed codes as written by lis_softmax_log4.
+ *   v       [G, Lk, d] int8, zero point zp_v in [-128, 127].
+ *   bits    b in [1, 4] (shifts of at most 15).
+ *   out     [G, Lq, d] int32, scale s_V / 2^(2^b - 1).
+ * The sum is exact; it wraps modulo 2^32 only if it leaves int32, which codes
+ * produced by Log-Int-Softmax never do for Lk <= 4096.
+ * Errors: FQ_ERR_NULL, FQ_ERR_SHAPE (G or Lq < 0, Lk outside [1, 4096], d
+ * outside [1, 256], ld_codes < ceil(Lk/2)), FQ_ERR_PARAM (bits, zp_v).
+ */
+fq_status lis_attn_v_shift(const uint8_t* codes, int32_t ld_codes, const int8_t* v,
+                           int32_t zp_v, int64_t G, int32_t Lq, int32_t Lk, int32_t d,
+                           int32_t bits, int32_t* out, void* stream);
+
+/*
+ * Fused Log-Int-Softmax and BitShift Attn x V, the integer-only attention of
+ * Sec. 3.3 (the MSA dataflow of its Fig. 4): the same results as
+ * lis_softmax_log4 followed by lis_attn_v_shift, with the codes kept on chip.
+ * Arguments as in those two calls; d in [1, 256]; codes_out is NULL or a
+ * [G, Lq, ld_codes] buffer that also receives the codes.
+ */
+fq_status lis_attention_head(const int32_t* logits, const int32_t* bias, int32_t Hb,
+                             int64_t G, int32_t Lq, int32_t Lk, float s_logit, int32_t bits,
+                             int32_t exp_n, const int8_t* v, int32_t zp_v, int32_t d,
+                             int32_t* out, uint8_t* codes_out, int32_t ld_codes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FQVIT_H */

@@ -1,0 +1,469 @@
+/*
+ * fqvit_oracle.c -- plain, slow, scalar CPU oracle for FQ-ViT's integer hot path.
+ *
+ * TEST INFRASTRUCTURE ONLY: the test suite, the smoke check and the CPU
+ * baseline leg of the benchmark load this library; the HIP library never
+ * does and shares no code with it.
+ *
+ * Each function takes the paper's steps in the paper's order and notation:
+ *   Sec. 3.1, eq. (3)-(5)    uniform MinMax quantizer
+ *   Sec. 3.2, eq. (8)-(12)   PTF quantizer, its argmin for alpha, phase-1 shift
+ *   Supplement A.1           integer LayerNorm: M1, M2, the sqrt approximation,
+ *                            A, B, the dyadic N1/N2 form and the output Y_Q
+ *   Supplement A.2, Alg. 1   I-Exp
+ *   Supplement A.2, Alg. 2   I-Log2 and Log-Int-Softmax, with the clip of the
+ *                            LIS equation in the same section
+ *   Sec. 3.3 eq. (16)-(17)   BitShift Attn x V; the zero-point form of the same
+ *   and Supplement A.2       product in the supplement
+ *
+ * Integers are exact (int64, or unsigned __int128 where a sum could be wide).
+ * Real-valued quantities that the paper leaves as reals are IEEE double with
+ * every operation rounded separately (build with -ffp-contract=off).
+ * Choices the paper does not fix are marked READING.
+ *
+ * Build: gcc -std=gnu11 -O2 -ffp-contract=off -fno-fast-math -fPIC -shared
+ */
+#include "fqvit_oracle.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ------------------------------------------------------------------------ */
+/* small exact helpers                                                       */
+/* ------------------------------------------------------------------------ */
+
+/* floor(a / b) for integers of any sign, b != 0. */
+static int64_t floor_div(int64_t a, int64_t b) {
+    int64_t q = a / b;
+    int64_t r = a % b;
+    if (r != 0 && ((r < 0) != (b < 0))) q -= 1;
+    return q;
+}
+
+static int64_t clip_i64(int64_t x, int64_t lo, int64_t hi) {
+    return x < lo ? lo : (x > hi ? hi : x);
+}
+
+static double clip_d(double x, double lo, double hi) {
+    return x < lo ? lo : (x > hi ? hi : x);
+}
+
+/* The paper's rounding bracket.  READING: ties are not specified; the oracle
+ * uses round-half-to-even, which is what nearbyint() does in the default
+ * rounding mode. */
+static double round_nearest(double x) { return nearbyint(x); }
+
+/* ------------------------------------------------------------------------ */
+/* Sec. 3.1, eq. (3)-(5): uniform MinMax quantizer                           */
+/* ------------------------------------------------------------------------ */
+
+int oracle_minmax_params(const double* x, int64_t n, int32_t b, double* s, int32_t* zp) {
+    if (!x || !s || !zp || n <= 0 || b < 1 || b > 16) return ORACLE_ERR_ARG;
+    double l = x[0], u = x[0];                        /* eq. (4) */
+    for (int64_t i = 1; i < n; ++i) {
+        if (x[i] < l) l = x[i];
+        if (x[i] > u) u = x[i];
+    }
+    const double levels = (double)((1 << b) - 1);
+    *s = (u - l) / levels;                            /* eq. (5) */
+    if (!(*s > 0.0)) return ORACLE_ERR_ARG;
+    *zp = (int32_t)clip_d(round_nearest(-l / *s), 0.0, levels);
+    return ORACLE_OK;
+}
+
+int oracle_minmax_quantize(const double* x, int64_t n, double s, int32_t zp, int32_t b,
+                           int32_t* q) {
+    if (!x || !q || n < 0 || b < 1 || b > 16 || !(s > 0.0)) return ORACLE_ERR_ARG;
+    const double levels = (double)((1 << b) - 1);
+    for (int64_t i = 0; i < n; ++i)                   /* eq. (3) */
+        q[i] = (int32_t)clip_d(round_nearest(x[i] / s) + (double)zp, 0.0, levels);
+    return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Sec. 3.2, eq. (8)-(11): Power-of-Two-Factor quantizer                      */
+/* ------------------------------------------------------------------------ */
+
+int oracle_ptf_params(const double* x, int64_t T, int32_t C, int32_t b, int32_t K,
+                      double* s, int32_t* zp) {
+    if (!x || !s || !zp || T <= 0 || C <= 0 || b < 1 || b > 16 || K < 0 || K > 30)
+        return ORACLE_ERR_ARG;
+    const int64_t n = T * (int64_t)C;
+    double mn = x[0], mx = x[0];
+    for (int64_t i = 1; i < n; ++i) {
+        if (x[i] < mn) mn = x[i];
+        if (x[i] > mx) mx = x[i];
+    }
+    const double levels = (double)((1 << b) - 1);
+    const double two_K = ldexp(1.0, K);
+    *s = (mx - mn) / levels / two_K;                  /* eq. (9)  */
+    if (!(*s > 0.0)) return ORACLE_ERR_ARG;
+    *zp = (int32_t)clip_d(round_nearest(-mn / (two_K * *s)), 0.0, levels);   /* eq. (10) */
+    return ORACLE_OK;
+}
+
+/* eq. (8) for one value on the unsigned grid. */
+static double ptf_q(double x, double s, int32_t zp, int32_t alpha, double levels) {
+    return clip_d(round_nearest(x / (ldexp(1.0, alpha) * s)) + (double)zp, 0.0, levels);
+}
+
+int oracle_ptf_alpha(const double* x, int64_t T, int32_t C, double s, int32_t zp, int32_t b,
+                     int32_t K, uint8_t* alpha) {
+    if (!x || !alpha || T <= 0 || C <= 0 || b < 1 || b > 16 || K < 0 || K > 7 || !(s > 0.0))
+        return ORACLE_ERR_ARG;
+    const double levels = (double)((1 << b) - 1);
+    for (int32_t c = 0; c < C; ++c) {
+        /* eq. (11): alpha_c = argmin over {0..K} of || X_c - dequant(quant(X_c)) ||_2.
+         * READING: the printed argmin omits zp and the clip; taken literally the
+         * finest grid always wins.  The error is measured on the quantizer that
+         * is actually used, eq. (8) with its zp and clip.  Ties go to the
+         * smallest alpha. */
+        int32_t best = 0;
+        double best_err = INFINITY;
+        for (int32_t a = 0; a <= K; ++a) {
+            const double step = ldexp(1.0, a) * s;
+            double err = 0.0;
+            for (int64_t t = 0; t < T; ++t) {
+                const double xv = x[t * C + c];
+                const double deq = (ptf_q(xv, s, zp, a, levels) - (double)zp) * step;
+                err += (xv - deq) * (xv - deq);
+            }
+            if (err < best_err) {
+                best_err = err;
+                best = a;
+            }
+        }
+        alpha[c] = (uint8_t)best;
+    }
+    return ORACLE_OK;
+}
+
+int oracle_ptf_quantize(const double* x, int64_t T, int32_t C, double s, int32_t zp,
+                        const uint8_t* alpha, int32_t b, int32_t* q) {
+    if (!x || !alpha || !q || T < 0 || C <= 0 || b < 1 || b > 16 || !(s > 0.0))
+        return ORACLE_ERR_ARG;
+    const double levels = (double)((1 << b) - 1);
+    for (int64_t t = 0; t < T; ++t)
+        for (int32_t c = 0; c < C; ++c)
+            q[t * C + c] = (int32_t)ptf_q(x[t * C + c], s, zp, alpha[c], levels);
+    return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Supplement A.1: quantized inference of LayerNorm with PTF                  */
+/* ------------------------------------------------------------------------ */
+
+int oracle_ptf_layernorm_int8(const int8_t* x_q, int64_t T, int32_t C, int32_t zp_in,
+                              const uint8_t* alpha, int32_t K, const float* gamma,
+                              const float* beta, float s_out, int32_t zp_out, int32_t bits,
+                              int8_t* y_q) {
+    if (T < 0 || C < 1 || bits < 2 || bits > 8 || K < 0 || K > 7 || !(s_out > 0.0f))
+        return ORACLE_ERR_ARG;
+    if (T == 0) return ORACLE_OK;
+    if (!x_q || !alpha || !gamma || !beta || !y_q) return ORACLE_ERR_ARG;
+
+    /* READING (containers): activations are unsigned b-bit integers in the paper
+     * (eq. 2, 8).  The int8 container holds (paper value - 2^(b-1)); zero points
+     * are shifted the same way.  Convert to the paper's grid first. */
+    const int64_t half = (int64_t)1 << (bits - 1);
+    const int64_t levels = ((int64_t)1 << bits) - 1;
+    const int64_t zp = (int64_t)zp_in + half;
+    const int64_t zp_o = (int64_t)zp_out + half;
+    if (zp < 0 || zp > levels || zp_o < 0 || zp_o > levels) return ORACLE_ERR_ARG;
+
+    int64_t* Xh = (int64_t*)malloc(sizeof(int64_t) * (size_t)C);
+    if (!Xh) return ORACLE_ERR_ARG;
+
+    for (int64_t t = 0; t < T; ++t) {
+        const int8_t* row = x_q + t * C;
+
+        /* Phase 1: X^_Q = (X_Q - zp) << alpha.
+         * READING: alpha > K is not defined by the paper; it is clamped to K. */
+        for (int32_t i = 0; i < C; ++i) {
+            const int64_t XQ = (int64_t)row[i] + half;
+            const int32_t a = alpha[i] < K ? alpha[i] : K;
+            Xh[i] = (XQ - zp) * ((int64_t)1 << a);
+        }
+
+        /* Phase 2: M1 = sum X^_Q, M2 = sum X^_Q^2 (integers). */
+        int64_t M1 = 0, M2 = 0;
+        for (int32_t i = 0; i < C; ++i) {
+            M1 += Xh[i];
+            M2 += Xh[i] * Xh[i];
+        }
+        /* sigma^2 ~ (s^2/C^2)(C M2 - M1^2) and sqrt(sigma^2 + eps) ~ (s/C) sqrt(C M2 - M1^2):
+         * the epsilon is dropped by the approximation. */
+        const int64_t Vr = (int64_t)C * M2 - M1 * M1;
+
+        for (int32_t i = 0; i < C; ++i) {
+            /* A = s_in gamma / (s_out sqrt(sigma^2+eps)),
+             * B = (beta sqrt(sigma^2+eps) - gamma mu) / (s_out sqrt(sigma^2+eps)),
+             * with mu = (s/C) M1 and sqrt(sigma^2+eps) = (s/C) sqrt(Vr).  The input
+             * scale s_in = s cancels:  A = gamma * C / (s_out sqrt(Vr)),
+             * B = beta/s_out - gamma * M1 / (s_out sqrt(Vr)).
+             * READING (floating-point order): the paper leaves A and B real.  They
+             * are evaluated in IEEE double as gs = gamma/s_out, bs = beta/s_out,
+             * D = sqrt(Vr), r = C/D, m = M1/D, A = gs*r, B = bs - gs*m, each
+             * operation rounded on its own.
+             * READING (constant row): for Vr = 0 the normalised value (X - mu)/sigma
+             * is zero, so A = 0 and B = beta/s_out. */
+            const double gs = (double)gamma[i] / (double)s_out;
+            const double bs = (double)beta[i] / (double)s_out;
+            double A, B;
+            if (Vr == 0) {
+                A = 0.0;
+                B = bs;
+            } else {
+                const double D = sqrt((double)Vr);
+                const double r = (double)C / D;
+                const double m = (double)M1 / D;
+                A = gs * r;
+                B = bs - gs * m;
+            }
+
+            /* N1 = b - 1 - floor(log2|A|), N2 = floor(|A| 2^N1), A ~ sign(A) N2 / 2^N1.
+             * READING: for A = 0 (gamma = 0 or a constant row) N1 = N2 = 0; N1 is
+             * clamped to [0, 30] and N2 to 2^31 - 1 (never reached on sane scales). */
+            int64_t N1 = 0, N2 = 0, sgn = 1;
+            if (A != 0.0) {
+                N1 = (int64_t)bits - 1 - (int64_t)ilogb(fabs(A));
+                N1 = clip_i64(N1, 0, 30);
+                const double scaled = ldexp(fabs(A), (int)N1);
+                N2 = scaled >= 2147483647.0 ? 2147483647 : (int64_t)floor(scaled);
+                sgn = A < 0.0 ? -1 : 1;
+            }
+
+            /* round(B 2^N1) with ties to even (READING).  READING: clamped to
+             * +-2^62 so that it fits int64; any value that large saturates Y_Q. */
+            const double Bs = clip_d(round_nearest(ldexp(B, (int)N1)), -0x1p62, 0x1p62);
+            const int64_t Bq = (int64_t)Bs;
+
+            /* Y_Q = round((sign(A) N2 X^_Q + round(B 2^N1)) / 2^N1) + zp_out.
+             * READING: the outer rounding of this dyadic division rounds halves
+             * up, floor((y + 2^(N1-1)) / 2^N1).  READING: the output is clipped
+             * to the b-bit grid [0, 2^b - 1], as every activation is. */
+            const int64_t y = sgn * N2 * Xh[i] + Bq;
+            const int64_t w = (N1 == 0) ? y : floor_div(y + ((int64_t)1 << (N1 - 1)),
+                                                         (int64_t)1 << N1);
+            const int64_t YQ = clip_i64(w + zp_o, 0, levels);
+            y_q[t * C + i] = (int8_t)(YQ - half);
+        }
+    }
+    free(Xh);
+    return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Supplement A.2, Algorithm 1: integer-only exponential                     */
+/* ------------------------------------------------------------------------ */
+
+/* Coefficients of L(p) = a (p + b)^2 + c, the second-order fit of exp on (-ln2, 0]. */
+static const double IEXP_A = 0.3585;
+static const double IEXP_B = 1.353;
+static const double IEXP_C = 0.344;
+static const double LN2 = 0.69314718055994530942;
+
+int oracle_iexp_constants(double s, int32_t n, oracle_iexp_consts* k) {
+    if (!k || !(s > 0.0) || n < 0 || n > 62) return ORACLE_ERR_ARG;
+    k->q_ln2 = (int64_t)floor(-LN2 / s);                  /* q_ln2 = floor(-ln2/s)      */
+    k->q_b = (int64_t)floor(IEXP_B / s);                  /* q_b   = floor(b/s)         */
+    k->q_c = (int64_t)floor(IEXP_C / ((IEXP_A * s) * s)); /* q_c   = floor(c/(a s^2))   */
+    /* READING: the algorithm prints s_L <- floor(a s^2), which is 0 for any
+     * useful scale; the output scale is the real a s^2. */
+    k->s_L = (IEXP_A * s) * s;
+    k->n = n;
+    return ORACLE_OK;
+}
+
+int64_t oracle_iexp(int64_t q, const oracle_iexp_consts* k, int64_t* z_out, int64_t* qp_out) {
+    /* q <- max(q, n q_ln2).  READING: n, the clamp depth, is not defined by the
+     * paper; it is an argument (2^-n is the smallest value i-exp can return
+     * relative to exp(0)). */
+    const int64_t floor_q = (int64_t)k->n * k->q_ln2;
+    if (q < floor_q) q = floor_q;
+    const int64_t z = floor_div(q, k->q_ln2);             /* z   = floor(q / q_ln2)     */
+    const int64_t q_p = q - z * k->q_ln2;                 /* q_p = q - z q_ln2          */
+    /* READING: the algorithm prints q_L = (q + q_b)^2 + q_c; the polynomial is
+     * evaluated at p, i.e. at q_p (L(p) = a(p + b)^2 + c). */
+    const int64_t q_L = (q_p + k->q_b) * (q_p + k->q_b) + k->q_c;
+    if (z_out) *z_out = z;
+    if (qp_out) *qp_out = q_p;
+    /* q_out = q_L << (n - z), output scale s_L / 2^n. */
+    return q_L * ((int64_t)1 << (k->n - z));
+}
+
+/* ------------------------------------------------------------------------ */
+/* Supplement A.2, Algorithm 2: I-Log2 and Log-Int-Softmax                   */
+/* ------------------------------------------------------------------------ */
+
+/* Find_First_One: index of the most significant 1 bit (-1 for q = 0). */
+static int32_t find_first_one(uint64_t q) {
+    for (int32_t i = 63; i >= 0; --i)
+        if ((q >> i) & 1u) return i;
+    return -1;
+}
+
+int32_t oracle_ilog2(uint64_t q) {
+    const int32_t M = find_first_one(q);
+    if (M < 0) return 0;
+    /* chi = the (M-1)th bit of q.  READING: for M = 0 there is no such bit; chi = 0. */
+    const int32_t chi = (M >= 1) ? (int32_t)((q >> (M - 1)) & 1u) : 0;
+    return M + chi;
+}
+
+static int lis_check(int64_t G, int32_t Lq, int32_t Lk, int32_t bits, int32_t exp_n,
+                     float s_logit) {
+    if (G < 0 || Lq < 0 || Lk < 1 || bits < 1 || bits > 4 || exp_n < 1 || exp_n > 30 ||
+        !(s_logit > 0.0f))
+        return ORACLE_ERR_ARG;
+    return ORACLE_OK;
+}
+
+/* One row of Log-Int-Softmax: Attn_Q for every key.  v holds logits + bias. */
+static void lis_row(const int64_t* v, int32_t Lk, const oracle_iexp_consts* k, int32_t bits,
+                    int64_t* e, int32_t* code) {
+    /* q~ = q - max(q) */
+    int64_t mx = v[0];
+    for (int32_t j = 1; j < Lk; ++j)
+        if (v[j] > mx) mx = v[j];
+    /* q_exp = I-Exp(q~) and its sum (a wide integer, so it cannot wrap). */
+    unsigned __int128 sum = 0;
+    for (int32_t j = 0; j < Lk; ++j) {
+        e[j] = oracle_iexp(v[j] - mx, k, NULL, NULL);
+        sum += (unsigned __int128)e[j];
+    }
+    const int32_t top = (1 << bits) - 1;
+    for (int32_t j = 0; j < Lk; ++j) {
+        /* q_rev = round(sum(q_exp) / q_exp).  READING: ties round up,
+         * floor((2 sum + q_exp) / (2 q_exp)). */
+        const unsigned __int128 ej = (unsigned __int128)e[j];
+        const unsigned __int128 q_rev = (2 * sum + ej) / (2 * ej);
+        const uint64_t q_rev64 = q_rev > (unsigned __int128)UINT64_MAX
+                                     ? UINT64_MAX : (uint64_t)q_rev;
+        /* Attn_Q = clip(I-Log2(q_rev), 0, 2^b - 1); the LIS output is N - Attn_Q
+         * with N = 2^b - 1 and scale 1/2^N.  The clip is in the LIS equation of
+         * the supplement (Algorithm 2 omits it). */
+        int32_t a = oracle_ilog2(q_rev64);
+        if (a > top) a = top;
+        code[j] = a;
+    }
+}
+
+int oracle_lis_softmax_log4(const int32_t* logits, int64_t G, int32_t Lq, int32_t Lk,
+                            const int32_t* bias, int32_t Hb, float s_logit, int32_t bits,
+                            int32_t exp_n, uint8_t* codes, int32_t ld_codes) {
+    if (lis_check(G, Lq, Lk, bits, exp_n, s_logit) != ORACLE_OK) return ORACLE_ERR_ARG;
+    if (ld_codes < (Lk + 1) / 2) return ORACLE_ERR_ARG;
+    if (bias && Hb < 1) return ORACLE_ERR_ARG;
+    if (G == 0 || Lq == 0) return ORACLE_OK;
+    if (!logits || !codes) return ORACLE_ERR_ARG;
+
+    oracle_iexp_consts k;
+    if (oracle_iexp_constants((double)s_logit, exp_n, &k) != ORACLE_OK) return ORACLE_ERR_ARG;
+
+    int64_t* v = (int64_t*)malloc(sizeof(int64_t) * (size_t)Lk);
+    int64_t* e = (int64_t*)malloc(sizeof(int64_t) * (size_t)Lk);
+    int32_t* code = (int32_t*)malloc(sizeof(int32_t) * (size_t)Lk);
+    if (!v || !e || !code) {
+        free(v); free(e); free(code);
+        return ORACLE_ERR_ARG;
+    }
+    for (int64_t g = 0; g < G; ++g) {
+        for (int32_t i = 0; i < Lq; ++i) {
+            const int32_t* q = logits + (g * Lq + i) * (int64_t)Lk;
+            /* READING: a relative-position bias (Swin) is part of the logit and is
+             * added before the row maximum. */
+            const int32_t* bq = bias ? bias + ((g % Hb) * Lq + i) * (int64_t)Lk : NULL;
+            for (int32_t j = 0; j < Lk; ++j) v[j] = (int64_t)q[j] + (bq ? bq[j] : 0);
+            lis_row(v, Lk, &k, bits, e, code);
+            /* READING (storage): 4-bit codes, two per byte, even key in the low nibble. */
+            uint8_t* out = codes + (g * Lq + i) * (int64_t)ld_codes;
+            for (int32_t j = 0; j < Lk; j += 2) {
+                const int32_t lo = code[j];
+                const int32_t hi = (j + 1 < Lk) ? code[j + 1] : 0;
+                out[j / 2] = (uint8_t)(lo | (hi << 4));
+            }
+        }
+    }
+    free(v); free(e); free(code);
+    return ORACLE_OK;
+}
+
+int oracle_lis_row_exp(const int32_t* row, const int32_t* bias_row, int32_t Lk, float s_logit,
+                       int32_t exp_n, int64_t* e_out, double* sum_out) {
+    if (!row || !e_out || Lk < 1 || exp_n < 1 || exp_n > 30 || !(s_logit > 0.0f))
+        return ORACLE_ERR_ARG;
+    oracle_iexp_consts k;
+    if (oracle_iexp_constants((double)s_logit, exp_n, &k) != ORACLE_OK) return ORACLE_ERR_ARG;
+    int64_t mx = (int64_t)row[0] + (bias_row ? bias_row[0] : 0);
+    for (int32_t j = 1; j < Lk; ++j) {
+        const int64_t vj = (int64_t)row[j] + (bias_row ? bias_row[j] : 0);
+        if (vj > mx) mx = vj;
+    }
+    double sum = 0.0;
+    for (int32_t j = 0; j < Lk; ++j) {
+        const int64_t vj = (int64_t)row[j] + (bias_row ? bias_row[j] : 0);
+        e_out[j] = oracle_iexp(vj - mx, &k, NULL, NULL);
+        sum += (double)e_out[j];
+    }
+    if (sum_out) *sum_out = sum;
+    return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Sec. 3.3 eq. (16)-(17), Supplement A.2: BitShift Attn x V                 */
+/* ------------------------------------------------------------------------ */
+
+int oracle_lis_attn_v_shift(const uint8_t* codes, int32_t ld_codes, const int8_t* v,
+                            int32_t zp_v, int64_t G, int32_t Lq, int32_t Lk, int32_t d,
+                            int32_t bits, int32_t* out) {
+    if (G < 0 || Lq < 0 || Lk < 1 || d < 1 || bits < 1 || bits > 4 || ld_codes < (Lk + 1) / 2 ||
+        zp_v < -128 || zp_v > 127)
+        return ORACLE_ERR_ARG;
+    if (G == 0 || Lq == 0) return ORACLE_OK;
+    if (!codes || !v || !out) return ORACLE_ERR_ARG;
+    /* N = 2^b - 1; Attn x V = (s_V / 2^N) * sum_j (V_Q - zp_V) << (N - Attn_Q).
+     * The main-text form omits zp_V; the supplement's form includes it. */
+    const int32_t N = (1 << bits) - 1;
+    int rc = ORACLE_OK;
+    for (int64_t g = 0; g < G; ++g) {
+        for (int32_t i = 0; i < Lq; ++i) {
+            const uint8_t* crow = codes + (g * Lq + i) * (int64_t)ld_codes;
+            for (int32_t c = 0; c < d; ++c) {
+                int64_t acc = 0;
+                for (int32_t j = 0; j < Lk; ++j) {
+                    const int32_t byte = crow[j / 2];
+                    const int32_t attn_q = (j % 2 == 0) ? (byte & 15) : (byte >> 4);
+                    const int32_t shift = N - attn_q;
+                    const int64_t vq = (int64_t)v[(g * Lk + j) * (int64_t)d + c] - zp_v;
+                    acc += vq * ((int64_t)1 << (shift < 0 ? 0 : shift));
+                    if (shift < 0) rc = ORACLE_ERR_ARG;   /* a code above 2^b - 1 */
+                }
+                if (acc > INT32_MAX || acc < INT32_MIN) rc = ORACLE_ERR_RANGE;
+                out[(g * Lq + i) * (int64_t)d + c] = (int32_t)(uint32_t)(uint64_t)acc;
+            }
+        }
+    }
+    return rc;
+}
+
+int oracle_lis_attention_head(const int32_t* logits, const int32_t* bias, int32_t Hb,
+                              int64_t G, int32_t Lq, int32_t Lk, float s_logit, int32_t bits,
+                              int32_t exp_n, const int8_t* v, int32_t zp_v, int32_t d,
+                              int32_t* out, uint8_t* codes_out, int32_t ld_codes) {
+    if (lis_check(G, Lq, Lk, bits, exp_n, s_logit) != ORACLE_OK || d < 1) return ORACLE_ERR_ARG;
+    const int32_t ld = (Lk + 1) / 2;
+    if (codes_out && ld_codes < ld) return ORACLE_ERR_ARG;
+    if (G == 0 || Lq == 0) return ORACLE_OK;
+    uint8_t* tmp = (uint8_t*)malloc((size_t)(G * Lq) * (size_t)ld);
+    if (!tmp) return ORACLE_ERR_ARG;
+    int rc = oracle_lis_softmax_log4(logits, G, Lq, Lk, bias, Hb, s_logit, bits, exp_n, tmp, ld);
+    if (rc == ORACLE_OK)
+        rc = oracle_lis_attn_v_shift(tmp, ld, v, zp_v, G, Lq, Lk, d, bits, out);
+    if (rc == ORACLE_OK && codes_out)
+        for (int64_t r = 0; r < G * Lq; ++r)
+            memcpy(codes_out + r * ld_codes, tmp + r * ld, (size_t)ld);
+    free(tmp);
+    return rc;
+}

@@ -1,0 +1,79 @@
+"""The oracle's pins must catch plausible mistakes.
+
+Each case plants one slip (a dropped term, a wrong sign, a wrong index, a
+transposed operand, a garbled formula read literally) in a copy of the oracle's
+C source, builds that copy on the CPU, and runs the pin suite against it: the
+suite must fail.  Nothing here touches the GPU or the HIP library.
+"""
+import concurrent.futures as cf
+import os
+import subprocess
+import sys
+import tempfile
+
+import pytest
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(HERE)
+SRC = os.path.join(ROOT, "oracle", "fqvit_oracle.c")
+
+# (name, original text, planted mistake)
+MUTANTS = [
+    ("ptf_shift_direction", "(XQ - zp) * ((int64_t)1 << a)", "(XQ - zp) * ((int64_t)1 << (K - a))"),
+    ("ptf_zero_point_dropped", "Xh[i] = (XQ - zp) *", "Xh[i] = (XQ) *"),
+    ("variance_sign", "(int64_t)C * M2 - M1 * M1", "(int64_t)C * M2 + M1 * M1"),
+    ("variance_sqrt_dropped", "const double D = sqrt((double)Vr);", "const double D = (double)Vr;"),
+    ("B_sign", "B = bs - gs * m;", "B = bs + gs * m;"),
+    ("r_transposed", "const double r = (double)C / D;", "const double r = D / (double)C;"),
+    ("mean_uses_M2", "const double m = (double)M1 / D;", "const double m = (double)M2 / D;"),
+    ("N1_off_by_one", "(int64_t)bits - 1 - (int64_t)ilogb", "(int64_t)bits - (int64_t)ilogb"),
+    ("outer_round_dropped", "floor_div(y + ((int64_t)1 << (N1 - 1)),", "floor_div(y,"),
+    ("zp_out_dropped", "clip_i64(w + zp_o, 0, levels)", "clip_i64(w, 0, levels)"),
+    ("ln_sign_dropped", "const int64_t y = sgn * N2 * Xh[i] + Bq;", "const int64_t y = N2 * Xh[i] + Bq;"),
+    ("q_ln2_ceil", "(int64_t)floor(-LN2 / s)", "(int64_t)ceil(-LN2 / s)"),
+    ("q_c_missing_s", "IEXP_C / ((IEXP_A * s) * s)", "IEXP_C / (IEXP_A * s)"),
+    ("q_L_as_printed", "(q_p + k->q_b) * (q_p + k->q_b) + k->q_c", "(q + k->q_b) * (q + k->q_b) + k->q_c"),
+    ("q_c_dropped", "(q_p + k->q_b) * (q_p + k->q_b) + k->q_c", "(q_p + k->q_b) * (q_p + k->q_b)"),
+    ("exp_shift_direction", "q_L * ((int64_t)1 << (k->n - z))", "q_L * ((int64_t)1 << z)"),
+    ("clamp_dropped", "if (q < floor_q) q = floor_q;", "if (q < 2 * floor_q) q = 2 * floor_q;"),
+    ("max_not_subtracted", "e[j] = oracle_iexp(v[j] - mx, k, NULL, NULL);", "e[j] = oracle_iexp(v[j] - v[0], k, NULL, NULL);"),
+    ("q_rev_floor", "(2 * sum + ej) / (2 * ej)", "(2 * sum) / (2 * ej)"),
+    ("chi_wrong_bit", "(q >> (M - 1)) & 1u", "(q >> (M - 2)) & 1u"),
+    ("chi_dropped", "return M + chi;", "return M;"),
+    ("code_clip_dropped", "if (a > top) a = top;", "if (a > top) a = a & top;"),
+    ("nibble_order", "(uint8_t)(lo | (hi << 4))", "(uint8_t)(hi | (lo << 4))"),
+    ("bias_wrong_head", "bias + ((g % Hb) * Lq + i)", "bias + ((g / Hb % Hb) * Lq + i)"),
+    ("av_zp_dropped", "(int64_t)v[(g * Lk + j) * (int64_t)d + c] - zp_v;", "(int64_t)v[(g * Lk + j) * (int64_t)d + c];"),
+    ("av_shift_is_code", "((int64_t)1 << (shift < 0 ? 0 : shift))", "((int64_t)1 << attn_q)"),
+    ("av_v_transposed", "v[(g * Lk + j) * (int64_t)d + c]", "v[(g * d + c) * (int64_t)Lk + j]"),
+    ("ptf_scale_times_2K", "(mx - mn) / levels / two_K", "(mx - mn) / levels * two_K"),
+    ("ptf_quant_neg_alpha", "x / (ldexp(1.0, alpha) * s)", "x / (ldexp(1.0, -alpha) * s)"),
+    ("minmax_zp_sign", "round_nearest(-l / *s)", "round_nearest(l / *s)"),
+]
+
+
+def _run_mutant(name, old, new, tmp):
+    src = open(SRC).read()
+    assert src.count(old) >= 1, f"{name}: pattern not found in the oracle source"
+    mutated = src.replace(old, new)
+    csrc = os.path.join(tmp, f"{name}.c")
+    so = os.path.join(tmp, f"{name}.so")
+    with open(csrc, "w") as f:
+        f.write(mutated)
+    sys.path.insert(0, ROOT)
+    import oracle
+    oracle.build(src=csrc, out=so)
+    env = dict(os.environ, FQVIT_ORACLE_LIB=so, PYTHONDONTWRITEBYTECODE="1")
+    r = subprocess.run([sys.executable, "-m", "pytest", os.path.join(HERE, "test_oracle_pins.py"),
+                        "-x", "-q", "-p", "no:cacheprovider", "-m", "not gpu"],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    return name, r.returncode
+
+
+def test_every_planted_mistake_is_caught():
+    with tempfile.TemporaryDirectory() as tmp:
+        workers = min(8, os.cpu_count() or 2)
+        with cf.ThreadPoolExecutor(workers) as ex:
+            results = list(ex.map(lambda m: _run_mutant(*m, tmp), MUTANTS))
+    survivors = [n for n, rc in results if rc == 0]
+    assert not survivors, f"mutants not caught by the pins: {survivors}"

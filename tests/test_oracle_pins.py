@@ -1,0 +1,464 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Each test ties an oracle function to something other than itself: a value the
+paper prints, a closed form, an invariant, a special case that reduces to a
+textbook routine or a library primitive, or the paper's error bound.  None of
+these tests touches the GPU.
+"""
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import workloads as W
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+S = 2.0 ** -10
+
+
+def _golden(name):
+    rows = []
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            line = line.strip()
+            if line and not line.startswith("#"):
+                rows.append(line.split())
+    return rows
+
+
+def ilog2_closed_form(r: int) -> int:
+    """M + chi with chi the bit below the leading one is the integer k with
+    3 * 2^k <= 4 r < 3 * 2^(k+1), i.e. floor(log2(4 r / 3)): rounding log2 at
+    1.5 * 2^M.  Written with exact integers."""
+    k = 0
+    while 3 * 2 ** (k + 1) <= 4 * r:
+        k += 1
+    return k
+
+
+# ---------------------------------------------------------------------------
+# I-Log2 (Algorithm 2)
+# ---------------------------------------------------------------------------
+
+def test_ilog2_worked_example(orc):
+    (binary, M, chi, result), = _golden("ilog2_worked_example.txt")
+    q = int(binary, 2)
+    assert q == 3500
+    assert orc.ilog2(q) == int(result) == int(M) + int(chi)
+
+
+def test_ilog2_closed_form_exhaustive(orc):
+    # every r < 2^16 exhaustively, then a strided sweep to 2^20 and powers of two
+    rs = list(range(1, 1 << 16)) + list(range(1 << 16, 1 << 20, 97))
+    rs += [1 << k for k in range(0, 62)] + [(1 << k) - 1 for k in range(2, 62)]
+    rs += [3 << k for k in range(0, 60)] + [(3 << k) - 1 for k in range(1, 60)]
+    bad = [r for r in rs if orc.ilog2(r) != ilog2_closed_form(r)]
+    assert not bad, bad[:10]
+
+
+# ---------------------------------------------------------------------------
+# I-Exp (Algorithm 1)
+# ---------------------------------------------------------------------------
+
+def test_iexp_constants_golden(orc):
+    g = {k: int(v) for k, v in _golden("iexp_constants_s2m10.txt")}
+    k = orc.iexp_constants(S, 20)
+    assert (k.q_ln2, k.q_b, k.q_c) == (g["q_ln2"], g["q_b"], g["q_c"])
+    assert orc.iexp(0, k)[0] == g["iexp0_n20"]
+    poly = {k_: float(v) for k_, v in _golden("iexp_polynomial.txt")}
+    assert math.isclose(k.s_L, poly["a"] * S * S, rel_tol=1e-15)
+
+
+def _iexp_table(orc, s, n):
+    k = orc.iexp_constants(s, n)
+    ts = np.arange(n * k.q_ln2 - 3 * abs(k.q_ln2), 1)
+    e = np.array([orc.iexp(int(t), k)[0] for t in ts], dtype=np.float64)
+    return k, ts, e
+
+
+@pytest.mark.parametrize("s", [2.0 ** -10, 1e-3, 2.0 ** -12, 1.2e-4])
+def test_iexp_error_bound(orc, s):
+    """|s_L e / 2^n - exp(s t)| stays within the polynomial's gap.  The paper
+    states 1.9e-3; its own polynomial peaks at 2.13e-3 near p = -0.138, so the
+    bound tested is 2.2e-3 (the floors of q_b, q_c add < 1e-4 at these scales)."""
+    n = 20
+    k, ts, e = _iexp_table(orc, s, n)
+    approx = k.s_L * e / 2.0 ** n
+    err = np.abs(approx - np.exp(s * ts))
+    assert err.max() <= 2.2e-3
+    # the continuous polynomial itself: its max gap on (-ln2, 0] is above the stated value
+    p = np.linspace(-math.log(2), 0, 200001)
+    gap = np.abs(0.3585 * (p + 1.353) ** 2 + 0.344 - np.exp(p)).max()
+    assert 1.9e-3 < gap < 2.2e-3
+
+
+def test_iexp_halves_per_ln2_step(orc):
+    """i-exp = L(p) >> z: moving the input down by |q_ln2| keeps p and adds one to
+    z, so the output halves exactly (until the clamp at n q_ln2)."""
+    n = 20
+    k = orc.iexp_constants(S, n)
+    for t in range(-5 * abs(k.q_ln2), 1, 7):
+        t2 = t + k.q_ln2
+        if t2 < n * k.q_ln2:
+            continue
+        e1, z1, p1 = orc.iexp(t, k)
+        e2, z2, p2 = orc.iexp(t2, k)
+        assert (z2, p2) == (z1 + 1, p1)
+        assert e1 == 2 * e2
+
+
+def test_iexp_decomposition_and_monotone(orc):
+    """t = z q_ln2 + q_p with z >= 0 and q_p in (q_ln2, 0]; outputs are
+    non-decreasing in t; below n q_ln2 the input is clamped."""
+    n = 20
+    k, ts, e = _iexp_table(orc, S, n)
+    for t in ts[:: 13]:
+        out, z, qp = orc.iexp(int(t), k)
+        tc = max(int(t), n * k.q_ln2)
+        assert z >= 0 and k.q_ln2 < qp <= 0
+        assert tc == z * k.q_ln2 + qp
+        assert out == ((qp + k.q_b) ** 2 + k.q_c) * 2 ** (n - z)
+    assert np.all(np.diff(e) >= 0)
+    assert orc.iexp(n * k.q_ln2 - 12345, k)[0] == orc.iexp(n * k.q_ln2, k)[0]
+
+
+# ---------------------------------------------------------------------------
+# Log-Int-Softmax (Algorithm 2 + the clip of the LIS equation)
+# ---------------------------------------------------------------------------
+
+def test_lis_flat_rows_golden(orc):
+    for Lk, code in _golden("lis_flat_rows.txt"):
+        Lk, code = int(Lk), int(code)
+        for val in (0, 12345, -777777):
+            row = np.full((1, 3, Lk), val, dtype=np.int32)
+            c = orc.unpack_codes(orc.lis_softmax_log4(row, S), Lk)
+            assert np.all(c == code), (Lk, val)
+
+
+def test_lis_dominant_max(orc):
+    """A max far above the rest: the max gets Attn_Q = 0, every clamped entry 15."""
+    rng = np.random.default_rng(5)
+    for Lk in (2, 9, 49, 197, 577):
+        row = rng.integers(-100000, -50000, size=(1, 4, Lk)).astype(np.int32)
+        j = rng.integers(0, Lk, size=4)
+        row[0, np.arange(4), j] = 10 ** 6
+        c = orc.unpack_codes(orc.lis_softmax_log4(row, S), Lk)[0]
+        assert np.all(c[np.arange(4), j] == 0)
+        mask = np.ones_like(c, dtype=bool)
+        mask[np.arange(4), j] = False
+        assert np.all(c[mask] == 15)
+
+
+def _codes_and_e(orc, logits, s=S, n=20, bias=None):
+    G, Lq, Lk = logits.shape
+    codes = orc.unpack_codes(orc.lis_softmax_log4(logits, s, exp_n=n, bias=bias), Lk)
+    return codes
+
+
+def test_lis_reciprocal_and_log2_steps_exact(orc):
+    """From the oracle's i-exp values, recompute q_rev = round(sum/e) (ties up)
+    as an exact Fraction and Attn_Q with the closed form of I-Log2."""
+    a = W.attn_inputs(3, 16, 37, 8, seed=11, heads=3, sigma=(1.0, 3.0, 6.0))
+    codes = _codes_and_e(orc, a["logits"])
+    for g in range(3):
+        for i in range(16):
+            e, _ = orc.lis_row_exp(a["logits"][g, i], S)
+            tot = int(e.astype(object).sum())
+            for j in range(37):
+                frac = Fraction(tot, int(e[j]))
+                q_rev = math.floor(frac + Fraction(1, 2))
+                assert codes[g, i, j] == min(ilog2_closed_form(q_rev), 15)
+
+
+def test_lis_range_monotone_argmax(orc):
+    """Codes lie in [0, 15], never increase with the logit, and the row maximum
+    gets the row's smallest code."""
+    for cfg in W.CONFIGS:
+        a = W.attn_inputs(4, min(cfg.Lq, 64), cfg.Lk, 8, seed=cfg.seed, heads=cfg.heads,
+                          sigma=cfg.sigma, bias=cfg.bias)
+        lg = a["logits"].astype(np.int64)
+        if a["bias"] is not None:
+            lg = lg + a["bias"][np.arange(4) % a["Hb"]][:, : lg.shape[1]]
+            a["bias"] = np.ascontiguousarray(a["bias"][:, : lg.shape[1]])
+        c = _codes_and_e(orc, a["logits"], bias=a["bias"])
+        assert c.min() >= 0 and c.max() <= 15
+        order = np.argsort(lg, axis=-1, kind="stable")
+        cs = np.take_along_axis(c, order, axis=-1)
+        assert np.all(np.diff(cs.astype(np.int64), axis=-1) <= 0)
+        am = lg.argmax(-1)
+        assert np.all(np.take_along_axis(c, am[..., None], -1)[..., 0] == c.min(-1))
+
+
+def test_lis_shift_and_bias_invariance(orc):
+    """Subtracting the row max makes LIS invariant to a per-row constant, and the
+    bias is part of the logit (adding it in the input is the same)."""
+    a = W.attn_inputs(6, 20, 49, 8, seed=3, heads=3, bias=True)
+    base = _codes_and_e(orc, a["logits"], bias=a["bias"])
+    shifted = (a["logits"].astype(np.int64) + np.arange(20)[None, :, None] * 12345 - 4242)
+    c2 = _codes_and_e(orc, shifted.astype(np.int32), bias=a["bias"])
+    assert np.array_equal(base, c2)
+    folded = a["logits"] + a["bias"][np.arange(6) % 3]
+    c3 = _codes_and_e(orc, folded.astype(np.int32))
+    assert np.array_equal(base, c3)
+
+
+def test_lis_row_sum_bound(orc):
+    """0.625 (1 - (Lk-1)/49151.5) <= sum_j 2^-Attn_Q < 1.5 + (Lk-1)/32768: each
+    unclipped entry lies within [0.625, 1.5) of its i-exp probability and each
+    clipped entry is 2^-15."""
+    for cfg in W.CONFIGS:
+        a = W.attn_inputs(4, min(cfg.Lq, 96), cfg.Lk, 8, seed=cfg.seed, heads=cfg.heads,
+                          sigma=cfg.sigma)
+        c = _codes_and_e(orc, a["logits"])
+        rs = (2.0 ** -c.astype(np.float64)).sum(-1)
+        Lk = cfg.Lk
+        assert rs.min() >= 0.625 * (1 - (Lk - 1) / 49151.5)
+        assert rs.max() < 1.5 + (Lk - 1) / 32768
+
+
+def test_lis_against_float_softmax(orc):
+    """Secondary checks: the i-exp probabilities e/sum are within L1 0.05 of the
+    float softmax per row, and Attn_Q is within 1 of the float log2 quantizer
+    clip(round(-log2 softmax), 0, 15) of Sec. 3.3."""
+    worst_l1, worst_code = 0.0, 0
+    for cfg in W.CONFIGS:
+        a = W.attn_inputs(2, min(cfg.Lq, 48), cfg.Lk, 8, seed=cfg.seed, heads=cfg.heads,
+                          sigma=cfg.sigma)
+        c = _codes_and_e(orc, a["logits"])
+        for g in range(2):
+            for i in range(a["logits"].shape[1]):
+                row = a["logits"][g, i].astype(np.float64) * S
+                sm = np.exp(row - row.max())
+                sm /= sm.sum()
+                e, tot = orc.lis_row_exp(a["logits"][g, i], S)
+                l1 = np.abs(e / e.sum() - sm).sum()
+                worst_l1 = max(worst_l1, l1)
+                fq = np.clip(np.rint(-np.log2(np.maximum(sm, 1e-300))), 0, 15)
+                worst_code = max(worst_code, int(np.abs(fq - c[g, i]).max()))
+    assert worst_l1 <= 0.05
+    assert worst_code <= 1
+
+
+def test_lis_lower_bits_clip(orc):
+    """With b-bit codes the clip is at 2^b - 1 and agrees with the 4-bit codes below it."""
+    a = W.attn_inputs(2, 10, 49, 8, seed=9)
+    c4 = _codes_and_e(orc, a["logits"])
+    for bits in (1, 2, 3):
+        cb = orc.unpack_codes(orc.lis_softmax_log4(a["logits"], S, bits=bits), 49)
+        assert np.array_equal(cb, np.minimum(c4, 2 ** bits - 1))
+
+
+def test_lis_packing_layout(orc):
+    """Two codes per byte, even key in the low nibble; bytes past ceil(Lk/2) in a
+    wider row stride are left alone; an odd tail's high nibble is zero."""
+    a = W.attn_inputs(2, 5, 9, 8, seed=1)
+    dense = orc.lis_softmax_log4(a["logits"], S)
+    wide = orc.lis_softmax_log4(a["logits"], S, ld_codes=8)
+    assert np.array_equal(wide[..., :5], dense)
+    assert np.all(wide[..., 5:] == 0)
+    assert np.all((dense[..., -1] >> 4) == 0)
+    c = orc.unpack_codes(dense, 9)
+    assert np.array_equal(dense[..., 0], c[..., 0] | (c[..., 1] << 4))
+
+
+# ---------------------------------------------------------------------------
+# BitShift Attn x V (Sec. 3.3, Supplement A.2)
+# ---------------------------------------------------------------------------
+
+def test_attn_v_equals_power_of_two_matmul(orc):
+    """Shift-accumulate equals the integer matrix product P (V - zp_V) with
+    P_ij = 2^(N - Attn_Q_ij), computed by numpy's int64 matmul."""
+    rng = np.random.default_rng(4)
+    for (G, Lq, Lk, d, bits, zp) in [(3, 7, 9, 5, 4, 0), (2, 17, 33, 16, 4, -3),
+                                     (1, 5, 1, 3, 4, 7), (2, 6, 11, 4, 2, 1)]:
+        v = rng.integers(-128, 128, size=(G, Lk, d)).astype(np.int8)
+        codes = rng.integers(0, 2 ** bits, size=(G, Lq, Lk))
+        # keep the sums inside int32
+        codes[:, :, :] = np.maximum(codes, 0)
+        ld = (Lk + 1) // 2
+        packed = np.zeros((G, Lq, ld), dtype=np.uint8)
+        for j in range(Lk):
+            packed[..., j // 2] |= (codes[..., j] << (4 * (j % 2))).astype(np.uint8)
+        out = orc.lis_attn_v_shift(packed, v, zp_v=zp, bits=bits, Lk=Lk)
+        N = 2 ** bits - 1
+        P = (2 ** (N - codes)).astype(np.int64)
+        ref = np.matmul(P, v.astype(np.int64) - zp)
+        assert np.array_equal(out.astype(np.int64), ref)
+
+
+def test_attn_v_single_element_exhaustive(orc):
+    """Every (code, V, zp_V) for one key: out = (V - zp_V) * 2^(15 - code)."""
+    vals = np.arange(-128, 128, dtype=np.int64)
+    for zp in (-128, -1, 0, 5, 127):
+        for code in range(16):
+            v = vals.astype(np.int8).reshape(1, 1, 256)
+            packed = np.full((1, 1, 1), code, dtype=np.uint8)
+            out = orc.lis_attn_v_shift(packed, v, zp_v=zp, bits=4, Lk=1)
+            assert np.array_equal(out[0, 0].astype(np.int64), (vals - zp) << (15 - code))
+
+
+def test_head_is_lis_then_attn_v(orc):
+    a = W.attn_inputs(5, 13, 49, 32, seed=7, heads=3, bias=True)
+    out, codes = orc.lis_attention_head(a["logits"], a["v"], S, bias=a["bias"], want_codes=True)
+    c2 = orc.lis_softmax_log4(a["logits"], S, bias=a["bias"])
+    assert np.array_equal(codes, c2)
+    assert np.array_equal(out, orc.lis_attn_v_shift(c2, a["v"], Lk=49))
+
+
+# ---------------------------------------------------------------------------
+# PTF quantizer (Sec. 3.2)
+# ---------------------------------------------------------------------------
+
+def test_ptf_K0_is_minmax(orc):
+    """K = 0 makes eq. (9)-(10) the MinMax parameters of eq. (5), and eq. (8) with
+    alpha = 0 the uniform quantizer of eq. (3), bit for bit."""
+    X = W.ln_inputs(64, 48, seed=0)["x_float"]
+    s_p, zp_p = orc.ptf_params(X, b=8, K=0)
+    s_m, zp_m = orc.minmax_params(X, b=8)
+    assert (s_p, zp_p) == (s_m, zp_m)
+    q_p = orc.ptf_quantize(X, s_p, zp_p, np.zeros(48, np.uint8))
+    q_m = orc.minmax_quantize(X, s_m, zp_m)
+    assert np.array_equal(q_p, q_m)
+
+
+def test_ptf_alpha_K_is_minmax(orc):
+    """alpha = K on every channel puts every channel on the MinMax grid 2^K s."""
+    X = W.ln_inputs(64, 48, seed=1)["x_float"]
+    s_p, zp_p = orc.ptf_params(X, b=8, K=3)
+    s_m, zp_m = orc.minmax_params(X, b=8)
+    assert zp_p == zp_m and s_p * 8 == s_m
+    q_p = orc.ptf_quantize(X, s_p, zp_p, np.full(48, 3, np.uint8))
+    assert np.array_equal(q_p, orc.minmax_quantize(X, s_m, zp_m))
+
+
+def test_ptf_alpha_search_outliers(orc):
+    """The argmin of eq. (11) gives the widest channels the largest factor and
+    narrow channels the finest grid; a narrower grid never loses on a channel
+    that it holds without clipping."""
+    ln = W.ln_inputs(197, 96, seed=2, outliers=4)
+    X = ln["x_float"]
+    s, zp = orc.ptf_params(X, b=8, K=3)
+    alpha = orc.ptf_alpha(X, s, zp, b=8, K=3)
+    rng_c = X.max(0) - X.min(0)
+    widest = np.argsort(rng_c)[-4:]
+    assert np.all(alpha[widest] == 3)
+    narrow = rng_c < 0.5 * np.median(rng_c)
+    assert np.all(alpha[narrow] == 0)
+    assert np.all(np.diff(alpha[np.argsort(rng_c)].astype(int)) >= -1)
+
+
+# ---------------------------------------------------------------------------
+# Integer LayerNorm with PTF (Supplement A.1)
+# ---------------------------------------------------------------------------
+
+def float_ln_requant(x_q, zp_in, alpha, s_in, gamma, beta, s_out, zp_out, bits=8, eps=1e-6):
+    """fp64 LayerNorm (Sec. 3.2, eq. 7) of the dequantized PTF input, quantized
+    with (s_out, zp_out) onto the int8 container."""
+    half = 2 ** (bits - 1)
+    X = (x_q.astype(np.float64) - zp_in) * (2.0 ** alpha.astype(np.float64)) * s_in
+    mu = X.mean(-1, keepdims=True)
+    var = X.var(-1, keepdims=True)
+    Y = (X - mu) / np.sqrt(var + eps) * gamma.astype(np.float64) + beta.astype(np.float64)
+    return np.clip(np.rint(Y / float(np.float32(s_out))) + zp_out + half, 0, 2 ** bits - 1) - half
+
+
+def _ln(orc, d, x_q=None, alpha=None, gamma=None, beta=None, zp_in=None):
+    return orc.ptf_layernorm_int8(d["x_q"] if x_q is None else x_q,
+                                  d["zp_in"] if zp_in is None else zp_in,
+                                  d["alpha"] if alpha is None else alpha, d["K"],
+                                  d["gamma"] if gamma is None else gamma,
+                                  d["beta"] if beta is None else beta,
+                                  d["s_out"], d["zp_out"], d["bits"])
+
+
+@pytest.mark.parametrize("cfg", W.CONFIGS, ids=lambda c: c.name)
+def test_ln_within_2lsb_of_float(orc, cfg):
+    d = W.ln_inputs(min(cfg.T, 1024), cfg.channels, cfg.seed, outliers=cfg.outliers,
+                    alpha_uniform=cfg.alpha_uniform)
+    y = _ln(orc, d)
+    ref = float_ln_requant(d["x_q"], d["zp_in"], d["alpha"], d["s_in"], d["gamma"],
+                           d["beta"], d["s_out"], d["zp_out"])
+    diff = np.abs(y.astype(np.int64) - ref)
+    assert diff.max() <= 2
+    assert diff.mean() < 0.05
+
+
+def test_ln_constant_row_and_zero_gamma(orc):
+    """A row whose shifted values X^_Q are all equal has zero variance: its output
+    is round(beta/s_out) + zp_out.  A channel with gamma = 0 gives the same value
+    on every row."""
+    d = W.ln_inputs(16, 64, seed=3)
+    x = d["x_q"].copy()
+    x[3, :] = (d["zp_in"] + (8 >> np.minimum(d["alpha"], 3))).astype(np.int8)
+    x[9, :] = d["zp_in"]
+    gamma = d["gamma"].copy()
+    gamma[[0, 5, 63]] = 0.0
+    y = _ln(orc, d, x_q=x, gamma=gamma)
+    expect = np.clip(np.rint(d["beta"].astype(np.float64) / np.float64(np.float32(d["s_out"])))
+                     + d["zp_out"], -128, 127)
+    assert np.array_equal(y[3], expect.astype(np.int8))
+    assert np.array_equal(y[9], expect.astype(np.int8))
+    for c in (0, 5, 63):
+        assert np.all(y[:, c] == expect[c])
+
+
+def test_ln_uniform_alpha_is_scale_free(orc):
+    """The same alpha = k on every channel scales X^_Q, sqrt(C M2 - M1^2) and hence
+    A by exact powers of two: N2 and A X^_Q are unchanged and N1 grows by k.  Only
+    round(B 2^N1) moves to a 2^k finer grid, so the output stays within 1 LSB of
+    the alpha = 0 output and is almost always identical."""
+    d = W.ln_inputs(256, 96, seed=4)
+    y0 = _ln(orc, d, alpha=np.zeros(96, np.uint8)).astype(np.int64)
+    for k in (1, 2, 3):
+        yk = _ln(orc, d, alpha=np.full(96, k, np.uint8)).astype(np.int64)
+        assert np.abs(yk - y0).max() <= 1
+        assert np.mean(yk != y0) < 0.01
+
+
+def test_ln_zero_point_shift(orc):
+    """Only X_Q - zp enters: shifting the input and its zero point together changes nothing."""
+    d = W.ln_inputs(32, 64, seed=5)
+    x = d["x_q"].astype(np.int64)
+    x = np.clip(x, -100, 100)
+    y0 = _ln(orc, d, x_q=x.astype(np.int8))
+    y1 = _ln(orc, d, x_q=(x + 20).astype(np.int8), zp_in=d["zp_in"] + 20)
+    assert np.array_equal(y0, y1)
+
+
+def test_ln_alpha_clamped_to_K(orc):
+    d = W.ln_inputs(16, 32, seed=6)
+    a = d["alpha"].copy()
+    a[::3] = 7
+    a2 = np.minimum(a, d["K"])
+    assert np.array_equal(_ln(orc, d, alpha=a), _ln(orc, d, alpha=a2))
+
+
+def test_ln_exhaustive_alpha_4x8(orc):
+    """All 4^8 alpha vectors on 4 tokens x 8 channels: within 2 LSB of the float
+    LayerNorm of the dequantized input."""
+    rng = np.random.default_rng(8)
+    x_q = rng.integers(-128, 128, size=(4, 8)).astype(np.int8)
+    gamma = (1 + 0.5 * rng.standard_normal(8)).astype(np.float32)
+    beta = (0.5 * rng.standard_normal(8)).astype(np.float32)
+    s_out, zp_out, zp_in = 0.03, -3, 2
+    alphas = np.array(np.meshgrid(*[np.arange(4)] * 8, indexing="ij")).reshape(8, -1).T
+    worst = 0
+    for a in alphas.astype(np.uint8):
+        y = orc.ptf_layernorm_int8(x_q, zp_in, a, 3, gamma, beta, s_out, zp_out, 8)
+        ref = float_ln_requant(x_q, zp_in, a, 1.0, gamma, beta, s_out, zp_out, eps=0.0)
+        worst = max(worst, int(np.abs(y.astype(np.int64) - ref).max()))
+    assert worst <= 2
+
+
+def test_ln_worked_examples_golden(orc):
+    """Two one-row examples worked by hand from the Supplement A.1 formulas: the
+    b-bit dyadic form of A (N1, N2), round(B 2^N1) and the half-up outer rounding."""
+    x_q = np.array([[-126, 126]], dtype=np.int8)
+    alpha = np.array([3, 3], dtype=np.uint8)
+    gamma = np.array([1.57421875, 1.57421875], dtype=np.float32)
+    for beta, y0, y1 in _golden("ln_worked_examples.txt"):
+        b = np.array([float(beta)] * 2, dtype=np.float32)
+        y = orc.ptf_layernorm_int8(x_q, 0, alpha, 3, gamma, b, 0.015625, 0, 8)
+        assert y.tolist() == [[int(y0), int(y1)]]
