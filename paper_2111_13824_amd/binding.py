@@ -1,0 +1,188 @@
+"""ctypes binding of libfqvit (include/fqvit.h).
+
+Argument marshalling only: each function checks dtypes, devices, shapes and
+contiguity of torch tensors, passes their device pointers and the current HIP
+stream to the C ABI entry point of the same name, and raises ``FqError`` on a
+non-zero status.  Every step of the computation runs in the HIP kernels; there
+is no fallback.  If libfqvit.so is not built the first call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libfqvit.so")
+
+FQ_OK, FQ_ERR_NULL, FQ_ERR_SHAPE, FQ_ERR_PARAM, FQ_ERR_HEADROOM, FQ_ERR_HIP = range(6)
+
+# Entry points declared in include/fqvit.h and their C argument types.
+_P = ctypes.c_void_p
+_I32, _I64, _F32 = ctypes.c_int32, ctypes.c_int64, ctypes.c_float
+SIGNATURES = {
+    "ptf_layernorm_int8": [_P, _I64, _I32, _I32, _P, _I32, _P, _P, _F32, _I32, _I32, _P, _P],
+    "lis_softmax_log4": [_P, _I64, _I32, _I32, _P, _I32, _F32, _I32, _I32, _P, _I32, _P],
+    "lis_attn_v_shift": [_P, _I32, _P, _I32, _I64, _I32, _I32, _I32, _I32, _P, _P],
+    "lis_attention_head": [_P, _P, _I32, _I64, _I32, _I32, _F32, _I32, _I32, _P, _I32, _I32, _P,
+                           _P, _I32, _P],
+}
+
+
+class FqError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        self.status = status
+        super().__init__(f"{fn}: {status_str(status)}")
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded C library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -c "
+                               f"'import __graft_entry__ as g; g.build()'` (no fallback exists)")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, args in SIGNATURES.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = ctypes.c_int32
+        L.fq_status_str.argtypes = [ctypes.c_int]
+        L.fq_status_str.restype = ctypes.c_char_p
+        L.fq_version.argtypes = []
+        L.fq_version.restype = ctypes.c_int32
+        _lib = L
+    return _lib
+
+
+def status_str(status: int) -> str:
+    return lib().fq_status_str(int(status)).decode()
+
+
+def version() -> int:
+    return lib().fq_version()
+
+
+def _stream(stream=None) -> int:
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def _dev_ptr(t, dtype, name: str, ndim: Optional[int] = None):
+    import torch
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dimensions, got {t.dim()}")
+    return t.data_ptr()
+
+
+def _check(fn: str, status: int) -> None:
+    if status != FQ_OK:
+        raise FqError(fn, status)
+
+
+def ptf_layernorm_int8(x_q, zp_in: int, alpha, K: int, gamma, beta, s_out: float, zp_out: int,
+                       bits: int = 8, y_q=None, stream=None):
+    """PTF LayerNorm of an int8 [T, C] tensor; returns (or fills) int8 [T, C]."""
+    import torch
+    T, C = x_q.shape
+    if y_q is None:
+        y_q = torch.empty_like(x_q)
+    if alpha.shape != (C,) or gamma.shape != (C,) or beta.shape != (C,) or y_q.shape != (T, C):
+        raise ValueError("alpha, gamma, beta must be [C] and y_q [T, C]")
+    st = lib().ptf_layernorm_int8(_dev_ptr(x_q, torch.int8, "x_q", 2), T, C, zp_in,
+                                  _dev_ptr(alpha, torch.uint8, "alpha", 1), K,
+                                  _dev_ptr(gamma, torch.float32, "gamma", 1),
+                                  _dev_ptr(beta, torch.float32, "beta", 1), s_out, zp_out, bits,
+                                  _dev_ptr(y_q, torch.int8, "y_q", 2), _stream(stream))
+    _check("ptf_layernorm_int8", st)
+    return y_q
+
+
+def codes_ld(Lk: int) -> int:
+    return (Lk + 1) // 2
+
+
+def lis_softmax_log4(logits, s_logit: float, bits: int = 4, exp_n: int = 20, bias=None,
+                     codes=None, stream=None):
+    """Packed 4-bit Log-Int-Softmax codes [G, Lq, ld] of int32 logits [G, Lq, Lk]."""
+    import torch
+    G, Lq, Lk = logits.shape
+    if codes is None:
+        codes = torch.zeros((G, Lq, codes_ld(Lk)), dtype=torch.uint8, device=logits.device)
+    if codes.dim() != 3 or codes.shape[:2] != (G, Lq):
+        raise ValueError("codes must be [G, Lq, ld_codes]")
+    Hb = 0
+    if bias is not None:
+        if bias.dim() != 3 or bias.shape[1:] != (Lq, Lk):
+            raise ValueError("bias must be [Hb, Lq, Lk]")
+        Hb = bias.shape[0]
+    st = lib().lis_softmax_log4(_dev_ptr(logits, torch.int32, "logits", 3), G, Lq, Lk,
+                                _dev_ptr(bias, torch.int32, "bias", 3), Hb, s_logit, bits, exp_n,
+                                _dev_ptr(codes, torch.uint8, "codes", 3), codes.shape[2],
+                                _stream(stream))
+    _check("lis_softmax_log4", st)
+    return codes
+
+
+def lis_attn_v_shift(codes, v, Lk: int, zp_v: int = 0, bits: int = 4, out=None, stream=None):
+    """BitShift Attn x V: int32 [G, Lq, d] from packed codes [G, Lq, ld] and int8 V [G, Lk, d]."""
+    import torch
+    G, Lq, ld = codes.shape
+    d = v.shape[2]
+    if v.dim() != 3 or v.shape[:2] != (G, Lk):
+        raise ValueError("v must be [G, Lk, d]")
+    if out is None:
+        out = torch.empty((G, Lq, d), dtype=torch.int32, device=v.device)
+    if out.shape != (G, Lq, d):
+        raise ValueError("out must be [G, Lq, d]")
+    st = lib().lis_attn_v_shift(_dev_ptr(codes, torch.uint8, "codes", 3), ld,
+                                _dev_ptr(v, torch.int8, "v", 3), zp_v, G, Lq, Lk, d, bits,
+                                _dev_ptr(out, torch.int32, "out", 3), _stream(stream))
+    _check("lis_attn_v_shift", st)
+    return out
+
+
+def lis_attention_head(logits, v, s_logit: float, bits: int = 4, exp_n: int = 20, zp_v: int = 0,
+                       bias=None, out=None, codes_out=None, stream=None):
+    """Fused Log-Int-Softmax + BitShift Attn x V; returns int32 [G, Lq, d]."""
+    import torch
+    G, Lq, Lk = logits.shape
+    d = v.shape[2]
+    if v.dim() != 3 or v.shape[:2] != (G, Lk):
+        raise ValueError("v must be [G, Lk, d]")
+    if out is None:
+        out = torch.empty((G, Lq, d), dtype=torch.int32, device=logits.device)
+    if out.shape != (G, Lq, d):
+        raise ValueError("out must be [G, Lq, d]")
+    Hb = 0
+    if bias is not None:
+        if bias.dim() != 3 or bias.shape[1:] != (Lq, Lk):
+            raise ValueError("bias must be [Hb, Lq, Lk]")
+        Hb = bias.shape[0]
+    ld = 0
+    if codes_out is not None:
+        if codes_out.dim() != 3 or codes_out.shape[:2] != (G, Lq):
+            raise ValueError("codes_out must be [G, Lq, ld_codes]")
+        ld = codes_out.shape[2]
+    st = lib().lis_attention_head(_dev_ptr(logits, torch.int32, "logits", 3),
+                                  _dev_ptr(bias, torch.int32, "bias", 3), Hb, G, Lq, Lk, s_logit,
+                                  bits, exp_n, _dev_ptr(v, torch.int8, "v", 3), zp_v, d,
+                                  _dev_ptr(out, torch.int32, "out", 3),
+                                  _dev_ptr(codes_out, torch.uint8, "codes_out", 3), ld,
+                                  _stream(stream))
+    _check("lis_attention_head", st)
+    return out

@@ -1,0 +1,158 @@
+// C ABI of libfqvit (declared in include/fqvit.h): argument validation, the
+// host-side integer constants of I-Exp, and the kernel launches.  Nothing here
+// allocates, synchronises or keeps state between calls.
+#include "fqvit.h"
+
+#include <cmath>
+#include <cstdint>
+
+#include "fqvit_internal.h"
+
+namespace {
+
+constexpr int32_t kMaxC = 8192;
+constexpr int32_t kMaxLk = 4096;
+constexpr int32_t kMaxD = 256;
+
+fq_status from_hip(hipError_t e) { return e == hipSuccess ? FQ_OK : FQ_ERR_HIP; }
+
+// Integer constants of Algorithm 1 (Supplement A.2) for input scale s, plus the
+// bounds that let the kernels use 32-bit and 24-bit arithmetic.
+fq_status lis_constants(float s_logit, int32_t bits, int32_t n, int32_t Lk,
+                        fqvit::LisConsts* k) {
+    if (!(s_logit >= 1e-4f && s_logit <= 0.5f)) return FQ_ERR_PARAM;
+    if (bits < 1 || bits > 4 || n < 1 || n > 30) return FQ_ERR_PARAM;
+    const double s = (double)s_logit;
+    const double q_ln2 = std::floor(-0.69314718055994530942 / s);   // floor(-ln2 / s)
+    const double q_b = std::floor(1.353 / s);                       // floor(b / s)
+    const double q_c = std::floor(0.344 / ((0.3585 * s) * s));      // floor(c / (a s^2))
+    const uint64_t d = (uint64_t)(-q_ln2);
+    const uint64_t qb = (uint64_t)q_b;
+    const uint64_t qc = (uint64_t)q_c;
+    // q_p + q_b lies in [q_b - d + 1, q_b]: positive and below 2^16; 3 q_L < 2^32.
+    if (d < 1 || qb < d || qb >= 65536 || 3 * (qb * qb + qc) >= (1ull << 32)) return FQ_ERR_PARAM;
+    int pre = 0;
+    while ((d << pre) <= 256) ++pre;
+    const uint64_t dp = d << pre;
+    if ((uint64_t)n * dp * dp >= (1ull << 32) || (uint64_t)n * dp >= (1ull << 24)) return FQ_ERR_PARAM;
+    // The row sum (and 2 sum + e) must stay below 2^63.
+    const unsigned __int128 emax = (unsigned __int128)(qb * qb + qc) << n;
+    if ((unsigned __int128)(2 * (uint64_t)Lk + 1) * emax >= ((unsigned __int128)1 << 63))
+        return FQ_ERR_HEADROOM;
+    k->d_ln2 = (uint32_t)d;
+    k->qb = (uint32_t)qb;
+    k->qc = (uint32_t)qc;
+    k->u_max = (uint32_t)(n * d);
+    k->magic = (uint32_t)((1ull << 32) / dp + 1);
+    k->pre = pre;
+    k->n = n;
+    k->top = (1 << bits) - 1;
+    return FQ_OK;
+}
+
+bool grid_fits(int64_t G, int32_t Lq, int32_t rows_per_block) {
+    const int64_t tiles = (Lq + rows_per_block - 1) / rows_per_block;
+    return G <= (int64_t)0x7FFFFFFF / (tiles > 0 ? tiles : 1);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* fq_status_str(int status) {
+    switch (status) {
+        case FQ_OK: return "FQ_OK";
+        case FQ_ERR_NULL: return "FQ_ERR_NULL: a required pointer is NULL";
+        case FQ_ERR_SHAPE: return "FQ_ERR_SHAPE: a size is out of the supported range";
+        case FQ_ERR_PARAM: return "FQ_ERR_PARAM: a scalar parameter is out of range";
+        case FQ_ERR_HEADROOM: return "FQ_ERR_HEADROOM: the i-exp row sum could overflow 64 bits";
+        case FQ_ERR_HIP: return "FQ_ERR_HIP: the HIP runtime rejected a launch";
+        default: return "unknown fq_status";
+    }
+}
+
+int32_t fq_version(void) { return 100; }
+
+fq_status ptf_layernorm_int8(const int8_t* x_q, int64_t T, int32_t C, int32_t zp_in,
+                             const uint8_t* alpha, int32_t K, const float* gamma,
+                             const float* beta, float s_out, int32_t zp_out, int32_t bits,
+                             int8_t* y_q, void* stream) {
+    if (T < 0 || C < 1 || C > kMaxC) return FQ_ERR_SHAPE;
+    if (bits < 2 || bits > 8 || K < 0 || K > 7) return FQ_ERR_PARAM;
+    if (!(s_out > 0.0f) || !std::isfinite(s_out)) return FQ_ERR_PARAM;
+    const int32_t half = 1 << (bits - 1);
+    if (zp_in < -half || zp_in >= half || zp_out < -half || zp_out >= half) return FQ_ERR_PARAM;
+    if (T == 0) return FQ_OK;
+    if (!x_q || !alpha || !gamma || !beta || !y_q) return FQ_ERR_NULL;
+    fqvit::LnArgs a{x_q, y_q, alpha, gamma, beta, T, C, zp_in, K, s_out, zp_out, bits};
+    return from_hip(fqvit::launch_ptf_layernorm(a, (hipStream_t)stream));
+}
+
+fq_status lis_softmax_log4(const int32_t* logits, int64_t G, int32_t Lq, int32_t Lk,
+                           const int32_t* bias, int32_t Hb, float s_logit, int32_t bits,
+                           int32_t exp_n, uint8_t* codes, int32_t ld_codes, void* stream) {
+    if (G < 0 || Lq < 0 || Lk < 1 || Lk > kMaxLk || ld_codes < (Lk + 1) / 2 || (bias && Hb < 1) ||
+        !grid_fits(G, Lq, 64))
+        return FQ_ERR_SHAPE;
+    fqvit::LisConsts k;
+    const fq_status st = lis_constants(s_logit, bits, exp_n, Lk, &k);
+    if (st != FQ_OK) return st;
+    if (G == 0 || Lq == 0) return FQ_OK;
+    if (!logits || !codes) return FQ_ERR_NULL;
+    fqvit::LisArgs a{};
+    a.logits = logits;
+    a.bias = bias;
+    a.Hb = bias ? Hb : 1;
+    a.G = G;
+    a.Lq = Lq;
+    a.Lk = Lk;
+    a.k = k;
+    a.codes = codes;
+    a.ld_codes = ld_codes;
+    return from_hip(fqvit::launch_lis(a, (hipStream_t)stream));
+}
+
+fq_status lis_attn_v_shift(const uint8_t* codes, int32_t ld_codes, const int8_t* v,
+                           int32_t zp_v, int64_t G, int32_t Lq, int32_t Lk, int32_t d,
+                           int32_t bits, int32_t* out, void* stream) {
+    if (G < 0 || Lq < 0 || Lk < 1 || Lk > kMaxLk || d < 1 || d > kMaxD ||
+        ld_codes < (Lk + 1) / 2 || !grid_fits(G, Lq, 16))
+        return FQ_ERR_SHAPE;
+    if (bits < 1 || bits > 4 || zp_v < -128 || zp_v > 127) return FQ_ERR_PARAM;
+    if (G == 0 || Lq == 0) return FQ_OK;
+    if (!codes || !v || !out) return FQ_ERR_NULL;
+    fqvit::AvArgs a{codes, ld_codes, v, zp_v, G, Lq, Lk, d, (1 << bits) - 1, out};
+    return from_hip(fqvit::launch_attn_v_shift(a, (hipStream_t)stream));
+}
+
+fq_status lis_attention_head(const int32_t* logits, const int32_t* bias, int32_t Hb,
+                             int64_t G, int32_t Lq, int32_t Lk, float s_logit, int32_t bits,
+                             int32_t exp_n, const int8_t* v, int32_t zp_v, int32_t d,
+                             int32_t* out, uint8_t* codes_out, int32_t ld_codes, void* stream) {
+    if (G < 0 || Lq < 0 || Lk < 1 || Lk > kMaxLk || d < 1 || d > kMaxD || (bias && Hb < 1) ||
+        (codes_out && ld_codes < (Lk + 1) / 2) || !grid_fits(G, Lq, 64))
+        return FQ_ERR_SHAPE;
+    if (zp_v < -128 || zp_v > 127) return FQ_ERR_PARAM;
+    fqvit::LisConsts k;
+    const fq_status st = lis_constants(s_logit, bits, exp_n, Lk, &k);
+    if (st != FQ_OK) return st;
+    if (G == 0 || Lq == 0) return FQ_OK;
+    if (!logits || !v || !out) return FQ_ERR_NULL;
+    fqvit::LisArgs a{};
+    a.logits = logits;
+    a.bias = bias;
+    a.Hb = bias ? Hb : 1;
+    a.G = G;
+    a.Lq = Lq;
+    a.Lk = Lk;
+    a.k = k;
+    a.v = v;
+    a.zp_v = zp_v;
+    a.d = d;
+    a.out = out;
+    a.codes = codes_out;
+    a.ld_codes = codes_out ? ld_codes : 0;
+    return from_hip(fqvit::launch_lis(a, (hipStream_t)stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,78 @@
+// Internal declarations shared by the gfx950 kernels and the C ABI wrappers of
+// libfqvit.  Not part of the public interface (include/fqvit.h is).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fqvit {
+
+// ---------------------------------------------------------------------------
+// PTF LayerNorm
+// ---------------------------------------------------------------------------
+
+struct LnArgs {
+    const int8_t* x;
+    int8_t* y;
+    const uint8_t* alpha;
+    const float* gamma;
+    const float* beta;
+    int64_t T;
+    int32_t C;
+    int32_t zp_in;     // container form
+    int32_t K;
+    float s_out;
+    int32_t zp_out;    // container form
+    int32_t bits;
+};
+
+hipError_t launch_ptf_layernorm(const LnArgs& a, hipStream_t stream);
+
+// ---------------------------------------------------------------------------
+// Log-Int-Softmax / BitShift attention
+// ---------------------------------------------------------------------------
+
+// Integer constants of the I-Exp / code pipeline, derived on the host.
+struct LisConsts {
+    uint32_t d_ln2;     // -q_ln2 = -floor(-ln2 / s) > 0
+    uint32_t qb;        // floor(1.353 / s)
+    uint32_t qc;        // floor(0.344 / ((0.3585 s) s))
+    uint32_t u_max;     // n * d_ln2: inputs below -u_max are clamped
+    uint32_t magic;     // floor(2^32 / (d_ln2 << pre)) + 1
+    int32_t pre;        // pre-shift making (d_ln2 << pre) > 256
+    int32_t n;          // clamp depth
+    int32_t top;        // 2^bits - 1
+};
+
+struct LisArgs {
+    const int32_t* logits;  // [G, Lq, Lk]
+    const int32_t* bias;    // nullable [Hb, Lq, Lk]
+    int32_t Hb;
+    int64_t G;
+    int32_t Lq, Lk;
+    LisConsts k;
+    // fused / A.V part
+    const int8_t* v;        // [G, Lk, d]  (nullable for codes-only)
+    int32_t zp_v;
+    int32_t d;
+    int32_t* out;           // [G, Lq, d]  (nullable for codes-only)
+    uint8_t* codes;         // nullable [G, Lq, ld_codes]
+    int32_t ld_codes;
+};
+
+hipError_t launch_lis(const LisArgs& a, hipStream_t stream);
+
+struct AvArgs {
+    const uint8_t* codes;
+    int32_t ld_codes;
+    const int8_t* v;
+    int32_t zp_v;
+    int64_t G;
+    int32_t Lq, Lk, d;
+    int32_t top;            // 2^bits - 1
+    int32_t* out;
+};
+
+hipError_t launch_attn_v_shift(const AvArgs& a, hipStream_t stream);
+
+}  // namespace fqvit

@@ -1,0 +1,153 @@
+"""The C ABI library loads, exports every entry point its header declares, and
+rejects invalid arguments on the host before anything is enqueued.  No test
+here launches a kernel or needs a GPU: every call below fails validation (or
+is empty) before the first HIP runtime call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2111_13824_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fqvit.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return re.findall(r"^\s*(?:const\s+)?[A-Za-z_][A-Za-z0-9_]*\**\s+\**([a-z_][a-z0-9_]*)\s*\(",
+                      text, flags=re.M)
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(B.LIB_PATH):
+        from paper_2111_13824_amd import build
+        build.build()
+    return B.lib()
+
+
+def test_header_symbols_exported(lib):
+    names = _declared_functions()
+    assert set(names) >= {"ptf_layernorm_int8", "lis_softmax_log4", "lis_attn_v_shift",
+                          "lis_attention_head", "fq_status_str", "fq_version"}
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in fqvit.h but not exported"
+    # the binding exposes the compute entry points under the same names
+    for n in B.SIGNATURES:
+        assert n in names
+
+
+def test_status_strings(lib):
+    for s in range(6):
+        assert B.status_str(s).startswith("FQ_")
+    assert "unknown" in B.status_str(99)
+    assert B.version() == 100
+
+
+NULL = None
+
+
+def test_layernorm_validation(lib):
+    f = lib.ptf_layernorm_int8
+    args = dict(x=1, T=4, C=8, zp=0, alpha=1, K=3, g=1, b=1, s=0.1, zpo=0, bits=8, y=1)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return f(a["x"], a["T"], a["C"], a["zp"], a["alpha"], a["K"], a["g"], a["b"], a["s"],
+                 a["zpo"], a["bits"], a["y"], NULL)
+
+    assert call(C=0) == B.FQ_ERR_SHAPE
+    assert call(C=8193) == B.FQ_ERR_SHAPE
+    assert call(T=-1) == B.FQ_ERR_SHAPE
+    assert call(bits=9) == B.FQ_ERR_PARAM
+    assert call(bits=1) == B.FQ_ERR_PARAM
+    assert call(K=8) == B.FQ_ERR_PARAM
+    assert call(K=-1) == B.FQ_ERR_PARAM
+    assert call(s=0.0) == B.FQ_ERR_PARAM
+    assert call(s=float("inf")) == B.FQ_ERR_PARAM
+    assert call(s=float("nan")) == B.FQ_ERR_PARAM
+    assert call(zp=128) == B.FQ_ERR_PARAM
+    assert call(zpo=-129) == B.FQ_ERR_PARAM
+    assert call(bits=4, zp=8) == B.FQ_ERR_PARAM
+    assert call(x=NULL) == B.FQ_ERR_NULL
+    assert call(y=NULL) == B.FQ_ERR_NULL
+    assert call(alpha=NULL) == B.FQ_ERR_NULL
+    assert call(T=0, x=NULL, y=NULL) == B.FQ_OK     # empty: nothing enqueued
+
+
+def test_lis_validation(lib):
+    f = lib.lis_softmax_log4
+    args = dict(lg=1, G=2, Lq=3, Lk=5, bias=NULL, Hb=0, s=2.0 ** -10, bits=4, n=20, codes=1, ld=3)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return f(a["lg"], a["G"], a["Lq"], a["Lk"], a["bias"], a["Hb"], a["s"], a["bits"], a["n"],
+                 a["codes"], a["ld"], NULL)
+
+    assert call(Lk=0) == B.FQ_ERR_SHAPE
+    assert call(Lk=4097, ld=2049) == B.FQ_ERR_SHAPE
+    assert call(ld=2) == B.FQ_ERR_SHAPE
+    assert call(G=-1) == B.FQ_ERR_SHAPE
+    assert call(bias=1, Hb=0) == B.FQ_ERR_SHAPE
+    assert call(bits=0) == B.FQ_ERR_PARAM
+    assert call(bits=5) == B.FQ_ERR_PARAM
+    assert call(n=0) == B.FQ_ERR_PARAM
+    assert call(n=31) == B.FQ_ERR_PARAM
+    assert call(s=0.6) == B.FQ_ERR_PARAM
+    assert call(s=5e-5) == B.FQ_ERR_PARAM
+    assert call(s=1e-4, n=30, Lk=4096, ld=2048) == B.FQ_ERR_HEADROOM
+    assert call(lg=NULL) == B.FQ_ERR_NULL
+    assert call(codes=NULL) == B.FQ_ERR_NULL
+    assert call(G=0, lg=NULL, codes=NULL) == B.FQ_OK
+    assert call(Lq=0, lg=NULL, codes=NULL) == B.FQ_OK
+
+
+def test_attn_v_validation(lib):
+    f = lib.lis_attn_v_shift
+    args = dict(codes=1, ld=3, v=1, zp=0, G=2, Lq=3, Lk=5, d=64, bits=4, out=1)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return f(a["codes"], a["ld"], a["v"], a["zp"], a["G"], a["Lq"], a["Lk"], a["d"], a["bits"],
+                 a["out"], NULL)
+
+    assert call(d=0) == B.FQ_ERR_SHAPE
+    assert call(d=257) == B.FQ_ERR_SHAPE
+    assert call(ld=2) == B.FQ_ERR_SHAPE
+    assert call(bits=5) == B.FQ_ERR_PARAM
+    assert call(zp=128) == B.FQ_ERR_PARAM
+    assert call(out=NULL) == B.FQ_ERR_NULL
+    assert call(v=NULL) == B.FQ_ERR_NULL
+    assert call(G=0, codes=NULL, v=NULL, out=NULL) == B.FQ_OK
+
+
+def test_head_validation(lib):
+    f = lib.lis_attention_head
+    args = dict(lg=1, bias=NULL, Hb=0, G=2, Lq=3, Lk=5, s=2.0 ** -10, bits=4, n=20, v=1, zp=0,
+                d=64, out=1, codes=NULL, ld=0)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return f(a["lg"], a["bias"], a["Hb"], a["G"], a["Lq"], a["Lk"], a["s"], a["bits"], a["n"],
+                 a["v"], a["zp"], a["d"], a["out"], a["codes"], a["ld"], NULL)
+
+    assert call(d=300) == B.FQ_ERR_SHAPE
+    assert call(codes=1, ld=2) == B.FQ_ERR_SHAPE
+    assert call(bias=1, Hb=0) == B.FQ_ERR_SHAPE
+    assert call(zp=-200) == B.FQ_ERR_PARAM
+    assert call(s=0.0) == B.FQ_ERR_PARAM
+    assert call(bits=0) == B.FQ_ERR_PARAM
+    assert call(v=NULL) == B.FQ_ERR_NULL
+    assert call(out=NULL) == B.FQ_ERR_NULL
+    assert call(Lq=0, lg=NULL, v=NULL, out=NULL) == B.FQ_OK
+
+
+def test_binding_requires_library(monkeypatch):
+    """The binding refuses to run without the HIP library instead of falling back."""
+    monkeypatch.setattr(B, "_lib", None)
+    monkeypatch.setattr(B, "LIB_PATH", "/nonexistent/libfqvit.so")
+    with pytest.raises(RuntimeError, match="missing"):
+        B.lib()

@@ -1,0 +1,308 @@
+"""Parity of the HIP library with the CPU oracle, element by element.
+
+Every integer output must be bit-exact.  Small cases span several tiles and
+ragged tails; the full-size configs run the exact launch the benchmark times
+and compare every LayerNorm row and a sample of attention units (all units on
+the two smaller configs).  Each case prints its name before its GPU step."""
+import numpy as np
+import pytest
+
+import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+S = 2.0 ** -10
+
+
+@pytest.fixture(scope="module")
+def fq():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2111_13824_amd as fq
+    return fq
+
+
+def dev(x):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(x)).to("cuda:0")
+
+
+def host(t):
+    import torch
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def say(*a):
+    print("CASE", *a, flush=True)
+
+
+# ---------------------------------------------------------------------------
+# PTF LayerNorm
+# ---------------------------------------------------------------------------
+
+def _ln_gpu(fq, d, **over):
+    p = dict(d, **over)
+    return host(fq.ptf_layernorm_int8(dev(p["x_q"]), p["zp_in"], dev(p["alpha"]), p["K"],
+                                      dev(p["gamma"]), dev(p["beta"]), p["s_out"], p["zp_out"],
+                                      p["bits"]))
+
+
+def _ln_ref(orc, d, **over):
+    p = dict(d, **over)
+    return orc.ptf_layernorm_int8(p["x_q"], p["zp_in"], p["alpha"], p["K"], p["gamma"], p["beta"],
+                                  p["s_out"], p["zp_out"], p["bits"])
+
+
+LN_SHAPES = [(1, 192), (7, 96), (197, 192), (333, 384), (64, 768), (100, 1024), (37, 100),
+             (9, 13), (5, 2048), (3, 4096), (2, 8192), (65, 4), (3, 1), (70, 2000)]
+
+
+@pytest.mark.parametrize("T,C", LN_SHAPES)
+def test_ln_shapes(fq, orc, T, C):
+    say("ln", T, C)
+    d = W.ln_inputs(T, C, seed=T * 31 + C)
+    assert np.array_equal(_ln_gpu(fq, d), _ln_ref(orc, d))
+
+
+@pytest.mark.parametrize("K,bits", [(0, 8), (3, 8), (7, 8), (5, 8), (3, 4), (2, 2), (6, 6)])
+def test_ln_params(fq, orc, K, bits):
+    say("ln params", K, bits)
+    rng = np.random.default_rng(K * 10 + bits)
+    d = W.ln_inputs(150, 768, seed=5)
+    half = 2 ** (bits - 1)
+    x = rng.integers(-half, half, size=(150, 768)).astype(np.int8)
+    alpha = rng.integers(0, 8, size=768).astype(np.uint8)
+    zp = int(rng.integers(-half, half))
+    zpo = int(rng.integers(-half, half))
+    over = dict(x_q=x, alpha=alpha, K=K, bits=bits, zp_in=zp, zp_out=zpo)
+    assert np.array_equal(_ln_gpu(fq, d, **over), _ln_ref(orc, d, **over))
+
+
+def test_ln_edge_rows(fq, orc):
+    """Constant rows (zero variance), rows at the zero point, gamma = 0, extreme
+    affine values, tiny and huge s_out."""
+    say("ln edges")
+    d = W.ln_inputs(64, 384, seed=9)
+    x = d["x_q"].copy()
+    x[0] = d["zp_in"]
+    x[1] = (d["zp_in"] + (8 >> np.minimum(d["alpha"], 3))).astype(np.int8)
+    x[2] = 127
+    x[3] = -128
+    gamma = d["gamma"].copy()
+    beta = d["beta"].copy()
+    gamma[:5] = 0.0
+    gamma[5] = -gamma[5]
+    gamma[6] = 1e-30
+    gamma[7] = 3e4
+    beta[8] = 1e6
+    beta[9] = -1e6
+    for s_out in (d["s_out"], 1e-6, 1e3, 0.5):
+        over = dict(x_q=x, gamma=gamma, beta=beta, s_out=s_out)
+        assert np.array_equal(_ln_gpu(fq, d, **over), _ln_ref(orc, d, **over)), s_out
+
+
+@pytest.mark.parametrize("cfg", W.CONFIGS, ids=lambda c: c.name)
+def test_ln_full_config(fq, orc, cfg):
+    say("ln full", cfg.name)
+    d = W.config_inputs(cfg, "ln")["ln"]
+    assert np.array_equal(_ln_gpu(fq, d), _ln_ref(orc, d))
+
+
+def test_ln_unaligned_pointers(fq, orc):
+    """A row-major view starting one byte into an allocation takes the general path."""
+    import torch
+    say("ln unaligned")
+    d = W.ln_inputs(40, 192, seed=2)
+    xb = torch.zeros(40 * 192 + 1, dtype=torch.int8, device="cuda:0")
+    xb[1:] = dev(d["x_q"]).reshape(-1)
+    yb = torch.zeros(40 * 192 + 1, dtype=torch.int8, device="cuda:0")
+    x = xb[1:].view(40, 192)
+    y = yb[1:].view(40, 192)
+    fq.ptf_layernorm_int8(x, d["zp_in"], dev(d["alpha"]), d["K"], dev(d["gamma"]),
+                          dev(d["beta"]), d["s_out"], d["zp_out"], d["bits"], y_q=y)
+    assert np.array_equal(host(y), _ln_ref(orc, d))
+
+
+# ---------------------------------------------------------------------------
+# Log-Int-Softmax codes
+# ---------------------------------------------------------------------------
+
+LIS_SHAPES = [(3, 5, 1), (2, 17, 2), (2, 17, 33), (3, 64, 197), (2, 70, 197), (1, 65, 577),
+              (4, 49, 49), (2, 3, 640), (1, 3, 700), (1, 2, 4096), (5, 1, 31), (2, 130, 96)]
+
+
+@pytest.mark.parametrize("G,Lq,Lk", LIS_SHAPES)
+def test_lis_codes_shapes(fq, orc, G, Lq, Lk):
+    say("lis", G, Lq, Lk)
+    a = W.attn_inputs(G, Lq, Lk, 8, seed=G + Lq + Lk, heads=G, sigma=(1.0, 3.0, 6.0))
+    got = host(fq.lis_softmax_log4(dev(a["logits"]), S))
+    assert np.array_equal(got, orc.lis_softmax_log4(a["logits"], S))
+
+
+@pytest.mark.parametrize("s", [0.5, 1e-2, 1e-3, 2.0 ** -10, 2.0 ** -12, 1.2e-4, 1e-4])
+@pytest.mark.parametrize("n", [1, 20, 30])
+def test_lis_codes_scales(fq, orc, s, n):
+    say("lis scale", s, n)
+    a = W.attn_inputs(2, 40, 197, 8, seed=3, sigma=(3.0,), s_logit=s)
+    try:
+        got = host(fq.lis_softmax_log4(dev(a["logits"]), s, exp_n=n))
+    except fq.FqError as e:
+        assert e.status == 4 and n == 30  # headroom rejection at the deepest clamp
+        return
+    assert np.array_equal(got, orc.lis_softmax_log4(a["logits"], s, exp_n=n))
+
+
+@pytest.mark.parametrize("bits", [1, 2, 3, 4])
+def test_lis_codes_bits(fq, orc, bits):
+    say("lis bits", bits)
+    a = W.attn_inputs(3, 33, 77, 8, seed=bits)
+    got = host(fq.lis_softmax_log4(dev(a["logits"]), S, bits=bits))
+    assert np.array_equal(got, orc.lis_softmax_log4(a["logits"], S, bits=bits))
+
+
+def test_lis_codes_bias_and_stride(fq, orc):
+    """Swin relative-position bias (head g % Hb) and a wider code row stride whose
+    extra bytes must stay untouched."""
+    import torch
+    say("lis bias stride")
+    a = W.attn_inputs(12, 49, 49, 8, seed=4, heads=3, bias=True)
+    codes = torch.full((12, 49, 32), 0xAB, dtype=torch.uint8, device="cuda:0")
+    fq.lis_softmax_log4(dev(a["logits"]), S, bias=dev(a["bias"]), codes=codes)
+    got = host(codes)
+    ref = orc.lis_softmax_log4(a["logits"], S, bias=a["bias"])
+    assert np.array_equal(got[..., :25], ref)
+    assert np.all(got[..., 25:] == 0xAB)
+
+
+def test_lis_extreme_logits(fq, orc):
+    """Logits near +-2^30, flat rows, one-hot rows, rows mixing both ends."""
+    say("lis extreme")
+    rng = np.random.default_rng(1)
+    lg = rng.integers(-(2 ** 30) + 1, 2 ** 30, size=(4, 20, 197)).astype(np.int32)
+    lg[0, :5] = 12345
+    lg[1, :, :] = -(2 ** 30) + 1
+    lg[1, np.arange(20), np.arange(20)] = 2 ** 30 - 1
+    lg[2, :, ::2] = 0
+    got = host(fq.lis_softmax_log4(dev(lg), S))
+    assert np.array_equal(got, orc.lis_softmax_log4(lg, S))
+
+
+# ---------------------------------------------------------------------------
+# BitShift Attn x V and the fused head
+# ---------------------------------------------------------------------------
+
+def _random_codes(rng, G, Lq, Lk, bits=4):
+    codes = rng.integers(0, 2 ** bits, size=(G, Lq, Lk))
+    ld = (Lk + 1) // 2
+    packed = np.zeros((G, Lq, ld), dtype=np.uint8)
+    for j in range(Lk):
+        packed[..., j // 2] |= (codes[..., j] << (4 * (j % 2))).astype(np.uint8)
+    return packed
+
+
+@pytest.mark.parametrize("G,Lq,Lk,d,zp", [(2, 5, 1, 64, 0), (3, 17, 33, 16, 3), (2, 64, 197, 64, 0),
+                                          (2, 70, 197, 17, -7), (1, 9, 577, 64, 0),
+                                          (4, 49, 49, 32, 0), (1, 3, 700, 256, 1), (2, 20, 96, 100, 0)])
+def test_attn_v_shift(fq, orc, G, Lq, Lk, d, zp):
+    say("av", G, Lq, Lk, d, zp)
+    rng = np.random.default_rng(G * Lk + d)
+    a = W.attn_inputs(G, Lq, Lk, d, seed=7, v_lo=-128, v_hi=127)
+    codes = orc.lis_softmax_log4(a["logits"], S) if Lk > 1 else _random_codes(rng, G, Lq, Lk)
+    got = host(fq.lis_attn_v_shift(dev(codes), dev(a["v"]), Lk, zp_v=zp))
+    assert np.array_equal(got, orc.lis_attn_v_shift(codes, a["v"], zp_v=zp, Lk=Lk))
+
+
+def test_attn_v_shift_any_codes(fq, orc):
+    """Arbitrary codes (not from LIS), including small-bit widths."""
+    say("av any codes")
+    rng = np.random.default_rng(3)
+    for bits in (1, 2, 3, 4):
+        codes = _random_codes(rng, 2, 33, 65, bits)
+        v = rng.integers(-128, 128, size=(2, 65, 48)).astype(np.int8)
+        got = host(fq.lis_attn_v_shift(dev(codes), dev(v), 65, zp_v=-3, bits=bits))
+        assert np.array_equal(got, orc.lis_attn_v_shift(codes, v, zp_v=-3, bits=bits, Lk=65))
+
+
+HEAD_SHAPES = [(3, 5, 1, 64), (2, 17, 33, 16), (3, 64, 197, 64), (2, 70, 197, 64), (1, 65, 577, 64),
+               (12, 49, 49, 32), (2, 3, 640, 64), (1, 3, 700, 64), (1, 2, 4096, 32), (2, 20, 96, 100),
+               (2, 33, 65, 256), (2, 19, 129, 1)]
+
+
+@pytest.mark.parametrize("G,Lq,Lk,d", HEAD_SHAPES)
+def test_head_shapes(fq, orc, G, Lq, Lk, d):
+    say("head", G, Lq, Lk, d)
+    a = W.attn_inputs(G, Lq, Lk, d, seed=G * 7 + Lk, heads=G, sigma=(1.0, 3.0, 6.0), v_lo=-128,
+                      v_hi=127)
+    got = host(fq.lis_attention_head(dev(a["logits"]), dev(a["v"]), S, zp_v=-2))
+    ref = orc.lis_attention_head(a["logits"], a["v"], S, zp_v=-2)
+    assert np.array_equal(got, ref)
+
+
+def test_head_codes_out_and_unfused_equal(fq, orc):
+    """The fused head writes the same codes as lis_softmax_log4, and its output
+    equals lis_attn_v_shift of those codes (MFMA product vs VALU shifts)."""
+    import torch
+    say("head vs unfused")
+    a = W.attn_inputs(12, 49, 49, 32, seed=11, heads=3, bias=True)
+    codes = torch.zeros((12, 49, 25), dtype=torch.uint8, device="cuda:0")
+    out = fq.lis_attention_head(dev(a["logits"]), dev(a["v"]), S, bias=dev(a["bias"]),
+                                codes_out=codes)
+    c2 = fq.lis_softmax_log4(dev(a["logits"]), S, bias=dev(a["bias"]))
+    out2 = fq.lis_attn_v_shift(c2, dev(a["v"]), 49)
+    assert np.array_equal(host(codes), host(c2))
+    assert np.array_equal(host(out), host(out2))
+    assert np.array_equal(host(out), orc.lis_attention_head(a["logits"], a["v"], S, bias=a["bias"]))
+
+
+def test_head_dominant_rows_saturate_exactly(fq, orc):
+    """Rows whose codes are all 0 but one produce the largest sums the LIS bound
+    allows; the MFMA accumulation must stay exact there."""
+    say("head dominant")
+    lg = np.full((2, 64, 197), -(2 ** 29), dtype=np.int32)
+    lg[:, np.arange(64), np.arange(64)] = 2 ** 29
+    v = np.full((2, 197, 64), 127, dtype=np.int8)
+    v[1] = -128
+    got = host(fq.lis_attention_head(dev(lg), dev(v), S, zp_v=127))
+    assert np.array_equal(got, orc.lis_attention_head(lg, v, S, zp_v=127))
+
+
+def test_empty_calls_are_noops(fq):
+    import torch
+    say("empty")
+    z = torch.zeros((0, 5, 7), dtype=torch.int32, device="cuda:0")
+    v = torch.zeros((0, 7, 8), dtype=torch.int8, device="cuda:0")
+    assert fq.lis_attention_head(z, v, S).shape == (0, 5, 8)
+    x = torch.zeros((0, 16), dtype=torch.int8, device="cuda:0")
+    al = torch.zeros(16, dtype=torch.uint8, device="cuda:0")
+    gm = torch.ones(16, dtype=torch.float32, device="cuda:0")
+    assert fq.ptf_layernorm_int8(x, 0, al, 3, gm, gm, 0.1, 0).shape == (0, 16)
+
+
+# ---------------------------------------------------------------------------
+# Full-size configs (the benchmark's launch), sampled units
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("cfg", W.CONFIGS, ids=lambda c: c.name)
+def test_head_full_config(fq, orc, cfg):
+    import torch
+    say("head full", cfg.name)
+    a = W.config_inputs(cfg, "attn")["attn"]
+    bias = dev(a["bias"]) if a["bias"] is not None else None
+    out = host(fq.lis_attention_head(dev(a["logits"]), dev(a["v"]), a["s_logit"], a["bits"],
+                                     a["exp_n"], a["zp_v"], bias=bias))
+    G = cfg.G
+    if G <= 64:
+        units = np.arange(G)
+    else:
+        units = np.unique(np.concatenate([np.arange(8), np.arange(G - 8, G),
+                                          np.random.default_rng(0).choice(G, 48, replace=False)]))
+    b = None
+    if a["bias"] is not None:
+        # the sampled units keep their own heads: reorder the bias to match
+        b = a["bias"][units % a["Hb"]]
+    ref = orc.lis_attention_head(a["logits"][units], a["v"][units], a["s_logit"], a["bits"],
+                                 a["exp_n"], a["zp_v"], bias=b)
+    assert np.array_equal(out[units], ref)
+    del torch

@@ -145,6 +145,8 @@ def ln_inputs(T: int, C: int, seed: int, outliers: int = 0, alpha_uniform: bool 
     var = Xs.var(axis=1, keepdims=True)
     Y = (Xs - mu) / np.sqrt(var + 1e-6) * gamma.astype(np.float64) + beta.astype(np.float64)
     ylo, yhi = float(Y.min()), float(Y.max())
+    if yhi - ylo < 1e-3:            # e.g. C = 1: the output is beta on every row
+        ylo, yhi = ylo - 0.5, yhi + 0.5
     s_out = np.float32((yhi - ylo) / 255.0)
     zp_out = int(np.clip(np.rint(-ylo / float(s_out)), 0, 255)) - 128
 
