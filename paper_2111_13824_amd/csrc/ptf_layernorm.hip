@@ -49,6 +49,28 @@ __device__ __forceinline__ T seg_sum(T v, int L) {
     return v;
 }
 
+// Sum over aligned segments of L lanes (L a power of two <= 64), result in
+// every lane of the segment.  Within a row of 16 lanes: DPP quad permutes
+// (xor 1, xor 2), then half-row and row mirrors, each of which pairs lanes
+// whose partial sums are already equal across the group they stand for.
+// Across rows: readlane of the row totals.
+__device__ __forceinline__ int dpp_seg_sum(int v, int L) {
+    if (L >= 2) v += __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);   // quad_perm 1,0,3,2
+    if (L >= 4) v += __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);   // quad_perm 2,3,0,1
+    if (L >= 8) v += __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false);  // row_half_mirror
+    if (L >= 16) v += __builtin_amdgcn_update_dpp(0, v, 0x140, 0xF, 0xF, false); // row_mirror
+    if (L >= 32) {
+        const int r0 = __builtin_amdgcn_readlane(v, 0), r1 = __builtin_amdgcn_readlane(v, 16);
+        const int r2 = __builtin_amdgcn_readlane(v, 32), r3 = __builtin_amdgcn_readlane(v, 48);
+        if (L == 64) {
+            v = r0 + r1 + r2 + r3;
+        } else {
+            v = ((threadIdx.x & 63) < 32) ? r0 + r1 : r2 + r3;
+        }
+    }
+    return v;
+}
+
 // Per-row factors: r = C / sqrt(V), m = M1 / sqrt(V); both 0 for V = 0.
 __device__ __forceinline__ void row_factors(int64_t m1, int64_t m2, int C, double& r,
                                             double& m) {
@@ -62,27 +84,69 @@ __device__ __forceinline__ void row_factors(int64_t m1, int64_t m2, int C, doubl
     }
 }
 
+// Output of one element when A = gs r is known to lie in [2^(b-31), 2^b): then
+// N1 = b - 1 - floor(log2 |A|) needs no clamp and sign(A) N2 / 2^N1 is A with
+// its significand cut to b bits, a mask on the high word (b <= 8 keeps the
+// low word zero).  Same result as ln_requant.
+// dlo, dhi: the output bounds minus zp_out.
+__device__ __forceinline__ int ln_requant_fast(double A, double B, int xh, int bits,
+                                               uint32_t hi_mask, int zp_out, double dlo,
+                                               double dhi) {
+    const int N1 = bits - __builtin_amdgcn_frexp_exp(A);
+    const uint64_t ab = __double_as_longlong(A);
+    const double At = __longlong_as_double((int64_t)(((uint64_t)((uint32_t)(ab >> 32) & hi_mask)) << 32));
+    const double Bg = ldexp(rint(ldexp(B, N1)), -N1);
+    const double val = fma(At, (double)xh, Bg + 0.5);
+    return (int)floor(fmin(fmax(val, dlo), dhi)) + zp_out;
+}
+
 // Fast path: C % 4 == 0, dword-aligned rows, W dwords per lane (W <= 8).
 // WIDE selects 64-bit per-lane sums of squares (K >= 6).
 template <int W, bool WIDE>
 __global__ __launch_bounds__(kBlock) void ln_fast_kernel(LnArgs a, int lshift) {
     extern __shared__ double smem[];
+    const int nd = a.C >> 2;
+    // LDS layout [b][dword]: lane li reads entry (b, li + L w), so the lanes of
+    // a wavefront read consecutive entries.
     double* s_gs = smem;
     double* s_bs = smem + a.C;
-    int* s_mul = reinterpret_cast<int*>(smem + 2 * a.C);
+    int* s_sh = reinterpret_cast<int*>(smem + 2 * a.C);
+    __shared__ double s_ext[2][kBlock / 64];
+    __shared__ int s_zero[kBlock / 64];
+    double gmax = 0.0, gmin = INFINITY;
+    int anyzero = 0;
     for (int c = threadIdx.x; c < a.C; c += blockDim.x) {
-        s_gs[c] = (double)a.gamma[c] / (double)a.s_out;
-        s_bs[c] = (double)a.beta[c] / (double)a.s_out;
-        s_mul[c] = 1 << min((int)a.alpha[c], a.K);
+        const int e = (c & 3) * nd + (c >> 2);
+        const double gs = (double)a.gamma[c] / (double)a.s_out;
+        s_gs[e] = gs;
+        s_bs[e] = (double)a.beta[c] / (double)a.s_out;
+        s_sh[e] = min((int)a.alpha[c], a.K);
+        const double ag = fabs(gs);
+        gmax = fmax(gmax, ag);
+        if (ag == 0.0) anyzero = 1; else gmin = fmin(gmin, ag);
+    }
+    for (int off = 1; off < 64; off <<= 1) {
+        gmax = fmax(gmax, __shfl_xor(gmax, off, 64));
+        gmin = fmin(gmin, __shfl_xor(gmin, off, 64));
+        anyzero |= __shfl_xor(anyzero, off, 64);
+    }
+    if ((threadIdx.x & 63) == 0) {
+        s_ext[0][threadIdx.x >> 6] = gmax;
+        s_ext[1][threadIdx.x >> 6] = gmin;
+        s_zero[threadIdx.x >> 6] = anyzero;
     }
     __syncthreads();
+    for (int w = 0; w < (int)(blockDim.x >> 6); ++w) {
+        gmax = fmax(gmax, s_ext[0][w]);
+        gmin = fmin(gmin, s_ext[1][w]);
+        anyzero |= s_zero[w];
+    }
 
     const int lane = threadIdx.x & 63;
     const int L = 1 << lshift;
     const int seg = lane >> lshift;
     const int li = lane & (L - 1);
     const int R = 64 >> lshift;
-    const int nd = a.C >> 2;
 
     double gs[4 * W], bs[4 * W];
     int mul[4 * W];
@@ -93,62 +157,104 @@ __global__ __launch_bounds__(kBlock) void ln_fast_kernel(LnArgs a, int lshift) {
         ok[w] = dw < nd;
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
-            const int c = ok[w] ? 4 * dw + b : 0;
-            gs[4 * w + b] = s_gs[c];
-            bs[4 * w + b] = s_bs[c];
-            mul[4 * w + b] = ok[w] ? s_mul[c] : 0;
+            const int e = ok[w] ? b * nd + dw : 0;
+            gs[4 * w + b] = s_gs[e];
+            bs[4 * w + b] = s_bs[e];
+            mul[4 * w + b] = ok[w] ? 1 << s_sh[e] : 0;
         }
     }
 
     const int qlo = -(1 << (a.bits - 1));
     const int qhi = (1 << (a.bits - 1)) - 1;
+    const uint32_t hi_mask = ~((1u << (21 - a.bits)) - 1u);   // keep sign, exponent, b-1 bits
+    const double amax = ldexp(1.0, a.bits), amin = ldexp(1.0, a.bits - 31);
+    const double dlo = (double)(qlo - a.zp_out), dhi = (double)(qhi - a.zp_out);
     const int64_t gw = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
     const int64_t nw = ((int64_t)gridDim.x * blockDim.x) >> 6;
 
-    for (int64_t r0 = gw * R; r0 < a.T; r0 += nw * R) {
+    int64_t r0 = gw * R;
+    uint32_t xn[W];
+    {
+        const int64_t row = r0 + seg;
+        const uint32_t* xr = reinterpret_cast<const uint32_t*>(a.x + (row < a.T ? row : 0) * a.C);
+#pragma unroll
+        for (int w = 0; w < W; ++w) xn[w] = ok[w] ? __builtin_nontemporal_load(xr + li + (w << lshift)) : 0u;
+    }
+    for (; r0 < a.T; r0 += nw * R) {
         const int64_t row = r0 + seg;
         const bool rok = row < a.T;
         const int64_t rr = rok ? row : 0;
-        const uint32_t* xr = reinterpret_cast<const uint32_t*>(a.x + rr * a.C);
         uint32_t xv[W];
 #pragma unroll
-        for (int w = 0; w < W; ++w)
-            xv[w] = ok[w] ? __builtin_nontemporal_load(xr + li + (w << lshift)) : 0u;
+        for (int w = 0; w < W; ++w) xv[w] = xn[w];
+        {   // prefetch the next row of this lane
+            const int64_t nrow = r0 + nw * R + seg;
+            const uint32_t* xr = reinterpret_cast<const uint32_t*>(a.x + (nrow < a.T ? nrow : 0) * a.C);
+#pragma unroll
+            for (int w = 0; w < W; ++w)
+                xn[w] = (ok[w] && r0 + nw * R < a.T) ? __builtin_nontemporal_load(xr + li + (w << lshift)) : 0u;
+        }
 
         int xh[4 * W];
         int m1 = 0;
-        int m2 = 0;
+        uint32_t m2 = 0;
         int64_t m2w = 0;
 #pragma unroll
         for (int w = 0; w < W; ++w) {
 #pragma unroll
             for (int b = 0; b < 4; ++b) {
                 const int x = (int)(int8_t)(xv[w] >> (8 * b));
-                const int h = (x - a.zp_in) * mul[4 * w + b];   // 0 for channels past C
+                const int h = __mul24(x - a.zp_in, mul[4 * w + b]);   // 0 past C
                 xh[4 * w + b] = h;
                 m1 += h;
                 if (WIDE) m2w += (int64_t)h * h;
-                else m2 += h * h;
+                else m2 += (uint32_t)__mul24(h, h);
             }
         }
-        const int64_t M1 = seg_sum<int>(m1, L);
-        const int64_t M2 = WIDE ? seg_sum<int64_t>(m2w, L) : seg_sum<int64_t>((int64_t)m2, L);
+        int64_t M1, M2;
+        if (WIDE) {
+            M1 = seg_sum<int>(m1, L);
+            M2 = seg_sum<int64_t>(m2w, L);
+        } else {
+            // per-lane m2 < 2^31: sum its 16-bit halves separately in 32 bits
+            M1 = dpp_seg_sum(m1, L);
+            const int lo = dpp_seg_sum((int)(m2 & 0xFFFFu), L);
+            const int hi = dpp_seg_sum((int)(m2 >> 16), L);
+            M2 = ((int64_t)hi << 16) + lo;
+        }
         double r, m;
         row_factors(M1, M2, a.C, r, m);
+        const bool fast = r > 0.0 && !anyzero && gmax * r < amax && gmin * r >= amin;
 
         uint32_t* yr = reinterpret_cast<uint32_t*>(a.y + rr * a.C);
+        if (fast) {
 #pragma unroll
-        for (int w = 0; w < W; ++w) {
-            uint32_t pack = 0;
+            for (int w = 0; w < W; ++w) {
+                uint32_t pack = 0;
 #pragma unroll
-            for (int b = 0; b < 4; ++b) {
-                const int k = 4 * w + b;
-                const double A = gs[k] * r;
-                const double B = bs[k] - gs[k] * m;
-                const int q = ln_requant(A, B, xh[k], a.bits, a.zp_out, qlo, qhi);
-                pack |= ((uint32_t)q & 0xFFu) << (8 * b);
+                for (int b = 0; b < 4; ++b) {
+                    const int k = 4 * w + b;
+                    const double A = gs[k] * r;
+                    const double B = bs[k] - gs[k] * m;
+                    const int q = ln_requant_fast(A, B, xh[k], a.bits, hi_mask, a.zp_out, dlo, dhi);
+                    pack |= ((uint32_t)q & 0xFFu) << (8 * b);
+                }
+                if (rok && ok[w]) __builtin_nontemporal_store(pack, yr + li + (w << lshift));
             }
-            if (rok && ok[w]) __builtin_nontemporal_store(pack, yr + li + (w << lshift));
+        } else {
+#pragma unroll
+            for (int w = 0; w < W; ++w) {
+                uint32_t pack = 0;
+#pragma unroll
+                for (int b = 0; b < 4; ++b) {
+                    const int k = 4 * w + b;
+                    const double A = gs[k] * r;
+                    const double B = bs[k] - gs[k] * m;
+                    const int q = ln_requant(A, B, xh[k], a.bits, a.zp_out, qlo, qhi);
+                    pack |= ((uint32_t)q & 0xFFu) << (8 * b);
+                }
+                if (rok && ok[w]) __builtin_nontemporal_store(pack, yr + li + (w << lshift));
+            }
         }
     }
 }
