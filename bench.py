@@ -9,7 +9,10 @@ Inputs are synthetic (seeded generators of ``workloads``) and resident in HBM
 before timing.  Four independent copies of every tensor (4 x 187 MB) rotate
 from step to step so that the 256 MB Infinity Cache cannot hold the working
 set.  Warm-up steps are untimed; the K timed steps are bracketed by device
-synchronisation, and HIP events on the launch stream time every kernel launch.
+synchronisation and two events on the launch stream.  Inside the timed
+region every kernel carries a pair of HIP events attached to its own launch
+(fq_time_next_call), which record the kernel's start and end without adding
+packets to the stream, so the per-kernel averages are kernel durations.
 
 Prints one JSON line with the throughput in tokens/s, the roofline of the
 dominant kernel (lis_attention_head) against the 8 TB/s HBM peak, and the
@@ -26,6 +29,91 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 N_SETS = 4
+COPY_BYTES = 512 * 2 ** 20
+COPY_REPS = 3
+# Summary of the counter runs of the fused head; its traffic figure is used only
+# while the hash of the LIS sources matches the one recorded with it.
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "lis_attention_head_vit_base16_224_b64_traffic.txt")
+LIS_SOURCES = ["lis_device.h", "lis_attention.hip", "lis_inst_lo.hip", "lis_inst_hi.hip",
+               "lis_inst_unit.hip",
+               "fqvit_internal.h"]
+
+
+def lis_sources_sha256():
+    import hashlib
+    h = hashlib.sha256()
+    for name in LIS_SOURCES:
+        with open(os.path.join(ROOT, "paper_2111_13824_amd", "csrc", name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()
+
+
+def recorded_traffic():
+    """HBM bytes per head launch from the counter summary, or None when the
+    summary is missing or was taken on other LIS sources."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    fields = {}
+    with open(TRAFFIC_FILE) as f:
+        for line in f:
+            if ":" in line:
+                key, val = line.split(":", 1)
+                fields[key.strip()] = val.strip()
+    if fields.get("lis_sources_sha256") != lis_sources_sha256():
+        return None
+    try:
+        return float(fields["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def pmc_summary(fetch_dir, write_dir):
+    """Per-dispatch FETCH_SIZE / WRITE_SIZE (KiB) of the LayerNorm and head
+    kernels, scaled by the same counter on the calibration copies (the copy
+    dispatches after the last head dispatch, COPY_BYTES read and written each)."""
+    import csv
+    import glob
+
+    def load(d, counter):
+        rows = []
+        for fn in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            with open(fn) as f:
+                rows += [r for r in csv.DictReader(f) if r["Counter_Name"] == counter]
+        rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+        groups = {"head": [], "ln": [], "copy": []}
+        last_head = max((int(r["Dispatch_Id"]) for r in rows if "lis_kernel" in r["Kernel_Name"]),
+                        default=-1)
+        for r in rows:
+            name, v = r["Kernel_Name"], float(r["Counter_Value"])
+            if "lis_kernel" in name:
+                groups["head"].append(v)
+            elif "ln_" in name:
+                groups["ln"].append(v)
+            elif "copy" in name.lower() and int(r["Dispatch_Id"]) > last_head:
+                groups["copy"].append(v)
+        return {k: (sum(v) / len(v) if v else float("nan"), len(v)) for k, v in groups.items()}
+
+    fetch, write = load(fetch_dir, "FETCH_SIZE"), load(write_dir, "WRITE_SIZE")
+    copy_kib = COPY_BYTES / 1024.0
+    f_scale = copy_kib / fetch["copy"][0]
+    w_scale = copy_kib / write["copy"][0]
+    cfg_bytes = algorithmic_bytes(__import__("workloads").BY_NAME["vit_base16_224_b64"])
+    out = []
+    out.append(f"calibration copy: {COPY_BYTES} B read + written per dispatch, "
+               f"FETCH_SIZE {fetch['copy'][0]:.1f} KiB (n={fetch['copy'][1]}), "
+               f"WRITE_SIZE {write['copy'][0]:.1f} KiB (n={write['copy'][1]})")
+    out.append(f"scale: fetch x{f_scale:.4f}, write x{w_scale:.4f}")
+    for key, alg in (("ln", cfg_bytes[0]), ("head", cfg_bytes[1])):
+        fb = fetch[key][0] * 1024.0 * f_scale
+        wb = write[key][0] * 1024.0 * w_scale
+        out.append(f"{key}: FETCH_SIZE {fetch[key][0]:.1f} KiB (n={fetch[key][1]}), "
+                   f"WRITE_SIZE {write[key][0]:.1f} KiB (n={write[key][1]}); scaled read {fb:.0f} B"
+                   f" + write {wb:.0f} B = {fb + wb:.0f} B per launch; algorithmic {alg} B"
+                   f" (ratio {(fb + wb) / alg:.3f})")
+        if key == "head":
+            out.append(f"traffic_bytes_per_launch: {fb + wb:.0f}")
+    out.append(f"lis_sources_sha256: {lis_sources_sha256()}")
+    print("\n".join(out))
 
 
 def parse():
@@ -35,8 +123,12 @@ def parse():
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--config", default="vit_base16_224_b64")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--traffic", default=None,
-                   help="JSON file with measured HBM bytes per head launch (from counters)")
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="after the timed steps, run COPY_REPS device copies of COPY_BYTES "
+                        "(the known-size kernel that scales the traffic counters)")
+    p.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                   help="no GPU: summarise two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) "
+                        "of this script with --copy-calibration and print the traffic per launch")
     return p.parse_args()
 
 
@@ -67,8 +159,44 @@ def cpu_baseline(cfg, inp, reps=2):
                       f" {dt:.1f} s"}
 
 
+class HipEvents:
+    """Pairs of hipEvent_t created through the HIP runtime the process has loaded."""
+
+    def __init__(self, n):
+        import ctypes
+        self.ct = ctypes
+        self.hip = ctypes.CDLL("libamdhip64.so.7")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                 ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.pairs = [(self._create(), self._create()) for _ in range(n)]
+
+    def _create(self):
+        ev = self.ct.c_void_p()
+        rc = self.hip.hipEventCreate(self.ct.byref(ev))
+        if rc != 0:
+            raise RuntimeError(f"hipEventCreate failed ({rc})")
+        return ev.value
+
+    def elapsed_ms(self, i):
+        ms = self.ct.c_float()
+        rc = self.hip.hipEventElapsedTime(self.ct.byref(ms), self.pairs[i][0], self.pairs[i][1])
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
+        return ms.value
+
+    def close(self):
+        for a, b in self.pairs:
+            self.hip.hipEventDestroy(a)
+            self.hip.hipEventDestroy(b)
+
+
 def main():
     args = parse()
+    if args.pmc_summary:
+        pmc_summary(*args.pmc_summary)
+        return
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
               "the hot path shards without communication, see the design notes.", file=sys.stderr)
@@ -101,47 +229,52 @@ def main():
         sets.append(t)
     torch.cuda.synchronize()
 
-    def step(t, ev=None):
-        if ev is not None:
-            ev[0].record()
+    def step(t, ev_ln=None, ev_head=None):
+        if ev_ln is not None:
+            fq.time_next_call(*ev_ln)
         fq.ptf_layernorm_int8(t["x"], ln["zp_in"], t["alpha"], ln["K"], t["gamma"], t["beta"],
                               ln["s_out"], ln["zp_out"], ln["bits"], y_q=t["y"])
-        if ev is not None:
-            ev[1].record()
+        if ev_head is not None:
+            fq.time_next_call(*ev_head)
         fq.lis_attention_head(t["logits"], t["v"], a["s_logit"], a["bits"], a["exp_n"], a["zp_v"],
                               bias=bias, out=t["out"])
-        if ev is not None:
-            ev[2].record()
 
     for i in range(args.warmup):
         step(sets[i % N_SETS])
     torch.cuda.synchronize()
 
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    ev_ln = HipEvents(args.steps)
+    ev_head = HipEvents(args.steps)
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     t_start.record()
     for i in range(args.steps):
-        step(sets[i % N_SETS], evs[i])
+        step(sets[i % N_SETS], ev_ln.pairs[i], ev_head.pairs[i])
     t_end.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
 
     total_ms = t_start.elapsed_time(t_end)
     ms_step = total_ms / args.steps
-    ln_ms = [e[0].elapsed_time(e[1]) for e in evs]
-    head_ms = [e[1].elapsed_time(e[2]) for e in evs]
+    ln_ms = [ev_ln.elapsed_ms(i) for i in range(args.steps)]
+    head_ms = [ev_head.elapsed_ms(i) for i in range(args.steps)]
+    ev_ln.close()
+    ev_head.close()
     ln_avg = sum(ln_ms) / len(ln_ms)
     head_avg = sum(head_ms) / len(head_ms)
 
     ln_bytes, head_bytes = algorithmic_bytes(cfg)
     achieved = head_bytes / (head_avg * 1e-3) / 1e9
-    traffic = None
-    if args.traffic and os.path.exists(args.traffic):
-        with open(args.traffic) as f:
-            traffic = json.load(f).get("head_bytes_per_launch")
+    traffic = recorded_traffic()
+    if args.copy_calibration:
+        src = torch.empty(COPY_BYTES // 4, dtype=torch.int32, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(COPY_REPS):
+            dst.copy_(src)
+        torch.cuda.synchronize()
 
     result = {
         "metric": "tokens/s and achieved HBM GB/s for PTF-LayerNorm + LIS attention, ViT-B bs64",

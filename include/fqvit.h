@@ -6,9 +6,10 @@
  *
  * Conventions shared by every entry point
  *   - Tensor arguments are DEVICE pointers into memory the caller owns (for
- *     example allocated through torch).  The library allocates nothing, keeps
- *     no state between calls, never synchronises, and enqueues its kernels on
- *     `stream` (a hipStream_t; NULL is the default stream).  It is re-entrant.
+ *     example allocated through torch).  The library allocates nothing, never
+ *     synchronises, and enqueues its kernels on `stream` (a hipStream_t; NULL
+ *     is the default stream).  It keeps no state between calls apart from the
+ *     per-thread timing events of fq_time_next_call.  It is re-entrant.
  *   - Scalars are passed by value.  Tensors are dense and row-major with the
  *     shapes given below; a tensor is read or written only inside the extent
  *     its shape gives.
@@ -45,6 +46,19 @@ const char* fq_status_str(int status);
 
 /* Library version as major * 10000 + minor * 100 + patch. */
 int32_t fq_version(void);
+
+/*
+ * Instrumentation, not part of the method.  Attaches two caller-created HIP
+ * events (hipEvent_t, from hipEventCreate; either may be NULL) to the kernel
+ * launched by the next entry-point call made on the calling thread: `start`
+ * then records that kernel's start and `stop` its end (hipExtLaunchKernel
+ * semantics), so hipEventElapsedTime gives the kernel's own duration with no
+ * extra packets on the stream.  Every entry point launches at most one kernel.
+ * The events are consumed by that next call whatever it returns; a call that
+ * enqueues nothing (empty tensors, failed validation) leaves them unrecorded.
+ * Always returns FQ_OK.
+ */
+fq_status fq_time_next_call(void* start_event, void* stop_event);
 
 /*
  * PTF LayerNorm, integer-only (Sec. 3.2, eq. 12 for the shift; Supplement A.1

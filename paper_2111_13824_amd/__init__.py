@@ -5,7 +5,8 @@ The computation lives in libfqvit.so (HIP kernels behind the C ABI of
 include/fqvit.h); this package only builds and binds it.
 """
 from .binding import (FqError, codes_ld, lis_attention_head, lis_attn_v_shift,  # noqa: F401
-                      lis_softmax_log4, ptf_layernorm_int8, status_str, version)
+                      lis_softmax_log4, ptf_layernorm_int8, status_str, time_next_call,
+                      version)
 
 __all__ = ["ptf_layernorm_int8", "lis_softmax_log4", "lis_attn_v_shift", "lis_attention_head",
-           "FqError", "codes_ld", "status_str", "version"]
+           "FqError", "codes_ld", "status_str", "time_next_call", "version"]

@@ -54,6 +54,8 @@ def lib() -> ctypes.CDLL:
         L.fq_status_str.restype = ctypes.c_char_p
         L.fq_version.argtypes = []
         L.fq_version.restype = ctypes.c_int32
+        L.fq_time_next_call.argtypes = [_P, _P]
+        L.fq_time_next_call.restype = ctypes.c_int32
         _lib = L
     return _lib
 
@@ -66,25 +68,36 @@ def version() -> int:
     return lib().fq_version()
 
 
-def _stream(stream=None) -> int:
+def time_next_call(start_event: int, stop_event: int) -> None:
+    """Attach two hipEvent_t handles (ints) to the kernel of the next call on
+    this thread: they record that kernel's own start and end."""
+    lib().fq_time_next_call(start_event or None, stop_event or None)
+
+
+def _stream(stream, like) -> int:
+    """Raw hipStream_t: the given torch stream, else torch's current stream on
+    the device of tensor `like` (read without creating a Stream object)."""
+    if stream is not None:
+        return stream.cuda_stream
     import torch
-    s = torch.cuda.current_stream() if stream is None else stream
-    return s.cuda_stream
+    return torch._C._cuda_getCurrentRawStream(like.device.index)
 
 
 def _dev_ptr(t, dtype, name: str, ndim: Optional[int] = None):
-    import torch
     if t is None:
         return None
-    if not isinstance(t, torch.Tensor):
-        raise TypeError(f"{name} must be a torch.Tensor")
-    if t.dtype != dtype:
-        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
-    if not t.is_cuda:
-        raise ValueError(f"{name} must be a device tensor")
-    if not t.is_contiguous():
-        raise ValueError(f"{name} must be contiguous")
-    if ndim is not None and t.dim() != ndim:
+    try:
+        ok = (t.dtype is dtype and t.is_cuda and (ndim is None or t.dim() == ndim)
+              and t.is_contiguous())
+    except AttributeError:
+        raise TypeError(f"{name} must be a torch.Tensor") from None
+    if not ok:
+        if t.dtype != dtype:
+            raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be a device tensor")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
         raise ValueError(f"{name} must have {ndim} dimensions, got {t.dim()}")
     return t.data_ptr()
 
@@ -107,7 +120,7 @@ def ptf_layernorm_int8(x_q, zp_in: int, alpha, K: int, gamma, beta, s_out: float
                                   _dev_ptr(alpha, torch.uint8, "alpha", 1), K,
                                   _dev_ptr(gamma, torch.float32, "gamma", 1),
                                   _dev_ptr(beta, torch.float32, "beta", 1), s_out, zp_out, bits,
-                                  _dev_ptr(y_q, torch.int8, "y_q", 2), _stream(stream))
+                                  _dev_ptr(y_q, torch.int8, "y_q", 2), _stream(stream, x_q))
     _check("ptf_layernorm_int8", st)
     return y_q
 
@@ -133,7 +146,7 @@ def lis_softmax_log4(logits, s_logit: float, bits: int = 4, exp_n: int = 20, bia
     st = lib().lis_softmax_log4(_dev_ptr(logits, torch.int32, "logits", 3), G, Lq, Lk,
                                 _dev_ptr(bias, torch.int32, "bias", 3), Hb, s_logit, bits, exp_n,
                                 _dev_ptr(codes, torch.uint8, "codes", 3), codes.shape[2],
-                                _stream(stream))
+                                _stream(stream, logits))
     _check("lis_softmax_log4", st)
     return codes
 
@@ -151,7 +164,7 @@ def lis_attn_v_shift(codes, v, Lk: int, zp_v: int = 0, bits: int = 4, out=None, 
         raise ValueError("out must be [G, Lq, d]")
     st = lib().lis_attn_v_shift(_dev_ptr(codes, torch.uint8, "codes", 3), ld,
                                 _dev_ptr(v, torch.int8, "v", 3), zp_v, G, Lq, Lk, d, bits,
-                                _dev_ptr(out, torch.int32, "out", 3), _stream(stream))
+                                _dev_ptr(out, torch.int32, "out", 3), _stream(stream, v))
     _check("lis_attn_v_shift", st)
     return out
 
@@ -183,6 +196,6 @@ def lis_attention_head(logits, v, s_logit: float, bits: int = 4, exp_n: int = 20
                                   bits, exp_n, _dev_ptr(v, torch.int8, "v", 3), zp_v, d,
                                   _dev_ptr(out, torch.int32, "out", 3),
                                   _dev_ptr(codes_out, torch.uint8, "codes_out", 3), ld,
-                                  _stream(stream))
+                                  _stream(stream, logits))
     _check("lis_attention_head", st)
     return out

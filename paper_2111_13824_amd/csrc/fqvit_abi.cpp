@@ -1,6 +1,7 @@
 // C ABI of libfqvit (declared in include/fqvit.h): argument validation, the
 // host-side integer constants of I-Exp, and the kernel launches.  Nothing here
-// allocates, synchronises or keeps state between calls.
+// allocates or synchronises; the only state is the per-thread pair of timing
+// events of fq_time_next_call, consumed by the next entry-point call.
 #include "fqvit.h"
 
 #include <cmath>
@@ -15,6 +16,13 @@ constexpr int32_t kMaxLk = 4096;
 constexpr int32_t kMaxD = 256;
 
 fq_status from_hip(hipError_t e) { return e == hipSuccess ? FQ_OK : FQ_ERR_HIP; }
+
+thread_local fqvit::LaunchEvents t_events;
+
+// Clears the timing events when an entry point returns, whatever the path.
+struct ConsumeEvents {
+    ~ConsumeEvents() { t_events = fqvit::LaunchEvents{}; }
+};
 
 // Integer constants of Algorithm 1 (Supplement A.2) for input scale s, plus the
 // bounds that let the kernels use 32-bit and 24-bit arithmetic.
@@ -47,6 +55,18 @@ fq_status lis_constants(float s_logit, int32_t bits, int32_t n, int32_t Lk,
     k->pre = pre;
     k->n = n;
     k->top = (1 << bits) - 1;
+    // The float form: every I-Exp intermediate is an integer below 2^24 (exact
+    // in binary32) and 2S + e is an integer below 2^53 (exact in binary64).
+    const uint64_t qlmax = qb * qb + qc;
+    k->fp_ok = qlmax < (1ull << 24) &&
+               (unsigned __int128)(2 * (uint64_t)Lk + 1) * ((unsigned __int128)qlmax << n) <
+                   ((unsigned __int128)1 << 53);
+    k->f_inv_d = (float)(1.0 / (double)d);
+    k->f_c0 = (float)(0.5 / (double)d - 0.5);
+    k->f_d = (float)d;
+    k->f_qb = (float)qb;
+    k->f_qc = (float)qc;
+    k->f_sK = 0x4B400000 + n;
     return FQ_OK;
 }
 
@@ -56,6 +76,8 @@ bool grid_fits(int64_t G, int32_t Lq, int32_t rows_per_block) {
 }
 
 }  // namespace
+
+const fqvit::LaunchEvents& fqvit::launch_events() { return t_events; }
 
 extern "C" {
 
@@ -73,10 +95,17 @@ const char* fq_status_str(int status) {
 
 int32_t fq_version(void) { return 100; }
 
+fq_status fq_time_next_call(void* start_event, void* stop_event) {
+    t_events.start = (hipEvent_t)start_event;
+    t_events.stop = (hipEvent_t)stop_event;
+    return FQ_OK;
+}
+
 fq_status ptf_layernorm_int8(const int8_t* x_q, int64_t T, int32_t C, int32_t zp_in,
                              const uint8_t* alpha, int32_t K, const float* gamma,
                              const float* beta, float s_out, int32_t zp_out, int32_t bits,
                              int8_t* y_q, void* stream) {
+    ConsumeEvents consume;
     if (T < 0 || C < 1 || C > kMaxC) return FQ_ERR_SHAPE;
     if (bits < 2 || bits > 8 || K < 0 || K > 7) return FQ_ERR_PARAM;
     if (!(s_out > 0.0f) || !std::isfinite(s_out)) return FQ_ERR_PARAM;
@@ -91,6 +120,7 @@ fq_status ptf_layernorm_int8(const int8_t* x_q, int64_t T, int32_t C, int32_t zp
 fq_status lis_softmax_log4(const int32_t* logits, int64_t G, int32_t Lq, int32_t Lk,
                            const int32_t* bias, int32_t Hb, float s_logit, int32_t bits,
                            int32_t exp_n, uint8_t* codes, int32_t ld_codes, void* stream) {
+    ConsumeEvents consume;
     if (G < 0 || Lq < 0 || Lk < 1 || Lk > kMaxLk || ld_codes < (Lk + 1) / 2 || (bias && Hb < 1) ||
         !grid_fits(G, Lq, 64))
         return FQ_ERR_SHAPE;
@@ -115,6 +145,7 @@ fq_status lis_softmax_log4(const int32_t* logits, int64_t G, int32_t Lq, int32_t
 fq_status lis_attn_v_shift(const uint8_t* codes, int32_t ld_codes, const int8_t* v,
                            int32_t zp_v, int64_t G, int32_t Lq, int32_t Lk, int32_t d,
                            int32_t bits, int32_t* out, void* stream) {
+    ConsumeEvents consume;
     if (G < 0 || Lq < 0 || Lk < 1 || Lk > kMaxLk || d < 1 || d > kMaxD ||
         ld_codes < (Lk + 1) / 2 || !grid_fits(G, Lq, 16))
         return FQ_ERR_SHAPE;
@@ -129,6 +160,7 @@ fq_status lis_attention_head(const int32_t* logits, const int32_t* bias, int32_t
                              int64_t G, int32_t Lq, int32_t Lk, float s_logit, int32_t bits,
                              int32_t exp_n, const int8_t* v, int32_t zp_v, int32_t d,
                              int32_t* out, uint8_t* codes_out, int32_t ld_codes, void* stream) {
+    ConsumeEvents consume;
     if (G < 0 || Lq < 0 || Lk < 1 || Lk > kMaxLk || d < 1 || d > kMaxD || (bias && Hb < 1) ||
         (codes_out && ld_codes < (Lk + 1) / 2) || !grid_fits(G, Lq, 64))
         return FQ_ERR_SHAPE;

@@ -2,10 +2,32 @@
 // libfqvit.  Not part of the public interface (include/fqvit.h is).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace fqvit {
+
+// Events attached to the kernel of the current entry-point call on this thread
+// (set by fq_time_next_call, cleared when that call returns).
+struct LaunchEvents {
+    hipEvent_t start = nullptr;
+    hipEvent_t stop = nullptr;
+};
+const LaunchEvents& launch_events();
+
+// Every kernel launch of the library goes through here so that the events, if
+// any, record the kernel's own start and end.
+template <typename... KArgs, typename... Args>
+inline void launch_kernel(void (*kernel)(KArgs...), dim3 grid, dim3 block, size_t lds,
+                          hipStream_t stream, Args... args) {
+    const LaunchEvents& ev = launch_events();
+    if (ev.start || ev.stop)
+        hipExtLaunchKernelGGL(kernel, grid, block, (uint32_t)lds, stream, ev.start, ev.stop, 0,
+                              args...);
+    else
+        hipLaunchKernelGGL(kernel, grid, block, lds, stream, args...);
+}
 
 // ---------------------------------------------------------------------------
 // PTF LayerNorm
@@ -42,6 +64,15 @@ struct LisConsts {
     int32_t pre;        // pre-shift making (d_ln2 << pre) > 256
     int32_t n;          // clamp depth
     int32_t top;        // 2^bits - 1
+    // Exact single/double precision form of the same arithmetic, valid when
+    // q_b^2 + q_c < 2^24 and (2 Lk + 1)(q_b^2 + q_c) 2^n < 2^53 (fp_ok).
+    int32_t fp_ok;
+    float f_inv_d;      // 1 / d_ln2 rounded to float
+    float f_c0;         // 0.5 / d_ln2 - 0.5 rounded to float
+    float f_d;          // d_ln2
+    float f_qb;         // q_b
+    float f_qc;         // q_c
+    int32_t f_sK;       // bit pattern of 1.5 * 2^23 plus n
 };
 
 struct LisArgs {

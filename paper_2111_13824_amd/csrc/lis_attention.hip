@@ -40,7 +40,7 @@ __global__ __launch_bounds__(kBlock) void lis_kernel_stream(LisArgs a, LisLaunch
     int mx = INT_MIN;
     for (int c = 0; c < nc; ++c) {
         int lg[8];
-        load_chunk(lg, row, brow, c, kg, Lk, tail_vec);
+        load_chunk<false>(lg, row, brow, c, kg, Lk, tail_vec);
 #pragma unroll
         for (int t = 0; t < 8; ++t) mx = max(mx, lg[t]);
     }
@@ -50,7 +50,7 @@ __global__ __launch_bounds__(kBlock) void lis_kernel_stream(LisArgs a, LisLaunch
     uint64_t sum = 0;
     for (int c = 0; c < nc; ++c) {
         int lg[8];
-        load_chunk(lg, row, brow, c, kg, Lk, tail_vec);
+        load_chunk<false>(lg, row, brow, c, kg, Lk, tail_vec);
 #pragma unroll
         for (int t = 0; t < 8; ++t) {
             uint32_t z;
@@ -79,7 +79,7 @@ __global__ __launch_bounds__(kBlock) void lis_kernel_stream(LisArgs a, LisLaunch
             __syncthreads();
         }
         int lg[8];
-        load_chunk(lg, row, brow, c, kg, Lk, tail_vec);
+        load_chunk<false>(lg, row, brow, c, kg, Lk, tail_vec);
         int code[8];
         uint32_t pbits[8];
 #pragma unroll
@@ -215,21 +215,34 @@ hipError_t launch_lis(const LisArgs& a, hipStream_t stream) {
     p.n_bias = a.bias ? (int64_t)a.Hb * a.Lq * a.Lk : 0;
     const int64_t blocks = a.G * (int64_t)p.ntiles;
     const dim3 grid((unsigned)blocks);
-    // Register-resident kernels for rows of up to 640 keys: codes only, or the
-    // fused product without a codes output and with d <= 64.
+    const bool fp = a.k.fp_ok != 0;
+    // Unit kernel: rows of up to 224 keys on the float path, V^T in one stage,
+    // and enough units to give every SIMD two busy wavefronts.
+    const int tiles16 = (a.Lq + 15) / 16;
+    const bool unit_ok = nc <= kUnitMaxNC && fp && (!fused || (a.codes == nullptr && dt <= 4)) &&
+                         a.G <= 0x7FFFFFFF && a.G * std::min(4, tiles16) >= 2048;
+    if (unit_ok) {
+        LisLaunch u = p;
+        u.ntiles = tiles16;
+        u.kb = nc * 32;
+        u.ld = u.kb + 8;
+        u.vt_bytes = fused ? u.dpad * u.ld * (int)sizeof(uint16_t) : 0;
+        const bool half = a.Lk - 32 * (nc - 1) <= 16;
+        return launch_lis_unit(nc, fused, dt, half, a, u, (size_t)u.vt_bytes, stream);
+    }
+    // Tile kernels for rows of up to 640 keys: codes only, or the fused product
+    // without a codes output and with d <= 64.
     const bool regs = nc <= 20 && (!fused || (a.codes == nullptr && dt <= 4));
     if (regs) {
-        const bool multi = fused && nc * 32 > max_keys;
         const size_t lds = (size_t)p.vt_bytes;
-        const bool pre0 = a.k.pre == 0;
-        return nc <= 10 ? launch_lis_regs_lo(nc, fused, multi, dt, pre0, a, p, grid, lds, stream)
-                        : launch_lis_regs_hi(nc, fused, multi, dt, pre0, a, p, grid, lds, stream);
+        return nc <= 10 ? launch_lis_regs_lo(nc, fused, dt, fp, a, p, grid, lds, stream)
+                        : launch_lis_regs_hi(nc, fused, dt, fp, a, p, grid, lds, stream);
     }
     const size_t lds = fused ? (size_t)p.vt_bytes : 0;
     if (fused)
-        hipLaunchKernelGGL((lis_kernel_stream<true>), grid, dim3(kBlock), lds, stream, a, p);
+        launch_kernel(lis_kernel_stream<true>, grid, dim3(kBlock), lds, stream, a, p);
     else
-        hipLaunchKernelGGL((lis_kernel_stream<false>), grid, dim3(kBlock), 0, stream, a, p);
+        launch_kernel(lis_kernel_stream<false>, grid, dim3(kBlock), 0, stream, a, p);
     return hipGetLastError();
 }
 
@@ -245,7 +258,7 @@ hipError_t launch_attn_v_shift(const AvArgs& a, hipStream_t stream) {
     kb = std::max(16, std::min(kb, 256));
     const size_t lds = (size_t)kb * dpad * sizeof(int16_t) + (size_t)rows * kb;
     const int64_t blocks = a.G * (int64_t)ntiles;
-    hipLaunchKernelGGL(lis::attn_v_shift_kernel, dim3((unsigned)blocks), dim3(kBlock), lds, stream, a,
+    launch_kernel(lis::attn_v_shift_kernel, dim3((unsigned)blocks), dim3(kBlock), lds, stream, a,
                        tpr, rows, ntiles, kb);
     return hipGetLastError();
 }

@@ -2,36 +2,45 @@
 // Algorithm 2 I-Log2 and Log-Int-Softmax, the clip of the LIS equation; the
 // BitShift product with V of Sec. 3.3 and its zero-point form).
 //
-// Work decomposition.  A workgroup of four wavefronts owns one attention unit
-// g (image x window x head) and 64 consecutive query rows; each wavefront owns
-// 16 rows.  Inside a wavefront, lane (r, kg) = (lane % 16, lane / 16) holds
-// row r and, in every 32-key chunk c, the eight keys
+// Lane layout.  A wavefront owns 16 query rows of one attention unit g
+// (image x window x head).  Lane (r, kg) = (lane % 16, lane / 16) holds row r
+// and, in every 32-key chunk c, the eight keys
 //     32c + 4kg + t       (t = 0..3)   and   32c + 16 + 4kg + t   (t = 0..3),
 // so each 16-byte load of a lane is contiguous and the four lanes of a row
 // cover 64 contiguous bytes per load instruction.  The same eight keys are the
-// eight k-slots the lane feeds to the 16x16x32 bf16 MFMA; V^T is staged in LDS
-// with its keys permuted the same way, so the contraction pairs every key of
-// the attention row with its own V row.
+// eight k-slots the lane feeds to the 16x16x32 bf16 MFMA (the first four are
+// its k-slots of the 16x16x16 MFMA used for a last chunk of at most 16 keys);
+// V^T is staged in LDS with its keys permuted the same way, so the contraction
+// pairs every key of the attention row with its own V row.
 //
-// Per row: max (lane-local, then two cross-lane shuffles), i-exp and the
-// 64-bit sum, then the 4-bit code of every key.  The codes never leave the
-// chip in the fused kernel: each becomes P = 2^(N - code) as a bf16 bit
-// pattern and the chunk is multiplied with V^T by MFMA.  That product is
-// exact: P and V - zp_V are exact in bf16, every product is an integer and
-// every partial sum is an integer of magnitude below 2^24 (the codes of a row
-// satisfy sum_j 2^-code_j < 1.5 + (Lk - 1)/2^15, so |out| <
-// 255 * (1.5 * 2^15 + Lk) < 2^24 for Lk <= 4096), so fp32 accumulation in any
-// order rounds nothing.
+// Per row: max (lane-local, then two cross-lane shuffles), I-Exp and the exact
+// sum S, then the code of every key.  The codes never leave the chip in the
+// fused kernels: each becomes P = 2^(N - code) as a bf16 bit pattern and the
+// chunk is multiplied with V^T by MFMA.  That product is exact: P and V - zp_V
+// are exact in bf16, every product is an integer and every partial sum is an
+// integer of magnitude below 2^24 (the codes of a row satisfy
+// sum_j 2^-code_j < 1.5 + (Lk - 1)/2^15, so |out| < 255 (1.5 2^15 + Lk) < 2^24
+// for Lk <= 4096), so fp32 accumulation in any order rounds nothing.
 //
-// The code needs no division.  With e = qL << s (qL = (q_p + q_b)^2 + q_c,
-// s = n - z), the paper's r = round(S / e) (ties up) and I-Log2 satisfy
-//     I-Log2(r) >= k   <=>   r >= T_k   <=>   2S + e >= 2 T_k e,
-// T_1 = 2, T_k = 3 * 2^(k-2).  Writing Sp = floor(2S / 2^s), W = Sp + qL and
-// Q = 3 qL this is Sp >= Q for k = 1 and W >= Q * 2^(k-1) for k >= 2, so the
-// code is j + 1 - [Sp < Q] with j = floor(log2(W / Q)).  Because msb(W) is
-// msb(2S) - s or one more, j is j0 - 1, j0 or j0 + 1 with
-// j0 = msb(2S) - s - msb(Q) (msb(2S) once per row), and two exact 64-bit
-// comparisons of W against Q 2^j0 and Q 2^(j0+1) settle it.
+// The code needs no division.  With e = qL 2^s (qL = (q_p + q_b)^2 + q_c,
+// s = n - z) and r = round(S / e) (ties up), I-Log2(r) >= k exactly when
+// 2S >= c_k e with c_1 = 3 and c_k = 3 2^(k-1) - 1: for k >= 2 that is
+// (2S + e) / (1.5 e) >= 2^k, and for k = 1 it is 2S >= 3e.  Hence
+//     code = min(m, N) - [2S < 3e],   m = floor(log2((2S + e) / (1.5 e))),
+// (m >= 1 always, since 2S >= 2e, and 2S < 3e forces m = 1).  Two exact
+// evaluations of this formula are implemented:
+//   * float path: I-Exp in binary32 (every intermediate is an integer below
+//     2^24) and the code in binary64 (2S + e is an integer below 2^53), m being
+//     the difference of the IEEE bit patterns of 2S + e and 1.5 e shifted right
+//     by 52 (both positive, so the pattern difference is the exponent
+//     difference minus a borrow exactly when the mantissa of the quotient
+//     falls below 1);
+//   * integer path (any scale the host accepts): 24-bit integer I-Exp and
+//     64-bit comparisons.  With Sp = floor(2S / 2^s), W = Sp + qL and Q = 3 qL,
+//     m = floor(log2(W / Q)) + 1 and 2S < 3e is Sp < Q; msb(W) is msb(2S) - s
+//     or one more, so floor(log2(W / Q)) is j0 - 1, j0 or j0 + 1 with
+//     j0 = msb(2S) - s - msb(Q), settled by two comparisons.
+// The host picks the float path whenever its exactness conditions hold.
 #pragma once
 
 #include "fqvit_internal.h"
@@ -40,10 +49,12 @@ namespace fqvit {
 namespace lis {
 
 constexpr int kBlock = 256;        // four wavefronts
-constexpr int kRowsPerBlock = 64;  // 16 rows per wavefront
+constexpr int kRowsPerBlock = 64;  // 16 rows per wavefront in the tile kernel
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef int32_t i32x4a4 __attribute__((ext_vector_type(4), aligned(4)));
 
@@ -55,37 +66,28 @@ __device__ __forceinline__ int64_t xcd_remap(int64_t b, int64_t total) {
     return (b & 7) * per + (b >> 3);
 }
 
-// floor(u / d) for u <= n d, with magic = floor(2^32 / (d << pre)) + 1 and
-// n (d << pre)^2 < 2^32, (d << pre) > 256 (checked on the host): the 24-bit
-// high multiply is exact under those bounds.
-__device__ __forceinline__ uint32_t div_ln2(uint32_t u, const LisConsts& k) {
-    const uint64_t prod = (uint64_t)((u << k.pre) & 0xFFFFFFu) * (uint64_t)(k.magic & 0xFFFFFFu);
-    return (uint32_t)(prod >> 32);
-}
-
-__device__ __forceinline__ uint16_t bf16_of_int(int x) {
-    // exact for |x| <= 256
-    return (uint16_t)(__float_as_uint((float)x) >> 16);
-}
-
 // Position of key j (0..31) of a chunk in the permuted order: the eight keys
 // of lane group kg are contiguous.
 __device__ __forceinline__ int chunk_pos(int j) {
     return ((j & 15) >> 2) * 8 + ((j >> 4) << 2) + (j & 3);
 }
 
-// Staging of keys [k0, k0 + kcnt) of V[g] into vt[dd][pos] as bf16 bits of
-// v - zp (kcnt a multiple of 32, dpad a multiple of 16).  A work item is a
-// key pair and a group of 16 columns: two 16-byte loads (V rows jj and jj + 1)
-// and sixteen 32-bit LDS stores of bf16 pairs.  The key pair runs fastest
-// across the threads, so the stores of a wavefront hit consecutive dwords
-// (bank-conflict free).  All loads of a thread are issued before its stores.
-// A stage holds at most 40 KB: kcnt * dpad / 32 <= 640 items, at most
-// kStageItems per thread of a 256-thread workgroup.
-constexpr int kStageItems = 3;
+// ---------------------------------------------------------------------------
+// V^T staging.  Keys [k0, k0 + kcnt) of V[g] go to vt[col][pos] as bf16 bits of
+// v - zp (kcnt a multiple of 32).  A work item is four consecutive keys (one
+// 8-byte run of the permuted order) and 16 columns: four 16-byte loads, then
+// per column two bf16 pairs written with one 8-byte LDS store.  Consecutive
+// threads take consecutive key quads, so a wavefront's stores to one column
+// row are contiguous.  Conversion: the byte b of v is flipped to b ^ 0x80
+// (= v + 128, unsigned), converted to float and reduced by 128 + zp, which is
+// exact; the bf16 pattern is the high half of that float.  Keys past Lk and
+// columns past d hold -zp: those keys get P = 0 and those columns are never
+// stored, so any finite value is harmless.
+// ---------------------------------------------------------------------------
+constexpr int kStageItems = 2;     // items per thread and stage: kcnt dpad / 64 <= 512
 
 struct StageRegs {
-    u32x4 w0[kStageItems], w1[kStageItems];
+    u32x4 w[kStageItems][4];
 };
 
 __device__ __forceinline__ u32x4 load_v16(const int8_t* vrow, int dd, int d, bool vec_ok) {
@@ -99,51 +101,65 @@ __device__ __forceinline__ u32x4 load_v16(const int8_t* vrow, int dd, int d, boo
 
 __device__ __forceinline__ void stage_load(StageRegs& sr, const int8_t* vg, int Lk, int d,
                                            int ncg, int k0, int kcnt, bool vec_ok) {
-    const int npairs = kcnt >> 1;
-    const int nitems = npairs * ncg;
+    const int nquads = kcnt >> 2;
+    const int nitems = nquads * ncg;
 #pragma unroll
     for (int it = 0; it < kStageItems; ++it) {
-        const int idx = (int)threadIdx.x + it * (int)blockDim.x;
-        const int cg = idx / npairs;
-        const int j = k0 + 2 * (idx - cg * npairs);
+        const int idx = (int)threadIdx.x + it * kBlock;
+        const int cg = idx / nquads;
+        const int j = k0 + 4 * (idx - cg * nquads);
         const int dd = 16 * cg;
         const bool ok = idx < nitems && dd < d;
-        sr.w0[it] = (ok && j < Lk) ? load_v16(vg + (int64_t)j * d, dd, d, vec_ok) : u32x4{0u, 0u, 0u, 0u};
-        sr.w1[it] = (ok && j + 1 < Lk) ? load_v16(vg + (int64_t)(j + 1) * d, dd, d, vec_ok)
-                                       : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+            sr.w[it][t] = (ok && j + t < Lk) ? load_v16(vg + (int64_t)(j + t) * d, dd, d, vec_ok)
+                                             : u32x4{0u, 0u, 0u, 0u};
     }
+}
+
+// Two bf16 from the high halves of two floats: lo in bits 0..15, hi in 16..31.
+__device__ __forceinline__ uint32_t bf16_pair(float lo, float hi) {
+    return __builtin_amdgcn_perm(__float_as_uint(hi), __float_as_uint(lo), 0x07060302u);
 }
 
 __device__ __forceinline__ void stage_store(const StageRegs& sr, uint16_t* vt, int ld, int ncg,
                                             int kcnt, int zp) {
-    const int npairs = kcnt >> 1;
-    const int nitems = npairs * ncg;
+    const int nquads = kcnt >> 2;
+    const int nitems = nquads * ncg;
+    const float off = (float)(128 + zp);
 #pragma unroll
     for (int it = 0; it < kStageItems; ++it) {
-        const int idx = (int)threadIdx.x + it * (int)blockDim.x;
+        const int idx = (int)threadIdx.x + it * kBlock;
         if (idx >= nitems) continue;
-        const int cg = idx / npairs;
-        const int jj = 2 * (idx - cg * npairs);
-        const int p0 = (jj & ~31) + chunk_pos(jj & 31);   // jj even: p0 + 1 is key jj + 1
+        const int cg = idx / nquads;
+        const int jj = 4 * (idx - cg * nquads);
+        const int pos = (jj & ~31) + chunk_pos(jj & 31);
+        u32x4 w[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) w[t] = sr.w[it][t] ^ 0x80808080u;
 #pragma unroll
         for (int q = 0; q < 16; ++q) {
-            // Keys past Lk and columns past d hold -zp: the keys get P = 0 and
-            // the columns are never stored, so any finite value is harmless.
-            const int x0 = (int)(int8_t)(sr.w0[it][q >> 2] >> (8 * (q & 3)));
-            const int x1 = (int)(int8_t)(sr.w1[it][q >> 2] >> (8 * (q & 3)));
-            *reinterpret_cast<uint32_t*>(vt + (16 * cg + q) * ld + p0) =
-                (uint32_t)bf16_of_int(x0 - zp) | ((uint32_t)bf16_of_int(x1 - zp) << 16);
+            float f[4];
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+                f[t] = (float)((w[t][q >> 2] >> (8 * (q & 3))) & 0xFFu) - off;
+            *reinterpret_cast<u32x2*>(vt + (16 * cg + q) * ld + pos) =
+                u32x2{bf16_pair(f[0], f[1]), bf16_pair(f[2], f[3])};
         }
     }
 }
 
-// Staging of one V^T stage by the whole workgroup (used between stages).
+// Staging of one V^T stage by the whole workgroup.
 __device__ __forceinline__ void stage_vt(uint16_t* vt, int ld, const int8_t* vg, int Lk, int d,
                                          int ncg, int k0, int kcnt, int zp, bool vec_ok) {
     StageRegs sr;
     stage_load(sr, vg, Lk, d, ncg, k0, kcnt, vec_ok);
     stage_store(sr, vt, ld, ncg, kcnt, zp);
 }
+
+// ---------------------------------------------------------------------------
+// Logits
+// ---------------------------------------------------------------------------
 
 // Load the 8 logits (+ bias) of lane (r, kg) in a chunk whose 32 keys are all valid.
 __device__ __forceinline__ void load_full(int (&dst)[8], const int32_t* row, const int32_t* brow,
@@ -164,11 +180,33 @@ __device__ __forceinline__ void load_full(int (&dst)[8], const int32_t* row, con
 // Load the 8 logits (+ bias) of lane (r, kg) in chunk c; keys past Lk get
 // INT_MIN.  vec_ok: the row and bias row are followed by at least 32 * (c + 1)
 // readable elements inside their tensors, so the chunk is read with full
-// vectors and masked afterwards.
+// vectors and masked afterwards.  HALF: only the first four keys (the last
+// chunk holds at most 16 keys).
+template <bool HALF>
 __device__ __forceinline__ void load_chunk(int (&dst)[8], const int32_t* row, const int32_t* brow,
                                            int c, int kg, int Lk, bool vec_ok) {
     const int k0 = 32 * c + 4 * kg;
     const int k1 = k0 + 16;
+    if (HALF) {
+        if (vec_ok || k0 + 4 <= Lk) {
+            const i32x4a4 a = *reinterpret_cast<const i32x4a4*>(row + k0);
+            dst[0] = a.x; dst[1] = a.y; dst[2] = a.z; dst[3] = a.w;
+            if (brow) {
+                const i32x4a4 ba = *reinterpret_cast<const i32x4a4*>(brow + k0);
+                dst[0] += ba.x; dst[1] += ba.y; dst[2] += ba.z; dst[3] += ba.w;
+            }
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+                if (k0 + t >= Lk) dst[t] = INT_MIN;
+        } else {
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+                dst[t] = k0 + t < Lk ? row[k0 + t] + (brow ? brow[k0 + t] : 0) : INT_MIN;
+        }
+#pragma unroll
+        for (int t = 4; t < 8; ++t) dst[t] = INT_MIN;
+        return;
+    }
     if (vec_ok || k1 + 4 <= Lk) {
         load_full(dst, row, brow, c, kg);
 #pragma unroll
@@ -200,13 +238,12 @@ __device__ __forceinline__ void store_codes(uint8_t* crow, int nbytes, int c, in
     if (b1 + 1 < nbytes) crow[b1 + 1] = v3;
 }
 
-
 // Keys of V^T per LDS stage for a padded head dimension dpad: at most 40 KB of
 // LDS per workgroup so that several workgroups share a CU.
 constexpr int vt_stage_keys(int dpad) { return (40960 / (2 * dpad) - 8) / 32 * 32; }
 
 struct LisLaunch {
-    int ntiles;     // row tiles of 64 per unit
+    int ntiles;     // tile kernel: row tiles of 64 per unit; unit kernel: 16-row tiles per unit
     int kb;         // keys per V^T stage (multiple of 32)
     int ld;         // LDS row stride of V^T in bf16 elements
     int dpad;       // 16 * (power of two >= ceil(d / 16))
@@ -216,6 +253,10 @@ struct LisLaunch {
     int64_t n_logits;  // elements of the logits tensor (G Lq Lk)
     int64_t n_bias;    // elements of the bias tensor (Hb Lq Lk), 0 without bias
 };
+
+// ---------------------------------------------------------------------------
+// Integer path
+// ---------------------------------------------------------------------------
 
 // Per-row state after the I-Exp pass.
 struct RowSum {
@@ -233,19 +274,17 @@ __device__ __forceinline__ RowSum row_sum(uint64_t sum, const LisConsts& k) {
 }
 
 // I-Exp of one key (Algorithm 1): returns qL = (q_p + q_b)^2 + q_c and z; the
-// i-exp value is e = qL << (n - z).
+// i-exp value is e = qL << (n - z).  u = -q clamped to n * d_ln2; z = floor(u
+// / d_ln2) by a 24-bit multiply-high with magic = floor(2^32 / (d << pre)) + 1,
+// exact for u <= n d with n (d << pre)^2 < 2^32 and (d << pre) > 256.
 __device__ __forceinline__ uint32_t iexp_qL(int v, int mx, const LisConsts& k, uint32_t& z) {
-    const uint32_t u = min((uint32_t)mx - (uint32_t)v, k.u_max);               // q <- max(q, n q_ln2)
-    z = (uint32_t)(((uint64_t)((u << k.pre) & 0xFFFFFFu) * (uint64_t)k.magic) >> 32);  // floor(q / q_ln2)
+    const uint32_t u = min((uint32_t)mx - (uint32_t)v, k.u_max);
+    z = (uint32_t)(((uint64_t)((u << k.pre) & 0xFFFFFFu) * (uint64_t)k.magic) >> 32);
     const uint32_t w = (k.qb - u + __umul24(z, k.d_ln2)) & 0xFFFFu;            // q_p + q_b
     return __umul24(w, w) + k.qc;
 }
 
-// bf16 exponent field (<< 7) of P = 2^(N - Attn_Q) for one key, from its qL,
-// z and the row state.  Attn_Q = min(I-Log2(round(S / e)), N) via
-// j = floor(log2(W / Q)) with W = floor(2S / 2^s) + qL, Q = 3 qL, s = n - z:
-// msb(W) is msb(2S) - s or one more, so j is j0 - 1, j0 or j0 + 1 with
-// j0 = msb(2S) - s - msb(Q), settled by two exact comparisons.
+// Code min(I-Log2(round(S / e)), N) of one key from its qL, z and the row state.
 __device__ __forceinline__ int lis_code(uint32_t qL, uint32_t z, const RowSum& rs,
                                          const LisConsts& k) {
     const uint64_t Sp = rs.S2 >> (k.n - (int)z);
@@ -257,16 +296,341 @@ __device__ __forceinline__ int lis_code(uint32_t qL, uint32_t z, const RowSum& r
     return min(code, k.top);
 }
 
+// ---------------------------------------------------------------------------
+// Float path
+// ---------------------------------------------------------------------------
+
+// I-Exp of one key in binary32: returns e = qL 2^(n - z) exactly.  u = -q is
+// clamped to n d (q <- max(q, n q_ln2)); z = floor(u / d) is the integer
+// nearest to u / d + 0.5 / d - 0.5, whose distance to the rounding boundaries
+// (at least 0.5 / d >= 2^-17) exceeds the error of the fma (below 2^-18 for
+// z <= 30); adding 1.5 * 2^23 rounds it to that integer, leaves z in the low
+// mantissa bits, and the exponent argument n - z is read from them.  Then
+// q_p + q_b = q_b - u + z d and qL = (q_p + q_b)^2 + q_c are integers below
+// 2^24, computed exactly by fma.
+__device__ __forceinline__ float iexp_f(int v, int mx, const LisConsts& k) {
+    const uint32_t u = min((uint32_t)mx - (uint32_t)v, k.u_max);
+    const float uf = (float)u;
+    const float t = __builtin_fmaf(uf, k.f_inv_d, k.f_c0);
+    const float zb = t + 12582912.0f;            // 1.5 * 2^23 + z
+    const float zf = zb - 12582912.0f;
+    const float w = __builtin_fmaf(zf, k.f_d, k.f_qb - uf);
+    const float qL = __builtin_fmaf(w, w, k.f_qc);
+    return __builtin_ldexpf(qL, k.f_sK - __float_as_int(zb));
+}
+
+// Code of one key from e and 2S (binary64, exact).
+__device__ __forceinline__ int code_f(float e, double S2, int top) {
+    const double ed = (double)e;
+    const double X = S2 + ed;
+    const double Y = ed * 1.5;
+    const int m = (int)((__double_as_longlong(X) - __double_as_longlong(Y)) >> 52);
+    return min(m, top) - (X < ed * 4.0 ? 1 : 0);
+}
+
 // Wavefronts per SIMD the register allocation aims for: the logits of NC chunks
 // take 8 NC registers per lane.
 constexpr int lis_waves_per_simd(int NC) { return NC <= 8 ? 3 : (NC <= 12 ? 2 : 1); }
 
-// FUSED = false: codes only.  FUSED = true: A x V by MFMA.  MULTI: V^T does
-// not fit one LDS stage.  PRE0: the I-Exp division needs no pre-shift.
-// NC = number of 32-key chunks exactly (32 (NC - 1) < Lk <= 32 NC): every
-// chunk but the last is full, so only the last one carries per-key masks.
-// DTMAX = 16-column output tiles, exactly dpad / 16.
-template <int NC, bool FUSED, bool MULTI, int DTMAX, bool PRE0>
+// ---------------------------------------------------------------------------
+// Per-tile steps shared by the kernels.  lg holds the logits of a lane's
+// keys; after tile_iexp it holds e (float path, as bits) or qL with z in zb
+// (integer path); masked keys hold 0 there.  NT = elements of the last chunk
+// that carry keys (4 with the half tail, else 8).
+// ---------------------------------------------------------------------------
+
+template <int NC>
+__device__ __forceinline__ int tile_max(const int (&lg)[NC][8]) {
+    int mx = INT_MIN;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+#pragma unroll
+        for (int t = 0; t < 8; t += 2) mx = max(mx, max(lg[c][t], lg[c][t + 1]));
+    }
+    mx = max(mx, __shfl_xor(mx, 16, 64));
+    mx = max(mx, __shfl_xor(mx, 32, 64));
+    return mx;
+}
+
+struct RowState {
+    double S2f;     // float path: 2S
+    RowSum rs;      // integer path
+};
+
+template <int NC, bool FP, int NT>
+__device__ __forceinline__ RowState tile_iexp(int (&lg)[NC][8], uint32_t (&zb)[NC][2],
+                                              const LisConsts& k) {
+    const int mx = tile_max<NC>(lg);
+    RowState st;
+    if constexpr (FP) {
+        double sum = 0.0;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+#pragma unroll
+            for (int t = 0; t < (c < NC - 1 ? 8 : NT); ++t) {
+                const int v = lg[c][t];
+                float e = iexp_f(v, mx, k);
+                if (c == NC - 1) e = v != INT_MIN ? e : 0.0f;
+                sum += (double)e;
+                lg[c][t] = __float_as_int(e);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        sum += __shfl_xor(sum, 16, 64);
+        sum += __shfl_xor(sum, 32, 64);
+        st.S2f = 2.0 * sum;
+    } else {
+        uint64_t sum = 0;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            zb[c][0] = zb[c][1] = 0;
+#pragma unroll
+            for (int t = 0; t < (c < NC - 1 ? 8 : NT); ++t) {
+                const int v = lg[c][t];
+                const uint32_t u = min((uint32_t)mx - (uint32_t)v, k.u_max);
+                const uint32_t z =
+                    (uint32_t)(((uint64_t)((u << k.pre) & 0xFFFFFFu) * (uint64_t)k.magic) >> 32);
+                const uint32_t w = __umul24(z, k.d_ln2) + (k.qb - u);
+                const uint32_t qL = __umul24(w, w) + k.qc;
+                const uint64_t e = (uint64_t)qL << (k.n - (int)z);
+                if (c < NC - 1) {
+                    sum += e;
+                    lg[c][t] = (int)qL;
+                } else {
+                    const bool valid = v != INT_MIN;
+                    sum += valid ? e : 0ull;
+                    lg[c][t] = valid ? (int)qL : 0;
+                }
+                zb[c][t >> 2] |= z << (8 * (t & 3));
+            }
+        }
+        st.rs = row_sum(sum, k);
+    }
+    return st;
+}
+
+// Codes of chunk c; in the last chunk masked keys (held as 0) get code 0 and
+// the entries past NT are 0.
+template <int NC, bool FP, int NT>
+__device__ __forceinline__ void chunk_codes(int (&code)[8], const int (&lg)[NC][8],
+                                            const uint32_t (&zb)[NC][2], const RowState& st,
+                                            const LisConsts& k, int c) {
+    const bool last = c == NC - 1;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+        if (last && t >= NT) {
+            code[t] = 0;
+            continue;
+        }
+        int cd;
+        if constexpr (FP) {
+            cd = code_f(__int_as_float(lg[c][t]), st.S2f, k.top);
+        } else {
+            const uint32_t z = (zb[c][t >> 2] >> (8 * (t & 3))) & 0xFFu;
+            cd = lis_code((uint32_t)lg[c][t], z, st.rs, k);
+        }
+        code[t] = (last && lg[c][t] == 0) ? 0 : cd;
+    }
+}
+
+// bf16 operand of P = 2^(N - code) for chunk c (masked keys 0), as four
+// dwords holding the pairs (t, t + 1).
+template <int NC, bool FP, int NT>
+__device__ __forceinline__ u32x4 chunk_pbits(const int (&lg)[NC][8], const uint32_t (&zb)[NC][2],
+                                             const RowState& st, const LisConsts& k, int c) {
+    const bool last = c == NC - 1;
+    const float ptop = (float)(1 << k.top);
+    float P[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+        if (last && t >= NT) {
+            P[t] = 0.0f;
+            continue;
+        }
+        int cd;
+        if constexpr (FP) {
+            cd = code_f(__int_as_float(lg[c][t]), st.S2f, k.top);
+        } else {
+            const uint32_t z = (zb[c][t >> 2] >> (8 * (t & 3))) & 0xFFu;
+            cd = lis_code((uint32_t)lg[c][t], z, st.rs, k);
+        }
+        const float p = __builtin_ldexpf(ptop, -cd);
+        P[t] = (last && lg[c][t] == 0) ? 0.0f : p;
+    }
+    return u32x4{bf16_pair(P[0], P[1]), bf16_pair(P[2], P[3]), bf16_pair(P[4], P[5]),
+                 bf16_pair(P[6], P[7])};
+}
+
+// acc[dt] += P x V^T for chunk c (cs: its index inside the current V^T stage).
+template <int DTMAX, bool HALFMMA>
+__device__ __forceinline__ void chunk_mfma(f32x4 (&acc)[DTMAX], u32x4 pb, const uint16_t* vt,
+                                           int ld, int cs, int r, int kg) {
+    if constexpr (HALFMMA) {
+        const i16x4 A = __builtin_bit_cast(i16x4, u32x2{pb.x, pb.y});
+#pragma unroll
+        for (int dt = 0; dt < DTMAX; ++dt) {
+            const u32x2 bv = *reinterpret_cast<const u32x2*>(vt + (16 * dt + r) * ld + 32 * cs + 8 * kg);
+            acc[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(A, __builtin_bit_cast(i16x4, bv),
+                                                                acc[dt], 0, 0, 0);
+        }
+    } else {
+        const bf16x8 A = __builtin_bit_cast(bf16x8, pb);
+#pragma unroll
+        for (int dt = 0; dt < DTMAX; ++dt) {
+            const u32x4 bv = *reinterpret_cast<const u32x4*>(vt + (16 * dt + r) * ld + 32 * cs + 8 * kg);
+            acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, __builtin_bit_cast(bf16x8, bv),
+                                                              acc[dt], 0, 0, 0);
+        }
+    }
+}
+
+// out[g][i0 + 4 kg + q][16 dt + r] = acc[dt][q]
+template <int DTMAX>
+__device__ __forceinline__ void store_out(const f32x4 (&acc)[DTMAX], const LisArgs& a, int64_t g,
+                                          int i0, int r, int kg) {
+#pragma unroll
+    for (int dt = 0; dt < DTMAX; ++dt) {
+        const int col = 16 * dt + r;
+        if (col >= a.d) continue;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int orow = i0 + 4 * kg + q;
+            if (orow < a.Lq) a.out[(g * a.Lq + orow) * (int64_t)a.d + col] = (int32_t)acc[dt][q];
+        }
+    }
+}
+
+// Row pointers of row i of unit g and whether its last chunk can be read with
+// full vectors (32 NC elements from the row start lie inside the tensors).
+struct RowPtrs {
+    const int32_t* row;
+    const int32_t* brow;
+    bool tail_vec;
+};
+
+template <int NC>
+__device__ __forceinline__ RowPtrs row_ptrs(const LisArgs& a, const LisLaunch& p, int64_t g, int i) {
+    RowPtrs rp;
+    const int64_t roff = (g * a.Lq + i) * (int64_t)a.Lk;
+    rp.row = a.logits + roff;
+    const int64_t boff = a.bias ? ((g % a.Hb) * a.Lq + i) * (int64_t)a.Lk : 0;
+    rp.brow = a.bias ? a.bias + boff : nullptr;
+    rp.tail_vec = roff + 32 * NC <= p.n_logits && (!rp.brow || boff + 32 * NC <= p.n_bias);
+    return rp;
+}
+
+// Loads chunks [C0, C1) of a lane's keys.
+template <int NC, bool HALF, int C0 = 0, int C1 = NC>
+__device__ __forceinline__ void tile_load(int (&lg)[NC][8], const RowPtrs& rp, int kg, int Lk) {
+#pragma unroll
+    for (int c = C0; c < C1; ++c) {
+        if (c < NC - 1) load_full(lg[c], rp.row, rp.brow, c, kg);
+        else load_chunk<HALF>(lg[NC - 1], rp.row, rp.brow, NC - 1, kg, Lk, rp.tail_vec);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Unit kernel: one workgroup per attention unit, V^T staged once (single
+// stage), each wavefront walks the unit's 16-row tiles w', w' + 4, ... and
+// prefetches its next tile's logits while it computes the current one.  The
+// wave with the extra tiles rotates with the unit so that the SIMDs of a CU
+// share the remainder.  Float path only.  HALF: the last chunk holds at most
+// 16 keys and is contracted by the 16x16x16 MFMA.
+// ---------------------------------------------------------------------------
+// Chunks of the next tile prefetched during the current one: as many as the
+// register budget of three wavefronts per SIMD allows.
+constexpr int unit_prefetch(int NC) { return NC < 4 ? NC : 4; }
+
+template <int NC, bool FUSED, int DTMAX, bool HALF>
+__device__ __forceinline__ void unit_tile(int (&cur)[NC][8], int (&nxt)[NC][8], const LisArgs& a,
+                                          const LisLaunch& p, const LisConsts& k, const uint16_t* vt,
+                                          int64_t g, int tile, int r, int kg) {
+    constexpr int NT = HALF ? 4 : 8;
+    constexpr int PF = unit_prefetch(NC);
+    const int i0 = 16 * tile;
+    // the chunks not prefetched
+    tile_load<NC, HALF, PF, NC>(cur, row_ptrs<NC>(a, p, g, min(i0 + r, a.Lq - 1)), kg, a.Lk);
+    uint32_t zb[NC][2];
+    const RowState st = tile_iexp<NC, true, NT>(cur, zb, k);
+    // Always prefetch (a conditional load would keep the stale buffer live
+    // across the loop); past the last tile the current rows, still in cache,
+    // are read again.
+    const int nt = tile + 4 < p.ntiles ? tile + 4 : tile;
+    tile_load<NC, HALF, 0, PF>(nxt, row_ptrs<NC>(a, p, g, min(16 * nt + r, a.Lq - 1)), kg, a.Lk);
+    if constexpr (FUSED) {
+        f32x4 acc[DTMAX];
+#pragma unroll
+        for (int dt = 0; dt < DTMAX; ++dt) acc[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            const u32x4 pb = chunk_pbits<NC, true, NT>(cur, zb, st, k, c);
+            if (HALF && c == NC - 1)
+                chunk_mfma<DTMAX, true>(acc, pb, vt, p.ld, c, r, kg);
+            else
+                chunk_mfma<DTMAX, false>(acc, pb, vt, p.ld, c, r, kg);
+            // keep each chunk's V^T reads next to its MFMAs (hoisting them all
+            // would take 4 DTMAX registers per chunk)
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        store_out<DTMAX>(acc, a, g, i0, r, kg);
+    } else {
+        const int i = i0 + r;
+        uint8_t* crow = a.codes + (g * a.Lq + min(i, a.Lq - 1)) * (int64_t)a.ld_codes;
+        const int nbytes = (a.Lk + 1) >> 1;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            int code[8];
+            chunk_codes<NC, true, NT>(code, cur, zb, st, k, c);
+            if (i < a.Lq) store_codes(crow, nbytes, c, kg, code);
+        }
+    }
+}
+
+template <int NC, bool FUSED, int DTMAX, bool HALF>
+__global__ __launch_bounds__(kBlock, 3) void lis_unit_kernel(LisArgs a, LisLaunch p) {
+    extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+    uint16_t* vt = reinterpret_cast<uint16_t*>(smem);
+    const int64_t g = blockIdx.x;
+    const int wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const int r = lane & 15;
+    const int kg = lane >> 4;
+
+    LisConsts k = a.k;
+    k.u_max &= 0xFFFFFFu;
+
+    StageRegs sr;
+    if constexpr (FUSED)
+        stage_load(sr, a.v + g * (int64_t)a.Lk * a.d, a.Lk, a.d, DTMAX, 0, 32 * NC, p.vec_ok);
+
+    int bufA[NC][8], bufB[NC][8];
+    int tile = (wave + (int)(g & 3)) & 3;
+    if (tile < p.ntiles)
+        tile_load<NC, HALF, 0, unit_prefetch(NC)>(
+            bufA, row_ptrs<NC>(a, p, g, min(16 * tile + r, a.Lq - 1)), kg, a.Lk);
+    if constexpr (FUSED) {
+        stage_store(sr, vt, p.ld, DTMAX, 32 * NC, a.zp_v);
+        __syncthreads();
+    }
+    while (tile < p.ntiles) {
+        unit_tile<NC, FUSED, DTMAX, HALF>(bufA, bufB, a, p, k, vt, g, tile, r, kg);
+        tile += 4;
+        if (tile >= p.ntiles) break;
+        unit_tile<NC, FUSED, DTMAX, HALF>(bufB, bufA, a, p, k, vt, g, tile, r, kg);
+        tile += 4;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Tile kernel: a workgroup of four wavefronts owns one unit g and 64
+// consecutive query rows.  FUSED = false: codes only.  FUSED = true: A x V by
+// MFMA.  MULTI: V^T does not fit one LDS stage and is staged chunk range by
+// chunk range.  FP: float path.  NC = number of 32-key chunks exactly
+// (32 (NC - 1) < Lk <= 32 NC): every chunk but the last is full, so only the
+// last one carries per-key masks.  DTMAX = 16-column output tiles, exactly
+// dpad / 16.
+// ---------------------------------------------------------------------------
+template <int NC, bool FUSED, bool MULTI, int DTMAX, bool FP>
 __global__ __launch_bounds__(kBlock, lis_waves_per_simd(NC)) void lis_kernel(LisArgs a,
                                                                             LisLaunch p) {
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
@@ -289,63 +653,19 @@ __global__ __launch_bounds__(kBlock, lis_waves_per_simd(NC)) void lis_kernel(Lis
     k.u_max &= 0xFFFFFFu;
 
     const int i = min(i0 + r, a.Lq - 1);
-    const int64_t roff = (g * a.Lq + i) * (int64_t)Lk;
-    const int32_t* row = a.logits + roff;
-    const int64_t boff = a.bias ? ((g % a.Hb) * a.Lq + i) * (int64_t)Lk : 0;
-    const int32_t* brow = a.bias ? a.bias + boff : nullptr;
     const int8_t* vg = FUSED ? a.v + g * (int64_t)Lk * a.d : nullptr;
-    const bool tail_vec = roff + 32 * NC <= p.n_logits && (!brow || boff + 32 * NC <= p.n_bias);
 
     StageRegs sr;
     if (FUSED) stage_load(sr, vg, Lk, a.d, p.ncg, 0, min(p.kb, NC * 32), p.vec_ok);
 
     int lg[NC][8];
-#pragma unroll
-    for (int c = 0; c < NC - 1; ++c) load_full(lg[c], row, brow, c, kg);
-    load_chunk(lg[NC - 1], row, brow, NC - 1, kg, Lk, tail_vec);
+    tile_load<NC, false>(lg, row_ptrs<NC>(a, p, g, i), kg, Lk);
 
     if (FUSED) stage_store(sr, vt, p.ld, p.ncg, min(p.kb, NC * 32), a.zp_v);
 
     uint32_t zb[NC][2];
-    RowSum rs;
-    if (active || MULTI) {
-        // row maximum (masked keys hold INT_MIN)
-        int mx = INT_MIN;
-#pragma unroll
-        for (int c = 0; c < NC; ++c) {
-#pragma unroll
-            for (int t = 0; t < 8; t += 2) mx = max(mx, max(lg[c][t], lg[c][t + 1]));
-        }
-        mx = max(mx, __shfl_xor(mx, 16, 64));
-        mx = max(mx, __shfl_xor(mx, 32, 64));
-
-        // I-Exp (Algorithm 1): lg <- qL (0 for masked keys), zb <- z bytes; row sum of e.
-        uint64_t sum = 0;
-#pragma unroll
-        for (int c = 0; c < NC; ++c) {
-            zb[c][0] = zb[c][1] = 0;
-#pragma unroll
-            for (int t = 0; t < 8; ++t) {
-                const int v = lg[c][t];
-                const uint32_t u = min((uint32_t)mx - (uint32_t)v, k.u_max);
-                const uint32_t up = PRE0 ? u : ((u << k.pre) & 0xFFFFFFu);
-                const uint32_t z = (uint32_t)(((uint64_t)up * (uint64_t)k.magic) >> 32);
-                const uint32_t w = __umul24(z, k.d_ln2) + (k.qb - u);
-                const uint32_t qL = __umul24(w, w) + k.qc;
-                const uint64_t e = (uint64_t)qL << (k.n - (int)z);
-                if (c < NC - 1) {
-                    sum += e;
-                    lg[c][t] = (int)qL;
-                } else {
-                    const bool valid = v != INT_MIN;
-                    sum += valid ? e : 0ull;
-                    lg[c][t] = valid ? (int)qL : 0;
-                }
-                zb[c][t >> 2] |= z << (8 * (t & 3));
-            }
-        }
-        rs = row_sum(sum, k);
-    }
+    RowState st;
+    if (active || MULTI) st = tile_iexp<NC, FP, 8>(lg, zb, k);
     if (FUSED) __syncthreads();   // V^T is visible
     if (!MULTI && !active) return;
 
@@ -357,7 +677,6 @@ __global__ __launch_bounds__(kBlock, lis_waves_per_simd(NC)) void lis_kernel(Lis
 #pragma unroll
         for (int dt = 0; dt < DTMAX; ++dt) acc[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-    const uint32_t ptop = (uint32_t)((127 + k.top) << 7);
     const int cps = p.kb >> 5;  // chunks per V^T stage
 
 #pragma unroll
@@ -373,89 +692,74 @@ __global__ __launch_bounds__(kBlock, lis_waves_per_simd(NC)) void lis_kernel(Lis
                 __syncthreads();
             }
         }
-        int code[8];
-        uint32_t pbits[8];
-#pragma unroll
-        for (int t = 0; t < 8; ++t) {
-            const uint32_t qL = (uint32_t)lg[c][t];
-            const uint32_t z = (zb[c][t >> 2] >> (8 * (t & 3))) & 0xFFu;
-            const int cd = lis_code(qL, z, rs, k);
-            const uint32_t pb = ptop - ((uint32_t)cd << 7);
-            if (c < NC - 1) {
-                code[t] = cd;
-                pbits[t] = pb;
-            } else {
-                const bool valid = qL != 0;
-                code[t] = valid ? cd : 0;
-                pbits[t] = valid ? pb : 0u;
-            }
-        }
-        if (!FUSED && row_ok) store_codes(crow, nbytes, c, kg, code);
         if (FUSED) {
-            u32x4 av;
-            av.x = pbits[0] | (pbits[1] << 16);
-            av.y = pbits[2] | (pbits[3] << 16);
-            av.z = pbits[4] | (pbits[5] << 16);
-            av.w = pbits[6] | (pbits[7] << 16);
-            const bf16x8 A = __builtin_bit_cast(bf16x8, av);
-#pragma unroll
-            for (int dt = 0; dt < DTMAX; ++dt) {
-                const u32x4 bv = *reinterpret_cast<const u32x4*>(
-                    vt + (16 * dt + r) * p.ld + 32 * cs + 8 * kg);
-                acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, __builtin_bit_cast(bf16x8, bv),
-                                                                  acc[dt], 0, 0, 0);
-            }
+            const u32x4 pb = chunk_pbits<NC, FP, 8>(lg, zb, st, k, c);
+            chunk_mfma<DTMAX, false>(acc, pb, vt, p.ld, cs, r, kg);
+            __builtin_amdgcn_sched_barrier(0);
+        } else {
+            int code[8];
+            chunk_codes<NC, FP, 8>(code, lg, zb, st, k, c);
+            if (row_ok) store_codes(crow, nbytes, c, kg, code);
         }
     }
 
-    if (FUSED && active) {
-        // acc[dt][q] = out[row i0 + 4 kg + q][col 16 dt + r]
-#pragma unroll
-        for (int dt = 0; dt < DTMAX; ++dt) {
-            const int col = 16 * dt + r;
-            if (col >= a.d) continue;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int orow = i0 + 4 * kg + q;
-                if (orow < a.Lq)
-                    a.out[(g * a.Lq + orow) * (int64_t)a.d + col] = (int32_t)acc[dt][q];
-            }
-        }
-    }
+    if (FUSED && active) store_out<DTMAX>(acc, a, g, i0, r, kg);
 }
 
-// Launch of the register kernel for exactly NC chunks; the host has checked
-// that dtm is 2 or 4 for fused calls (d <= 64) and set multi when V^T needs
-// more than one LDS stage.
+// Launch of the tile kernel for exactly NC chunks; the host has checked that
+// dtm is 2 or 4 for fused calls (d <= 64).  MULTI follows from NC and dtm.
 template <int NC>
-hipError_t launch_lis_nc(bool fused, bool multi, int dtm, bool pre0, const LisArgs& a,
-                         const LisLaunch& p, dim3 grid, size_t lds, hipStream_t s) {
-#define FQ_LIS(FUSED, MULTI, DTM, PRE0) \
-    hipLaunchKernelGGL((lis_kernel<NC, FUSED, MULTI, DTM, PRE0>), grid, dim3(kBlock), lds, s, a, p)
+hipError_t launch_lis_nc(bool fused, int dtm, bool fp, const LisArgs& a, const LisLaunch& p,
+                         dim3 grid, size_t lds, hipStream_t s) {
+#define FQ_LIS(FUSED, MULTI, DTM, FP) \
+    launch_kernel(lis_kernel<NC, FUSED, MULTI, DTM, FP>, grid, dim3(kBlock), lds, s, a, p)
     constexpr bool kMulti2 = NC * 32 > vt_stage_keys(32);
     constexpr bool kMulti4 = NC * 32 > vt_stage_keys(64);
     if (!fused) {
-        FQ_LIS(false, false, 1, false);
+        if (fp) FQ_LIS(false, false, 1, true);
+        else FQ_LIS(false, false, 1, false);
     } else if (dtm == 2) {
-        if (pre0) FQ_LIS(true, kMulti2, 2, true);
+        if (fp) FQ_LIS(true, kMulti2, 2, true);
         else FQ_LIS(true, kMulti2, 2, false);
     } else {
-        if (pre0) FQ_LIS(true, kMulti4, 4, true);
+        if (fp) FQ_LIS(true, kMulti4, 4, true);
         else FQ_LIS(true, kMulti4, 4, false);
     }
 #undef FQ_LIS
-    (void)multi;
     return hipGetLastError();
 }
 
-// Register-kernel launchers, instantiated per chunk count in lis_inst_lo.hip
-// (1..10 chunks) and lis_inst_hi.hip (11..20 chunks).
-hipError_t launch_lis_regs_lo(int nc, bool fused, bool multi, int dtm, bool pre0,
-                              const LisArgs& a, const LisLaunch& p, dim3 grid, size_t lds,
-                              hipStream_t stream);
-hipError_t launch_lis_regs_hi(int nc, bool fused, bool multi, int dtm, bool pre0,
-                              const LisArgs& a, const LisLaunch& p, dim3 grid, size_t lds,
-                              hipStream_t stream);
+// Launch of the unit kernel for exactly NC chunks (NC <= kUnitMaxNC).
+constexpr int kUnitMaxNC = 7;
+
+template <int NC>
+hipError_t launch_unit_nc(bool fused, int dtm, bool half, const LisArgs& a, const LisLaunch& p,
+                          size_t lds, hipStream_t s) {
+#define FQ_UNIT(FUSED, DTM, HALF)                                                           \
+    launch_kernel(lis_unit_kernel<NC, FUSED, DTM, HALF>, dim3((unsigned)a.G), dim3(kBlock), \
+                  lds, s, a, p)
+    if (!fused) {
+        if (half) FQ_UNIT(false, 1, true);
+        else FQ_UNIT(false, 1, false);
+    } else if (dtm == 2) {
+        if (half) FQ_UNIT(true, 2, true);
+        else FQ_UNIT(true, 2, false);
+    } else {
+        if (half) FQ_UNIT(true, 4, true);
+        else FQ_UNIT(true, 4, false);
+    }
+#undef FQ_UNIT
+    return hipGetLastError();
+}
+
+// Per chunk-count launchers, instantiated in lis_inst_lo.hip (1..10 chunks),
+// lis_inst_hi.hip (11..20 chunks) and lis_inst_unit.hip (unit kernel, 1..7).
+hipError_t launch_lis_regs_lo(int nc, bool fused, int dtm, bool fp, const LisArgs& a,
+                              const LisLaunch& p, dim3 grid, size_t lds, hipStream_t stream);
+hipError_t launch_lis_regs_hi(int nc, bool fused, int dtm, bool fp, const LisArgs& a,
+                              const LisLaunch& p, dim3 grid, size_t lds, hipStream_t stream);
+hipError_t launch_lis_unit(int nc, bool fused, int dtm, bool half, const LisArgs& a,
+                           const LisLaunch& p, size_t lds, hipStream_t stream);
 
 }  // namespace lis
 }  // namespace fqvit

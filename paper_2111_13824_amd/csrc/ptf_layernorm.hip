@@ -301,10 +301,10 @@ hipError_t launch_fast(const LnArgs& a, int lshift, bool wide, hipStream_t strea
     const int64_t blocks = std::min<int64_t>((waves + 3) / 4, 1024);
     const size_t lds = (size_t)a.C * (2 * sizeof(double) + sizeof(int));
     if (wide)
-        hipLaunchKernelGGL((ln_fast_kernel<W, true>), dim3((unsigned)blocks), dim3(kBlock), lds,
+        launch_kernel(ln_fast_kernel<W, true>, dim3((unsigned)blocks), dim3(kBlock), lds,
                            stream, a, lshift);
     else
-        hipLaunchKernelGGL((ln_fast_kernel<W, false>), dim3((unsigned)blocks), dim3(kBlock), lds,
+        launch_kernel(ln_fast_kernel<W, false>, dim3((unsigned)blocks), dim3(kBlock), lds,
                            stream, a, lshift);
     return hipGetLastError();
 }
@@ -329,7 +329,7 @@ hipError_t launch_ptf_layernorm(const LnArgs& a, hipStream_t stream) {
     }
     if (best_l < 0) {
         const int64_t blocks = std::min<int64_t>((a.T + 3) / 4, 2048);
-        hipLaunchKernelGGL(ln_generic_kernel, dim3((unsigned)blocks), dim3(kBlock), 0, stream, a);
+        launch_kernel(ln_generic_kernel, dim3((unsigned)blocks), dim3(kBlock), 0, stream, a);
         return hipGetLastError();
     }
     // Per-lane sums of squares: 4W values of at most (255 * 2^K)^2 each.

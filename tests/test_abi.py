@@ -32,12 +32,23 @@ def lib():
 def test_header_symbols_exported(lib):
     names = _declared_functions()
     assert set(names) >= {"ptf_layernorm_int8", "lis_softmax_log4", "lis_attn_v_shift",
-                          "lis_attention_head", "fq_status_str", "fq_version"}
+                          "lis_attention_head", "fq_status_str", "fq_version",
+                          "fq_time_next_call"}
     for n in names:
         assert hasattr(lib, n), f"{n} declared in fqvit.h but not exported"
     # the binding exposes the compute entry points under the same names
     for n in B.SIGNATURES:
         assert n in names
+
+
+def test_time_next_call_is_host_only(lib):
+    # setting and clearing the events touches no HIP state; a call that fails
+    # validation consumes them without enqueueing anything
+    assert lib.fq_time_next_call(None, None) == 0
+    assert lib.fq_time_next_call(ctypes.c_void_p(16), ctypes.c_void_p(32)) == 0
+    assert lib.ptf_layernorm_int8(None, 4, 0, 0, None, 3, None, None, ctypes.c_float(1.0), 0, 8,
+                                  None, None) == 2
+    assert lib.fq_time_next_call(None, None) == 0
 
 
 def test_status_strings(lib):
