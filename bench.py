@@ -81,13 +81,19 @@ def pmc_summary(fetch_dir, write_dir):
                 rows += [r for r in csv.DictReader(f) if r["Counter_Name"] == counter]
         rows.sort(key=lambda r: int(r["Dispatch_Id"]))
         groups = {"head": [], "ln": [], "copy": []}
-        last_head = max((int(r["Dispatch_Id"]) for r in rows if "lis_kernel" in r["Kernel_Name"]),
+        def is_head(name):
+            return "fqvit::lis::" in name
+
+        def is_ln(name):
+            return "fqvit::" in name and "ln_" in name
+
+        last_head = max((int(r["Dispatch_Id"]) for r in rows if is_head(r["Kernel_Name"])),
                         default=-1)
         for r in rows:
             name, v = r["Kernel_Name"], float(r["Counter_Value"])
-            if "lis_kernel" in name:
+            if is_head(name):
                 groups["head"].append(v)
-            elif "ln_" in name:
+            elif is_ln(name):
                 groups["ln"].append(v)
             elif "copy" in name.lower() and int(r["Dispatch_Id"]) > last_head:
                 groups["copy"].append(v)

@@ -211,6 +211,9 @@ hipError_t launch_lis(const LisArgs& a, hipStream_t stream) {
     p.ld = p.kb + 8;
     p.vec_ok = fused && (a.d % 16 == 0) && ((reinterpret_cast<uintptr_t>(a.v) & 15) == 0);
     p.vt_bytes = fused ? p.dpad * p.ld * (int)sizeof(uint16_t) : 0;
+    p.out_vec = fused && (a.d % 4 == 0) && ((reinterpret_cast<uintptr_t>(a.out) & 15) == 0);
+    // LDS of the row-wise output stores: one 16 x (dpad + 4) int32 block per wavefront
+    const size_t out_lds = p.out_vec ? (size_t)4 * 16 * (p.dpad + 4) * sizeof(int32_t) : 0;
     p.n_logits = a.G * (int64_t)a.Lq * a.Lk;
     p.n_bias = a.bias ? (int64_t)a.Hb * a.Lq * a.Lk : 0;
     const int64_t blocks = a.G * (int64_t)p.ntiles;
@@ -228,13 +231,13 @@ hipError_t launch_lis(const LisArgs& a, hipStream_t stream) {
         u.ld = u.kb + 8;
         u.vt_bytes = fused ? u.dpad * u.ld * (int)sizeof(uint16_t) : 0;
         const bool half = a.Lk - 32 * (nc - 1) <= 16;
-        return launch_lis_unit(nc, fused, dt, half, a, u, (size_t)u.vt_bytes, stream);
+        return launch_lis_unit(nc, fused, dt, half, a, u, (size_t)u.vt_bytes + out_lds, stream);
     }
     // Tile kernels for rows of up to 640 keys: codes only, or the fused product
     // without a codes output and with d <= 64.
     const bool regs = nc <= 20 && (!fused || (a.codes == nullptr && dt <= 4));
     if (regs) {
-        const size_t lds = (size_t)p.vt_bytes;
+        const size_t lds = (size_t)p.vt_bytes + out_lds;
         return nc <= 10 ? launch_lis_regs_lo(nc, fused, dt, fp, a, p, grid, lds, stream)
                         : launch_lis_regs_hi(nc, fused, dt, fp, a, p, grid, lds, stream);
     }

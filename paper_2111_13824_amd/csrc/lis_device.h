@@ -250,6 +250,7 @@ struct LisLaunch {
     int ncg;        // dpad / 16: 16-column groups of V
     int vec_ok;     // V rows read as 16-byte vectors (d % 16 == 0, 16-byte aligned V)
     int vt_bytes;   // LDS bytes of one V^T stage (0 for codes only)
+    int out_vec;    // output rows written through LDS as 16-byte units (d % 4 == 0, aligned out)
     int64_t n_logits;  // elements of the logits tensor (G Lq Lk)
     int64_t n_bias;    // elements of the bias tensor (Hb Lq Lk), 0 without bias
 };
@@ -319,8 +320,13 @@ __device__ __forceinline__ float iexp_f(int v, int mx, const LisConsts& k) {
     return __builtin_ldexpf(qL, k.f_sK - __float_as_int(zb));
 }
 
-// Code of one key from e and 2S (binary64, exact).
-__device__ __forceinline__ int code_f(float e, double S2, int top) {
+// Code of one key from e (its binary32 bit pattern) and 2S (binary64, exact).
+// The empty asm hides the pattern's origin so that the compiler converts it to
+// binary64 here rather than keeping the conversions of the I-Exp pass (two
+// registers per key) alive across both passes.
+__device__ __forceinline__ int code_f(int ebits, double S2, int top) {
+    asm volatile("" : "+v"(ebits));
+    const float e = __int_as_float(ebits);
     const double ed = (double)e;
     const double X = S2 + ed;
     const double Y = ed * 1.5;
@@ -363,7 +369,10 @@ __device__ __forceinline__ RowState tile_iexp(int (&lg)[NC][8], uint32_t (&zb)[N
     const int mx = tile_max<NC>(lg);
     RowState st;
     if constexpr (FP) {
-        double sum = 0.0;
+        // Four partial sums: every partial sum is an integer below 2^53, so the
+        // binary64 additions are exact in any order (one serial chain would
+        // make the scheduler hold every converted term in registers).
+        double part[4] = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
 #pragma unroll
@@ -371,11 +380,12 @@ __device__ __forceinline__ RowState tile_iexp(int (&lg)[NC][8], uint32_t (&zb)[N
                 const int v = lg[c][t];
                 float e = iexp_f(v, mx, k);
                 if (c == NC - 1) e = v != INT_MIN ? e : 0.0f;
-                sum += (double)e;
+                part[t & 3] += (double)e;
                 lg[c][t] = __float_as_int(e);
             }
             __builtin_amdgcn_sched_barrier(0);
         }
+        double sum = (part[0] + part[1]) + (part[2] + part[3]);
         sum += __shfl_xor(sum, 16, 64);
         sum += __shfl_xor(sum, 32, 64);
         st.S2f = 2.0 * sum;
@@ -424,7 +434,7 @@ __device__ __forceinline__ void chunk_codes(int (&code)[8], const int (&lg)[NC][
         }
         int cd;
         if constexpr (FP) {
-            cd = code_f(__int_as_float(lg[c][t]), st.S2f, k.top);
+            cd = code_f(lg[c][t], st.S2f, k.top);
         } else {
             const uint32_t z = (zb[c][t >> 2] >> (8 * (t & 3))) & 0xFFu;
             cd = lis_code((uint32_t)lg[c][t], z, st.rs, k);
@@ -449,13 +459,16 @@ __device__ __forceinline__ u32x4 chunk_pbits(const int (&lg)[NC][8], const uint3
         }
         int cd;
         if constexpr (FP) {
-            cd = code_f(__int_as_float(lg[c][t]), st.S2f, k.top);
+            cd = code_f(lg[c][t], st.S2f, k.top);
         } else {
             const uint32_t z = (zb[c][t >> 2] >> (8 * (t & 3))) & 0xFFu;
             cd = lis_code((uint32_t)lg[c][t], z, st.rs, k);
         }
         const float p = __builtin_ldexpf(ptop, -cd);
         P[t] = (last && lg[c][t] == 0) ? 0.0f : p;
+        // two keys at a time: interleaving all eight would hold about six
+        // registers of binary64 temporaries per key
+        if (t & 1) __builtin_amdgcn_sched_barrier(0);
     }
     return u32x4{bf16_pair(P[0], P[1]), bf16_pair(P[2], P[3]), bf16_pair(P[4], P[5]),
                  bf16_pair(P[6], P[7])};
@@ -500,6 +513,38 @@ __device__ __forceinline__ void store_out(const f32x4 (&acc)[DTMAX], const LisAr
     }
 }
 
+// The same tile written through LDS: the wavefront's 16 x dpad block goes to
+// its own LDS region ot (16 rows of 16 DTMAX + 4 dwords; the 4-dword pad makes
+// the scattered writes conflict-free), then each store instruction writes
+// whole output rows as 16-byte units, the tile being one contiguous range of
+// out.  Needs d % 4 == 0 and a 16-byte aligned out.
+template <int DTMAX>
+constexpr int out_lds_dwords() { return 16 * (16 * DTMAX + 4); }
+
+template <int DTMAX>
+__device__ __forceinline__ void store_out_rows(const f32x4 (&acc)[DTMAX], int32_t* ot,
+                                               const LisArgs& a, int64_t g, int i0, int lane,
+                                               int r, int kg) {
+    constexpr int LDO = 16 * DTMAX + 4;
+    constexpr int UPR = 4 * DTMAX;    // 16-byte units per row
+#pragma unroll
+    for (int dt = 0; dt < DTMAX; ++dt) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) ot[(4 * kg + q) * LDO + 16 * dt + r] = (int32_t)acc[dt][q];
+    }
+#pragma unroll
+    for (int j = 0; j < UPR / 4; ++j) {
+        const int u = lane + 64 * j;
+        const int row = u / UPR;
+        const int c4 = u - row * UPR;
+        const int orow = i0 + row;
+        typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+        const i32x4 v = *reinterpret_cast<const i32x4*>(ot + row * LDO + 4 * c4);
+        if (orow < a.Lq && 4 * c4 < a.d)
+            *reinterpret_cast<i32x4*>(a.out + (g * a.Lq + orow) * (int64_t)a.d + 4 * c4) = v;
+    }
+}
+
 // Row pointers of row i of unit g and whether its last chunk can be read with
 // full vectors (32 NC elements from the row start lie inside the tensors).
 struct RowPtrs {
@@ -537,26 +582,37 @@ __device__ __forceinline__ void tile_load(int (&lg)[NC][8], const RowPtrs& rp, i
 // share the remainder.  Float path only.  HALF: the last chunk holds at most
 // 16 keys and is contracted by the 16x16x16 MFMA.
 // ---------------------------------------------------------------------------
-// Chunks of the next tile prefetched during the current one: as many as the
-// register budget of three wavefronts per SIMD allows.
-constexpr int unit_prefetch(int NC) { return NC < 4 ? NC : 4; }
+// Prefetch of the next tile: its first PF chunks are requested right after
+// the I-Exp pass of the current tile, and chunk PF + c right after chunk c of
+// the current tile has gone through its MFMA (its registers are free by then),
+// so the next tile is in flight without holding two tiles in registers.
+// Measured on the ViT-B/16 shapes, PF = 0, 4 and 7 run equally fast and
+// requesting the next tile before the I-Exp pass is slower; PF = 0 needs the
+// fewest registers.
+constexpr int unit_prefetch(int NC) { return NC < 0 ? NC : 0; }
+
+template <int NC, bool HALF>
+__device__ __forceinline__ void load_one_chunk(int (&lg)[NC][8], const RowPtrs& rp, int c, int kg,
+                                               int Lk) {
+    if (c < NC - 1) load_full(lg[c], rp.row, rp.brow, c, kg);
+    else load_chunk<HALF>(lg[NC - 1], rp.row, rp.brow, NC - 1, kg, Lk, rp.tail_vec);
+}
 
 template <int NC, bool FUSED, int DTMAX, bool HALF>
 __device__ __forceinline__ void unit_tile(int (&cur)[NC][8], int (&nxt)[NC][8], const LisArgs& a,
                                           const LisLaunch& p, const LisConsts& k, const uint16_t* vt,
-                                          int64_t g, int tile, int r, int kg) {
+                                          int32_t* ot, int64_t g, int tile, int lane, int r, int kg) {
     constexpr int NT = HALF ? 4 : 8;
     constexpr int PF = unit_prefetch(NC);
     const int i0 = 16 * tile;
-    // the chunks not prefetched
-    tile_load<NC, HALF, PF, NC>(cur, row_ptrs<NC>(a, p, g, min(i0 + r, a.Lq - 1)), kg, a.Lk);
-    uint32_t zb[NC][2];
-    const RowState st = tile_iexp<NC, true, NT>(cur, zb, k);
     // Always prefetch (a conditional load would keep the stale buffer live
     // across the loop); past the last tile the current rows, still in cache,
     // are read again.
     const int nt = tile + 4 < p.ntiles ? tile + 4 : tile;
-    tile_load<NC, HALF, 0, PF>(nxt, row_ptrs<NC>(a, p, g, min(16 * nt + r, a.Lq - 1)), kg, a.Lk);
+    const RowPtrs rn = row_ptrs<NC>(a, p, g, min(16 * nt + r, a.Lq - 1));
+    uint32_t zb[NC][2];
+    const RowState st = tile_iexp<NC, true, NT>(cur, zb, k);
+    tile_load<NC, HALF, 0, PF>(nxt, rn, kg, a.Lk);
     if constexpr (FUSED) {
         f32x4 acc[DTMAX];
 #pragma unroll
@@ -568,11 +624,13 @@ __device__ __forceinline__ void unit_tile(int (&cur)[NC][8], int (&nxt)[NC][8], 
                 chunk_mfma<DTMAX, true>(acc, pb, vt, p.ld, c, r, kg);
             else
                 chunk_mfma<DTMAX, false>(acc, pb, vt, p.ld, c, r, kg);
+            if (PF + c < NC) load_one_chunk<NC, HALF>(nxt, rn, PF + c, kg, a.Lk);
             // keep each chunk's V^T reads next to its MFMAs (hoisting them all
             // would take 4 DTMAX registers per chunk)
             __builtin_amdgcn_sched_barrier(0);
         }
-        store_out<DTMAX>(acc, a, g, i0, r, kg);
+        if (p.out_vec) store_out_rows<DTMAX>(acc, ot, a, g, i0, lane, r, kg);
+        else store_out<DTMAX>(acc, a, g, i0, r, kg);
     } else {
         const int i = i0 + r;
         uint8_t* crow = a.codes + (g * a.Lq + min(i, a.Lq - 1)) * (int64_t)a.ld_codes;
@@ -582,6 +640,8 @@ __device__ __forceinline__ void unit_tile(int (&cur)[NC][8], int (&nxt)[NC][8], 
             int code[8];
             chunk_codes<NC, true, NT>(code, cur, zb, st, k, c);
             if (i < a.Lq) store_codes(crow, nbytes, c, kg, code);
+            if (PF + c < NC) load_one_chunk<NC, HALF>(nxt, rn, PF + c, kg, a.Lk);
+            __builtin_amdgcn_sched_barrier(0);
         }
     }
 }
@@ -606,17 +666,17 @@ __global__ __launch_bounds__(kBlock, 3) void lis_unit_kernel(LisArgs a, LisLaunc
     int bufA[NC][8], bufB[NC][8];
     int tile = (wave + (int)(g & 3)) & 3;
     if (tile < p.ntiles)
-        tile_load<NC, HALF, 0, unit_prefetch(NC)>(
-            bufA, row_ptrs<NC>(a, p, g, min(16 * tile + r, a.Lq - 1)), kg, a.Lk);
+        tile_load<NC, HALF>(bufA, row_ptrs<NC>(a, p, g, min(16 * tile + r, a.Lq - 1)), kg, a.Lk);
     if constexpr (FUSED) {
         stage_store(sr, vt, p.ld, DTMAX, 32 * NC, a.zp_v);
         __syncthreads();
     }
+    int32_t* ot = reinterpret_cast<int32_t*>(smem + p.vt_bytes) + wave * out_lds_dwords<DTMAX>();
     while (tile < p.ntiles) {
-        unit_tile<NC, FUSED, DTMAX, HALF>(bufA, bufB, a, p, k, vt, g, tile, r, kg);
+        unit_tile<NC, FUSED, DTMAX, HALF>(bufA, bufB, a, p, k, vt, ot, g, tile, lane, r, kg);
         tile += 4;
         if (tile >= p.ntiles) break;
-        unit_tile<NC, FUSED, DTMAX, HALF>(bufB, bufA, a, p, k, vt, g, tile, r, kg);
+        unit_tile<NC, FUSED, DTMAX, HALF>(bufB, bufA, a, p, k, vt, ot, g, tile, lane, r, kg);
         tile += 4;
     }
 }
@@ -703,7 +763,14 @@ __global__ __launch_bounds__(kBlock, lis_waves_per_simd(NC)) void lis_kernel(Lis
         }
     }
 
-    if (FUSED && active) store_out<DTMAX>(acc, a, g, i0, r, kg);
+    if (FUSED && active) {
+        int32_t* ot = reinterpret_cast<int32_t*>(smem + p.vt_bytes) + wave * out_lds_dwords<DTMAX>();
+        if (p.out_vec) {
+            store_out_rows<DTMAX>(acc, ot, a, g, i0, lane, r, kg);
+        } else {
+            store_out<DTMAX>(acc, a, g, i0, r, kg);
+        }
+    }
 }
 
 // Launch of the tile kernel for exactly NC chunks; the host has checked that
