@@ -107,22 +107,51 @@ def _check(fn: str, status: int) -> None:
         raise FqError(fn, status)
 
 
+class Prepared:
+    """A validated call with its arguments already converted to C types:
+    calling it only enters the library (for launch loops where Python
+    marshalling would otherwise dominate).  The stream is the one current when
+    the call was prepared; the tensors are kept alive by the object."""
+
+    __slots__ = ("_name", "_fn", "_args", "_keep")
+
+    def __init__(self, name: str, args, keep):
+        self._name = name
+        self._fn = getattr(lib(), name)
+        self._args = tuple(t(a) if a is not None else None
+                           for t, a in zip(SIGNATURES[name], args))
+        self._keep = keep
+
+    def __call__(self) -> None:
+        st = self._fn(*self._args)
+        if st != FQ_OK:
+            raise FqError(self._name, st)
+
+
+def _invoke(name: str, args, keep, prepare: bool, result):
+    """Run the entry point now, or return it prepared for repeated calls."""
+    if prepare:
+        return Prepared(name, args, keep)
+    _check(name, getattr(lib(), name)(*args))
+    return result
+
+
 def ptf_layernorm_int8(x_q, zp_in: int, alpha, K: int, gamma, beta, s_out: float, zp_out: int,
-                       bits: int = 8, y_q=None, stream=None):
-    """PTF LayerNorm of an int8 [T, C] tensor; returns (or fills) int8 [T, C]."""
+                       bits: int = 8, y_q=None, stream=None, prepare: bool = False):
+    """PTF LayerNorm of an int8 [T, C] tensor; returns (or fills) int8 [T, C].
+    With prepare=True returns a Prepared call instead of running it."""
     import torch
     T, C = x_q.shape
     if y_q is None:
         y_q = torch.empty_like(x_q)
     if alpha.shape != (C,) or gamma.shape != (C,) or beta.shape != (C,) or y_q.shape != (T, C):
         raise ValueError("alpha, gamma, beta must be [C] and y_q [T, C]")
-    st = lib().ptf_layernorm_int8(_dev_ptr(x_q, torch.int8, "x_q", 2), T, C, zp_in,
-                                  _dev_ptr(alpha, torch.uint8, "alpha", 1), K,
-                                  _dev_ptr(gamma, torch.float32, "gamma", 1),
-                                  _dev_ptr(beta, torch.float32, "beta", 1), s_out, zp_out, bits,
-                                  _dev_ptr(y_q, torch.int8, "y_q", 2), _stream(stream, x_q))
-    _check("ptf_layernorm_int8", st)
-    return y_q
+    args = (_dev_ptr(x_q, torch.int8, "x_q", 2), T, C, zp_in,
+            _dev_ptr(alpha, torch.uint8, "alpha", 1), K,
+            _dev_ptr(gamma, torch.float32, "gamma", 1),
+            _dev_ptr(beta, torch.float32, "beta", 1), s_out, zp_out, bits,
+            _dev_ptr(y_q, torch.int8, "y_q", 2), _stream(stream, x_q))
+    return _invoke("ptf_layernorm_int8", args, (x_q, alpha, gamma, beta, y_q), prepare, y_q)
 
 
 def codes_ld(Lk: int) -> int:
@@ -130,7 +159,7 @@ def codes_ld(Lk: int) -> int:
 
 
 def lis_softmax_log4(logits, s_logit: float, bits: int = 4, exp_n: int = 20, bias=None,
-                     codes=None, stream=None):
+                     codes=None, stream=None, prepare: bool = False):
     """Packed 4-bit Log-Int-Softmax codes [G, Lq, ld] of int32 logits [G, Lq, Lk]."""
     import torch
     G, Lq, Lk = logits.shape
@@ -143,15 +172,14 @@ def lis_softmax_log4(logits, s_logit: float, bits: int = 4, exp_n: int = 20, bia
         if bias.dim() != 3 or bias.shape[1:] != (Lq, Lk):
             raise ValueError("bias must be [Hb, Lq, Lk]")
         Hb = bias.shape[0]
-    st = lib().lis_softmax_log4(_dev_ptr(logits, torch.int32, "logits", 3), G, Lq, Lk,
-                                _dev_ptr(bias, torch.int32, "bias", 3), Hb, s_logit, bits, exp_n,
-                                _dev_ptr(codes, torch.uint8, "codes", 3), codes.shape[2],
-                                _stream(stream, logits))
-    _check("lis_softmax_log4", st)
-    return codes
+    args = (_dev_ptr(logits, torch.int32, "logits", 3), G, Lq, Lk,
+            _dev_ptr(bias, torch.int32, "bias", 3), Hb, s_logit, bits, exp_n,
+            _dev_ptr(codes, torch.uint8, "codes", 3), codes.shape[2], _stream(stream, logits))
+    return _invoke("lis_softmax_log4", args, (logits, bias, codes), prepare, codes)
 
 
-def lis_attn_v_shift(codes, v, Lk: int, zp_v: int = 0, bits: int = 4, out=None, stream=None):
+def lis_attn_v_shift(codes, v, Lk: int, zp_v: int = 0, bits: int = 4, out=None, stream=None,
+                     prepare: bool = False):
     """BitShift Attn x V: int32 [G, Lq, d] from packed codes [G, Lq, ld] and int8 V [G, Lk, d]."""
     import torch
     G, Lq, ld = codes.shape
@@ -162,15 +190,13 @@ def lis_attn_v_shift(codes, v, Lk: int, zp_v: int = 0, bits: int = 4, out=None, 
         out = torch.empty((G, Lq, d), dtype=torch.int32, device=v.device)
     if out.shape != (G, Lq, d):
         raise ValueError("out must be [G, Lq, d]")
-    st = lib().lis_attn_v_shift(_dev_ptr(codes, torch.uint8, "codes", 3), ld,
-                                _dev_ptr(v, torch.int8, "v", 3), zp_v, G, Lq, Lk, d, bits,
-                                _dev_ptr(out, torch.int32, "out", 3), _stream(stream, v))
-    _check("lis_attn_v_shift", st)
-    return out
+    args = (_dev_ptr(codes, torch.uint8, "codes", 3), ld, _dev_ptr(v, torch.int8, "v", 3), zp_v,
+            G, Lq, Lk, d, bits, _dev_ptr(out, torch.int32, "out", 3), _stream(stream, v))
+    return _invoke("lis_attn_v_shift", args, (codes, v, out), prepare, out)
 
 
 def lis_attention_head(logits, v, s_logit: float, bits: int = 4, exp_n: int = 20, zp_v: int = 0,
-                       bias=None, out=None, codes_out=None, stream=None):
+                       bias=None, out=None, codes_out=None, stream=None, prepare: bool = False):
     """Fused Log-Int-Softmax + BitShift Attn x V; returns int32 [G, Lq, d]."""
     import torch
     G, Lq, Lk = logits.shape
@@ -191,11 +217,8 @@ def lis_attention_head(logits, v, s_logit: float, bits: int = 4, exp_n: int = 20
         if codes_out.dim() != 3 or codes_out.shape[:2] != (G, Lq):
             raise ValueError("codes_out must be [G, Lq, ld_codes]")
         ld = codes_out.shape[2]
-    st = lib().lis_attention_head(_dev_ptr(logits, torch.int32, "logits", 3),
-                                  _dev_ptr(bias, torch.int32, "bias", 3), Hb, G, Lq, Lk, s_logit,
-                                  bits, exp_n, _dev_ptr(v, torch.int8, "v", 3), zp_v, d,
-                                  _dev_ptr(out, torch.int32, "out", 3),
-                                  _dev_ptr(codes_out, torch.uint8, "codes_out", 3), ld,
-                                  _stream(stream, logits))
-    _check("lis_attention_head", st)
-    return out
+    args = (_dev_ptr(logits, torch.int32, "logits", 3), _dev_ptr(bias, torch.int32, "bias", 3), Hb,
+            G, Lq, Lk, s_logit, bits, exp_n, _dev_ptr(v, torch.int8, "v", 3), zp_v, d,
+            _dev_ptr(out, torch.int32, "out", 3),
+            _dev_ptr(codes_out, torch.uint8, "codes_out", 3), ld, _stream(stream, logits))
+    return _invoke("lis_attention_head", args, (logits, bias, v, out, codes_out), prepare, out)

@@ -51,6 +51,15 @@ def test_time_next_call_is_host_only(lib):
     assert lib.fq_time_next_call(None, None) == 0
 
 
+def test_prepared_call_reports_status(lib):
+    # a prepared call that fails host validation raises like a direct call
+    call = B.Prepared("ptf_layernorm_int8",
+                      (None, 4, 0, 0, None, 3, None, None, 1.0, 0, 8, None, None), ())
+    with pytest.raises(B.FqError) as ei:
+        call()
+    assert ei.value.status == B.FQ_ERR_SHAPE
+
+
 def test_status_strings(lib):
     for s in range(6):
         assert B.status_str(s).startswith("FQ_")

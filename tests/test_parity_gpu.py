@@ -240,6 +240,61 @@ def test_head_shapes(fq, orc, G, Lq, Lk, d):
     assert np.array_equal(got, ref)
 
 
+# Shapes with enough units that the launch takes the one-workgroup-per-unit
+# kernel (G * min(4, ceil(Lq / 16)) >= 2048): half and full last chunks, waves
+# with several 16-row tiles, head dimensions that take the byte-wise V loads
+# (d % 16 != 0) and the scalar output stores (d % 4 != 0).
+UNIT_SHAPES = [(1024, 17, 16, 64), (1024, 17, 17, 64), (1024, 20, 100, 64), (512, 70, 197, 64),
+               (600, 49, 49, 32), (512, 65, 224, 64), (700, 33, 120, 48), (700, 33, 120, 20),
+               (2048, 2, 40, 17), (2048, 1, 5, 64)]
+
+
+@pytest.mark.parametrize("G,Lq,Lk,d", UNIT_SHAPES)
+def test_head_unit_kernel(fq, orc, G, Lq, Lk, d):
+    say("head unit", G, Lq, Lk, d)
+    a = W.attn_inputs(G, Lq, Lk, d, seed=G + Lk + d, heads=G, sigma=(1.0, 3.0, 6.0), v_lo=-128,
+                      v_hi=127)
+    got = host(fq.lis_attention_head(dev(a["logits"]), dev(a["v"]), S, zp_v=3))
+    ref = orc.lis_attention_head(a["logits"], a["v"], S, zp_v=3)
+    assert np.array_equal(got, ref)
+
+
+@pytest.mark.parametrize("G,Lq,Lk", [(1024, 17, 16), (1024, 20, 100), (512, 70, 197),
+                                     (2048, 1, 33)])
+def test_codes_unit_kernel(fq, orc, G, Lq, Lk):
+    say("codes unit", G, Lq, Lk)
+    a = W.attn_inputs(G, Lq, Lk, 1, seed=3 * G + Lk, heads=G, sigma=(1.0, 3.0, 6.0))
+    got = host(fq.lis_softmax_log4(dev(a["logits"]), S))
+    assert np.array_equal(got, orc.lis_softmax_log4(a["logits"], S))
+
+
+@pytest.mark.parametrize("s", [1e-4, 0.5, 0.0009765625])
+def test_head_integer_and_float_paths(fq, orc, s):
+    """s = 1e-4 exceeds the float path's 2^24 bound on q_b^2 + q_c and runs the
+    integer path; the others run the float path, on both kernels."""
+    for G, Lq, Lk, d in [(3, 40, 197, 64), (1024, 17, 100, 64)]:
+        say("head path", s, G, Lq, Lk, d)
+        a = W.attn_inputs(G, Lq, Lk, d, seed=5 + G, heads=G, s_logit=s, sigma=(0.5, 2.0, 8.0))
+        got = host(fq.lis_attention_head(dev(a["logits"]), dev(a["v"]), s))
+        assert np.array_equal(got, orc.lis_attention_head(a["logits"], a["v"], s))
+
+
+def test_prepared_calls_match_direct(fq, orc):
+    import torch
+    say("prepared")
+    a = W.attn_inputs(1024, 17, 100, 64, seed=9, heads=4)
+    lg, v = dev(a["logits"]), dev(a["v"])
+    out = torch.empty((1024, 17, 64), dtype=torch.int32, device="cuda:0")
+    call = fq.lis_attention_head(lg, v, S, out=out, prepare=True)
+    call()
+    assert np.array_equal(host(out), host(fq.lis_attention_head(lg, v, S)))
+    d = W.ln_inputs(100, 768, seed=4)
+    y = torch.empty((100, 768), dtype=torch.int8, device="cuda:0")
+    fq.ptf_layernorm_int8(dev(d["x_q"]), d["zp_in"], dev(d["alpha"]), d["K"], dev(d["gamma"]),
+                          dev(d["beta"]), d["s_out"], d["zp_out"], d["bits"], y_q=y, prepare=True)()
+    assert np.array_equal(host(y), _ln_ref(orc, d))
+
+
 def test_head_codes_out_and_unfused_equal(fq, orc):
     """The fused head writes the same codes as lis_softmax_log4, and its output
     equals lis_attn_v_shift of those codes (MFMA product vs VALU shifts)."""
