@@ -1,0 +1,98 @@
+"""The float form of I-Exp and of the LIS code, as the fused head evaluates it
+(binary32 I-Exp, binary64 code), against the oracle's integer definitions.
+
+The GPU parity tests compare the kernels with the oracle on sampled inputs;
+these tests establish, on the CPU, that the float formulation itself equals
+the definition on every input the I-Exp can see and at the exact code
+thresholds.  The binary32 fused multiply-add is emulated exactly: the product
+of two binary32 values is exact in the x87 extended format, the sum with the
+addend here stays within its 64-bit significand, and one rounding to binary32
+follows."""
+import numpy as np
+import pytest
+
+F32_MAGIC = np.float32(12582912.0)   # 1.5 * 2^23
+
+
+def _fma32(a, b, c):
+    return (a.astype(np.longdouble) * b.astype(np.longdouble)
+            + np.asarray(c, dtype=np.longdouble)).astype(np.float32)
+
+
+def _float_consts(k):
+    d = -k.q_ln2
+    return dict(inv_d=np.float32(1.0 / d), c0=np.float32(0.5 / d - 0.5), d=np.float32(d),
+                qb=np.float32(k.q_b), qc=np.float32(k.q_c), sK=np.int64(0x4B400000 + k.n),
+                umax=np.uint32(k.n * d))
+
+
+def _iexp_float(u_raw, f):
+    """e = qL 2^(n - z) from u = -q by the float steps of the kernel."""
+    u = np.minimum(u_raw.astype(np.uint32), f["umax"])
+    uf = u.astype(np.float32)
+    t = _fma32(uf, np.full_like(uf, f["inv_d"]), f["c0"])
+    zb = (t + F32_MAGIC).astype(np.float32)
+    zf = (zb - F32_MAGIC).astype(np.float32)
+    w = _fma32(zf, np.full_like(zf, f["d"]), (f["qb"] - uf).astype(np.float32))
+    qL = _fma32(w, w, f["qc"])
+    shift = f["sK"] - zb.view(np.int32).astype(np.int64)
+    return np.ldexp(qL.astype(np.float64), shift)
+
+
+@pytest.mark.parametrize("s", [0.5, 0.05, 2.0 ** -10, 0.0005])
+@pytest.mark.parametrize("n", [1, 8, 20, 30])
+def test_iexp_float_form_exhaustive(orc, s, n):
+    k = orc.iexp_constants(s, n)
+    d = -k.q_ln2
+    if k.q_b ** 2 + k.q_c >= 2 ** 24:
+        pytest.skip("outside the float path's bound")
+    f = _float_consts(k)
+    u = np.arange(n * d + 4, dtype=np.int64)          # every clamped input, plus beyond the clamp
+    got = _iexp_float(u, f)
+    ref = np.array([orc.iexp(-int(x), k)[0] for x in u], dtype=np.float64)
+    assert np.array_equal(got, ref)
+
+
+def _code_float(S2, e, top):
+    X = S2 + e
+    Y = e * 1.5
+    m = ((X.view(np.int64) - Y.view(np.int64)) >> 52).astype(np.int64)
+    return np.minimum(m, top) - (X < e * 4.0).astype(np.int64)
+
+
+def test_code_float_form_at_thresholds(orc):
+    """2S = c_k e + delta for every threshold c_k and small delta, i.e. exactly
+    where round(S / e) crosses an I-Log2 step."""
+    rng = np.random.default_rng(7)
+    cases = []
+    for _ in range(4000):
+        qL = int(rng.integers(1, 2 ** 24))
+        sh = int(rng.integers(0, 31))
+        e = qL << sh
+        k = int(rng.integers(1, 16))
+        ck = 3 if k == 1 else 3 * 2 ** (k - 1) - 1
+        for delta in (-2, -1, 0, 1, 2):
+            S2 = ck * e + delta
+            S2 += S2 & 1                                  # 2S is even
+            if S2 < 2 * e or S2 + e >= 2 ** 53:
+                continue
+            cases.append((S2, e))
+    S2 = np.array([c[0] for c in cases], dtype=np.float64)
+    e = np.array([c[1] for c in cases], dtype=np.float64)
+    for top in (1, 3, 7, 15):
+        got = _code_float(S2, e, top)
+        ref = np.array([min(orc.ilog2((a + b) // (2 * b)), top) for a, b in cases])
+        assert np.array_equal(got, ref)
+
+
+def test_code_float_form_on_rows(orc):
+    """Whole rows through the oracle's I-Exp: codes from the float form equal
+    the oracle's codes."""
+    rng = np.random.default_rng(3)
+    for sigma, Lk in [(1.0, 197), (3.0, 197), (6.0, 577), (0.2, 49)]:
+        row = np.rint(rng.standard_normal(Lk) * sigma / 2.0 ** -10).astype(np.int32)
+        e, ssum = orc.lis_row_exp(row, 2.0 ** -10, 20)
+        S2 = 2.0 * float(np.sum(e))
+        codes = orc.unpack_codes(orc.lis_softmax_log4(row[None, None, :], 2.0 ** -10), Lk)[0, 0]
+        got = _code_float(np.full(Lk, S2), e.astype(np.float64), 15)
+        assert np.array_equal(got, codes.astype(np.int64))
