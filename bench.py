@@ -151,16 +151,19 @@ def algorithmic_bytes(cfg):
     return ln, head
 
 
-def cpu_baseline(cfg, inp, reps=2):
-    """The CPU oracle on `reps` complete steps of the same workload (one thread)."""
+def cpu_baseline(cfg, inp, min_s=10.0, max_steps=12):
+    """The CPU oracle on complete steps of the same workload (one thread), repeated
+    until at least `min_s` seconds have passed (at most `max_steps` steps)."""
     import oracle
     ln, a = inp["ln"], inp["attn"]
+    reps = 0
     t0 = time.perf_counter()
-    for _ in range(reps):
+    while reps < max_steps and (reps == 0 or time.perf_counter() - t0 < min_s):
         oracle.ptf_layernorm_int8(ln["x_q"], ln["zp_in"], ln["alpha"], ln["K"], ln["gamma"],
                                   ln["beta"], ln["s_out"], ln["zp_out"], ln["bits"])
         oracle.lis_attention_head(a["logits"], a["v"], a["s_logit"], a["bits"], a["exp_n"],
                                   a["zp_v"], bias=a["bias"])
+        reps += 1
     dt = time.perf_counter() - t0
     return {"value": reps * cfg.T / dt, "unit": "tokens/s", "cores": 1, "kind": "oracle",
             "sample": f"{reps} complete steps of {cfg.name} (PTF-LayerNorm {cfg.T}x{cfg.channels}"

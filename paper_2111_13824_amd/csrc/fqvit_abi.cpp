@@ -56,11 +56,11 @@ fq_status lis_constants(float s_logit, int32_t bits, int32_t n, int32_t Lk,
     k->n = n;
     k->top = (1 << bits) - 1;
     // The float form: every I-Exp intermediate is an integer below 2^24 (exact
-    // in binary32) and 2S + e is an integer below 2^53 (exact in binary64).
+    // in binary32) and 2S + e + 1/2 lies below 2^52 (exact in binary64).
     const uint64_t qlmax = qb * qb + qc;
     k->fp_ok = qlmax < (1ull << 24) &&
                (unsigned __int128)(2 * (uint64_t)Lk + 1) * ((unsigned __int128)qlmax << n) <
-                   ((unsigned __int128)1 << 53);
+                   ((unsigned __int128)1 << 52);
     k->f_inv_d = (float)(1.0 / (double)d);
     k->f_c0 = (float)(0.5 / (double)d - 0.5);
     k->f_d = (float)d;

@@ -65,7 +65,7 @@ struct LisConsts {
     int32_t n;          // clamp depth
     int32_t top;        // 2^bits - 1
     // Exact single/double precision form of the same arithmetic, valid when
-    // q_b^2 + q_c < 2^24 and (2 Lk + 1)(q_b^2 + q_c) 2^n < 2^53 (fp_ok).
+    // q_b^2 + q_c < 2^24 and (2 Lk + 1)(q_b^2 + q_c) 2^n < 2^52 (fp_ok).
     int32_t fp_ok;
     float f_inv_d;      // 1 / d_ln2 rounded to float
     float f_c0;         // 0.5 / d_ln2 - 0.5 rounded to float

@@ -30,9 +30,9 @@
 // (m >= 1 always, since 2S >= 2e, and 2S < 3e forces m = 1).  Two exact
 // evaluations of this formula are implemented:
 //   * float path: I-Exp in binary32 (every intermediate is an integer below
-//     2^24) and the code in binary64 (2S + e is an integer below 2^53), m being
-//     the difference of the IEEE bit patterns of 2S + e and 1.5 e shifted right
-//     by 52 (both positive, so the pattern difference is the exponent
+//     2^24) and the code in binary64 (2S + e + 1/2 below 2^52), m being the
+//     difference of the IEEE bit patterns of 2S + e + 1/2 and 1.5 e shifted
+//     right by 52 (both positive, so the pattern difference is the exponent
 //     difference minus a borrow exactly when the mantissa of the quotient
 //     falls below 1);
 //   * integer path (any scale the host accepts): 24-bit integer I-Exp and
@@ -320,18 +320,29 @@ __device__ __forceinline__ float iexp_f(int v, int mx, const LisConsts& k) {
     return __builtin_ldexpf(qL, k.f_sK - __float_as_int(zb));
 }
 
-// Code of one key from e (its binary32 bit pattern) and 2S (binary64, exact).
+// Code of one key from e (its binary32 bit pattern), 2S and 2S + 1/2
+// (binary64; 2S + e + 1/2 < 2^52, so every value below is exact).
+//   * m = floor(log2(X / Y)) with X = 2S + e + 1/2 and Y = 1.5 e: X is a
+//     half-integer and Y 2^m an integer, so X / Y is never a power of two and
+//     the bit-pattern difference bits(X) - bits(Y) - 1 = bits(X) + ~bits(Y)
+//     (one v_lshl_add_u64, no carry through a scalar register) has the same
+//     top 12 bits as the exact difference; adding 1/2 to 2S + e changes no
+//     comparison with the integers Y 2^m.
+//   * [2S < 3e] is the sign of the exact fma(e, -3, 2S).
 // The empty asm hides the pattern's origin so that the compiler converts it to
 // binary64 here rather than keeping the conversions of the I-Exp pass (two
 // registers per key) alive across both passes.
-__device__ __forceinline__ int code_f(int ebits, double S2, int top) {
+__device__ __forceinline__ int code_f(int ebits, double S2h, double S2, int top) {
     asm volatile("" : "+v"(ebits));
-    const float e = __int_as_float(ebits);
-    const double ed = (double)e;
-    const double X = S2 + ed;
+    const double ed = (double)__int_as_float(ebits);
+    const double X = S2h + ed;
     const double Y = ed * 1.5;
-    const int m = (int)((__double_as_longlong(X) - __double_as_longlong(Y)) >> 52);
-    return min(m, top) - (X < ed * 4.0 ? 1 : 0);
+    const uint64_t nyb = ~(uint64_t)__double_as_longlong(Y);
+    uint64_t d;
+    asm("v_lshl_add_u64 %0, %1, 0, %2" : "=v"(d) : "v"((uint64_t)__double_as_longlong(X)), "v"(nyb));
+    const int m = (int)(d >> 52);
+    const int t = (int)((uint32_t)((uint64_t)__double_as_longlong(fma(ed, -3.0, S2)) >> 32) >> 31);
+    return min(m, top) - t;
 }
 
 // Wavefronts per SIMD the register allocation aims for: the logits of NC chunks
@@ -360,6 +371,7 @@ __device__ __forceinline__ int tile_max(const int (&lg)[NC][8]) {
 
 struct RowState {
     double S2f;     // float path: 2S
+    double S2h;     // float path: 2S + 1/2
     RowSum rs;      // integer path
 };
 
@@ -389,6 +401,7 @@ __device__ __forceinline__ RowState tile_iexp(int (&lg)[NC][8], uint32_t (&zb)[N
         sum += __shfl_xor(sum, 16, 64);
         sum += __shfl_xor(sum, 32, 64);
         st.S2f = 2.0 * sum;
+        st.S2h = st.S2f + 0.5;
     } else {
         uint64_t sum = 0;
 #pragma unroll
@@ -434,7 +447,7 @@ __device__ __forceinline__ void chunk_codes(int (&code)[8], const int (&lg)[NC][
         }
         int cd;
         if constexpr (FP) {
-            cd = code_f(lg[c][t], st.S2f, k.top);
+            cd = code_f(lg[c][t], st.S2h, st.S2f, k.top);
         } else {
             const uint32_t z = (zb[c][t >> 2] >> (8 * (t & 3))) & 0xFFu;
             cd = lis_code((uint32_t)lg[c][t], z, st.rs, k);
@@ -459,16 +472,13 @@ __device__ __forceinline__ u32x4 chunk_pbits(const int (&lg)[NC][8], const uint3
         }
         int cd;
         if constexpr (FP) {
-            cd = code_f(lg[c][t], st.S2f, k.top);
+            cd = code_f(lg[c][t], st.S2h, st.S2f, k.top);
         } else {
             const uint32_t z = (zb[c][t >> 2] >> (8 * (t & 3))) & 0xFFu;
             cd = lis_code((uint32_t)lg[c][t], z, st.rs, k);
         }
         const float p = __builtin_ldexpf(ptop, -cd);
         P[t] = (last && lg[c][t] == 0) ? 0.0f : p;
-        // two keys at a time: interleaving all eight would hold about six
-        // registers of binary64 temporaries per key
-        if (t & 1) __builtin_amdgcn_sched_barrier(0);
     }
     return u32x4{bf16_pair(P[0], P[1]), bf16_pair(P[2], P[3]), bf16_pair(P[4], P[5]),
                  bf16_pair(P[6], P[7])};
@@ -527,21 +537,33 @@ __device__ __forceinline__ void store_out_rows(const f32x4 (&acc)[DTMAX], int32_
                                                int r, int kg) {
     constexpr int LDO = 16 * DTMAX + 4;
     constexpr int UPR = 4 * DTMAX;    // 16-byte units per row
+    typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 #pragma unroll
     for (int dt = 0; dt < DTMAX; ++dt) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) ot[(4 * kg + q) * LDO + 16 * dt + r] = (int32_t)acc[dt][q];
+    }
+    int32_t* otile = a.out + (g * a.Lq + i0) * (int64_t)a.d;
+    if (i0 + 16 <= a.Lq && a.d == 16 * DTMAX) {
+        // a whole tile: 16 consecutive rows of d columns, one contiguous range
+#pragma unroll
+        for (int j = 0; j < UPR / 4; ++j) {
+            const int u = lane + 64 * j;
+            const int row = u / UPR;
+            const int c4 = u - row * UPR;
+            *reinterpret_cast<i32x4*>(otile + 4 * u) =
+                *reinterpret_cast<const i32x4*>(ot + row * LDO + 4 * c4);
+        }
+        return;
     }
 #pragma unroll
     for (int j = 0; j < UPR / 4; ++j) {
         const int u = lane + 64 * j;
         const int row = u / UPR;
         const int c4 = u - row * UPR;
-        const int orow = i0 + row;
-        typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
         const i32x4 v = *reinterpret_cast<const i32x4*>(ot + row * LDO + 4 * c4);
-        if (orow < a.Lq && 4 * c4 < a.d)
-            *reinterpret_cast<i32x4*>(a.out + (g * a.Lq + orow) * (int64_t)a.d + 4 * c4) = v;
+        if (i0 + row < a.Lq && 4 * c4 < a.d)
+            *reinterpret_cast<i32x4*>(otile + row * a.d + 4 * c4) = v;
     }
 }
 
@@ -559,6 +581,25 @@ __device__ __forceinline__ RowPtrs row_ptrs(const LisArgs& a, const LisLaunch& p
     const int64_t roff = (g * a.Lq + i) * (int64_t)a.Lk;
     rp.row = a.logits + roff;
     const int64_t boff = a.bias ? ((g % a.Hb) * a.Lq + i) * (int64_t)a.Lk : 0;
+    rp.brow = a.bias ? a.bias + boff : nullptr;
+    rp.tail_vec = roff + 32 * NC <= p.n_logits && (!rp.brow || boff + 32 * NC <= p.n_bias);
+    return rp;
+}
+
+// Row pointers inside one unit from its base offsets (unit kernel): the unit's
+// logit and bias planes are computed once, rows are offsets into them.
+struct UnitBase {
+    int64_t loff;   // offset of the unit's logits
+    int64_t boff;   // offset of its head's bias plane (0 without bias)
+};
+
+template <int NC>
+__device__ __forceinline__ RowPtrs unit_row(const LisArgs& a, const LisLaunch& p, const UnitBase& ub,
+                                            int i) {
+    RowPtrs rp;
+    const int64_t roff = ub.loff + (int64_t)i * a.Lk;
+    rp.row = a.logits + roff;
+    const int64_t boff = ub.boff + (int64_t)i * a.Lk;
     rp.brow = a.bias ? a.bias + boff : nullptr;
     rp.tail_vec = roff + 32 * NC <= p.n_logits && (!rp.brow || boff + 32 * NC <= p.n_bias);
     return rp;
@@ -601,7 +642,8 @@ __device__ __forceinline__ void load_one_chunk(int (&lg)[NC][8], const RowPtrs& 
 template <int NC, bool FUSED, int DTMAX, bool HALF>
 __device__ __forceinline__ void unit_tile(int (&cur)[NC][8], int (&nxt)[NC][8], const LisArgs& a,
                                           const LisLaunch& p, const LisConsts& k, const uint16_t* vt,
-                                          int32_t* ot, int64_t g, int tile, int lane, int r, int kg) {
+                                          int32_t* ot, const UnitBase& ub, int64_t g, int tile,
+                                          int lane, int r, int kg) {
     constexpr int NT = HALF ? 4 : 8;
     constexpr int PF = unit_prefetch(NC);
     const int i0 = 16 * tile;
@@ -609,7 +651,7 @@ __device__ __forceinline__ void unit_tile(int (&cur)[NC][8], int (&nxt)[NC][8], 
     // across the loop); past the last tile the current rows, still in cache,
     // are read again.
     const int nt = tile + 4 < p.ntiles ? tile + 4 : tile;
-    const RowPtrs rn = row_ptrs<NC>(a, p, g, min(16 * nt + r, a.Lq - 1));
+    const RowPtrs rn = unit_row<NC>(a, p, ub, min(16 * nt + r, a.Lq - 1));
     uint32_t zb[NC][2];
     const RowState st = tile_iexp<NC, true, NT>(cur, zb, k);
     tile_load<NC, HALF, 0, PF>(nxt, rn, kg, a.Lk);
@@ -663,20 +705,23 @@ __global__ __launch_bounds__(kBlock, 3) void lis_unit_kernel(LisArgs a, LisLaunc
     if constexpr (FUSED)
         stage_load(sr, a.v + g * (int64_t)a.Lk * a.d, a.Lk, a.d, DTMAX, 0, 32 * NC, p.vec_ok);
 
+    UnitBase ub;
+    ub.loff = g * a.Lq * (int64_t)a.Lk;
+    ub.boff = a.bias ? (g % a.Hb) * a.Lq * (int64_t)a.Lk : 0;
     int bufA[NC][8], bufB[NC][8];
     int tile = (wave + (int)(g & 3)) & 3;
     if (tile < p.ntiles)
-        tile_load<NC, HALF>(bufA, row_ptrs<NC>(a, p, g, min(16 * tile + r, a.Lq - 1)), kg, a.Lk);
+        tile_load<NC, HALF>(bufA, unit_row<NC>(a, p, ub, min(16 * tile + r, a.Lq - 1)), kg, a.Lk);
     if constexpr (FUSED) {
         stage_store(sr, vt, p.ld, DTMAX, 32 * NC, a.zp_v);
         __syncthreads();
     }
     int32_t* ot = reinterpret_cast<int32_t*>(smem + p.vt_bytes) + wave * out_lds_dwords<DTMAX>();
     while (tile < p.ntiles) {
-        unit_tile<NC, FUSED, DTMAX, HALF>(bufA, bufB, a, p, k, vt, ot, g, tile, lane, r, kg);
+        unit_tile<NC, FUSED, DTMAX, HALF>(bufA, bufB, a, p, k, vt, ot, ub, g, tile, lane, r, kg);
         tile += 4;
         if (tile >= p.ntiles) break;
-        unit_tile<NC, FUSED, DTMAX, HALF>(bufB, bufA, a, p, k, vt, ot, g, tile, lane, r, kg);
+        unit_tile<NC, FUSED, DTMAX, HALF>(bufB, bufA, a, p, k, vt, ot, ub, g, tile, lane, r, kg);
         tile += 4;
     }
 }

@@ -87,15 +87,20 @@ __device__ __forceinline__ void row_factors(int64_t m1, int64_t m2, int C, doubl
 // Output of one element when A = gs r is known to lie in [2^(b-31), 2^b): then
 // N1 = b - 1 - floor(log2 |A|) needs no clamp and sign(A) N2 / 2^N1 is A with
 // its significand cut to b bits, a mask on the high word (b <= 8 keeps the
-// low word zero).  Same result as ln_requant.
-// dlo, dhi: the output bounds minus zp_out.
-__device__ __forceinline__ int ln_requant_fast(double A, double B, int xh, int bits,
-                                               uint32_t hi_mask, int zp_out, double dlo,
+// low word zero).  rint(B 2^N1) 2^-N1 is B rounded to the grid of that last
+// bit, 2^(E - b + 1) with E the exponent of A, ties to even: adding and
+// subtracting M = 1.5 2^(E - b + 53) does exactly that while |B| < 2^(E - b + 52);
+// larger B (and the oracle's clamp of B 2^N1 at 2^62) saturate the output
+// either way, since |A X^| < 2^(E + 12).  Same result as ln_requant.
+// m_add = (53 - b) << 20 | 0x80000 builds M's high word from A's exponent
+// field; dlo, dhi: the output bounds minus zp_out.
+__device__ __forceinline__ int ln_requant_fast(double A, double B, int xh, uint32_t hi_mask,
+                                               uint32_t m_add, int zp_out, double dlo,
                                                double dhi) {
-    const int N1 = bits - __builtin_amdgcn_frexp_exp(A);
-    const uint64_t ab = __double_as_longlong(A);
-    const double At = __longlong_as_double((int64_t)(((uint64_t)((uint32_t)(ab >> 32) & hi_mask)) << 32));
-    const double Bg = ldexp(rint(ldexp(B, N1)), -N1);
+    const uint32_t hiA = (uint32_t)((uint64_t)__double_as_longlong(A) >> 32);
+    const double At = __longlong_as_double((int64_t)((uint64_t)(hiA & hi_mask) << 32));
+    const double M = __longlong_as_double((int64_t)((uint64_t)((hiA & 0x7FF00000u) + m_add) << 32));
+    const double Bg = (B + M) - M;
     const double val = fma(At, (double)xh, Bg + 0.5);
     return (int)floor(fmin(fmax(val, dlo), dhi)) + zp_out;
 }
@@ -167,6 +172,7 @@ __global__ __launch_bounds__(kBlock) void ln_fast_kernel(LnArgs a, int lshift) {
     const int qlo = -(1 << (a.bits - 1));
     const int qhi = (1 << (a.bits - 1)) - 1;
     const uint32_t hi_mask = ~((1u << (21 - a.bits)) - 1u);   // keep sign, exponent, b-1 bits
+    const uint32_t m_add = ((uint32_t)(53 - a.bits) << 20) | 0x80000u;
     const double amax = ldexp(1.0, a.bits), amin = ldexp(1.0, a.bits - 31);
     const double dlo = (double)(qlo - a.zp_out), dhi = (double)(qhi - a.zp_out);
     const int64_t gw = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
@@ -236,7 +242,7 @@ __global__ __launch_bounds__(kBlock) void ln_fast_kernel(LnArgs a, int lshift) {
                     const int k = 4 * w + b;
                     const double A = gs[k] * r;
                     const double B = bs[k] - gs[k] * m;
-                    const int q = ln_requant_fast(A, B, xh[k], a.bits, hi_mask, a.zp_out, dlo, dhi);
+                    const int q = ln_requant_fast(A, B, xh[k], hi_mask, m_add, a.zp_out, dlo, dhi);
                     pack |= ((uint32_t)q & 0xFFu) << (8 * b);
                 }
                 if (rok && ok[w]) __builtin_nontemporal_store(pack, yr + li + (w << lshift));
@@ -313,6 +319,8 @@ hipError_t launch_fast(const LnArgs& a, int lshift, bool wide, hipStream_t strea
 
 hipError_t launch_ptf_layernorm(const LnArgs& a, hipStream_t stream) {
     const bool aligned = ((reinterpret_cast<uintptr_t>(a.x) | reinterpret_cast<uintptr_t>(a.y)) & 3) == 0;
+    // Lanes per row L and dwords per lane W: least padding, then the most
+    // lanes per row (fewest registers, highest occupancy).
     int best_l = -1, best_w = 0, best_waste = 1 << 30;
     if (aligned && a.C % 4 == 0) {
         for (int l = 6; l >= 0; --l) {

@@ -54,10 +54,15 @@ def test_iexp_float_form_exhaustive(orc, s, n):
 
 
 def _code_float(S2, e, top):
-    X = S2 + e
+    """m from bits(2S + e + 1/2) + ~bits(1.5 e) (64-bit wrap), t from the sign
+    of fma(e, -3, 2S), as the kernel computes them."""
+    X = (S2 + 0.5) + e
     Y = e * 1.5
-    m = ((X.view(np.int64) - Y.view(np.int64)) >> 52).astype(np.int64)
-    return np.minimum(m, top) - (X < e * 4.0).astype(np.int64)
+    d = X.view(np.uint64) + ~Y.view(np.uint64)
+    m = (d >> np.uint64(52)).astype(np.int64)
+    s3 = (S2.astype(np.longdouble) - 3 * e.astype(np.longdouble)).astype(np.float64)
+    t = (s3.view(np.uint64) >> np.uint64(63)).astype(np.int64)
+    return np.minimum(m, top) - t
 
 
 def test_code_float_form_at_thresholds(orc):
@@ -74,7 +79,7 @@ def test_code_float_form_at_thresholds(orc):
         for delta in (-2, -1, 0, 1, 2):
             S2 = ck * e + delta
             S2 += S2 & 1                                  # 2S is even
-            if S2 < 2 * e or S2 + e >= 2 ** 53:
+            if S2 < 2 * e or S2 + e + 1 >= 2 ** 52:
                 continue
             cases.append((S2, e))
     S2 = np.array([c[0] for c in cases], dtype=np.float64)
