@@ -300,6 +300,282 @@ __global__ __launch_bounds__(kBlock) void ln_generic_kernel(LnArgs a) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// Row-batch kernel for rows of 256..1024 channels (C % 4 == 0, dword-aligned)
+// whose sums of squares fit 32 bits (C (255 2^K)^2 < 2^32).
+//
+// A wavefront owns a contiguous run of rows, taken four at a time; lane l owns
+// dwords l, l + 64, ... of each row (coalesced dword loads and stores).  The
+// per-channel (gs, bs) pairs stay in LDS in [byte][dword] order, so that the
+// 16-byte reads of a wavefront are consecutive.  Per dword, with xu = x + 128 (the byte with
+// its sign bit flipped, 0..255) and u = zp_in + 128:
+//   X^ pairs  = (xu pairs) * (2^alpha pairs) + (-u 2^alpha pairs)   packed i16,
+//               exact: |X^| <= 255 2^7 < 2^15
+//   M1 lane  += dot4(xu bytes, 2^alpha bytes), the -u sum_c 2^alpha part of
+//               every row being a per-lane constant
+//   M2 lane  += dot2(X^ pair, X^ pair), twice
+// The 4 x 2 per-row totals are reduced together: a 32-lane swap-add and a
+// 16-lane swap-add leave row j's partial sums in lanes 16 j .. 16 j + 15,
+// four row rotations finish them, and one evaluation of the square root and
+// the two divisions serves the four rows (lane group j).  The per-row factors
+// reach every lane as scalars.
+//
+// Output, when the row's factors fit (see ln_requant_fast): with
+// c = zp_out + 1/2 + 512, v = At X^ + (Bg + c) is exact (multiples of 2^-N1
+// below 2^53 2^-N1) and floor(v) = w + zp_out + 512; v_cvt_i32_f64 truncates
+// (floor for v >= 0) and saturates, and a clamp to [qlo + 512, qhi + 512]
+// (both positive, so a negative v lands on the lower bound either way) gives
+// Y + 512, whose low byte is Y's.
+constexpr int kRowBatch = 4;
+
+typedef short short2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint32_t swap_add32(uint32_t a, uint32_t b) {
+    // lanes 0-31: a summed over lanes l and l + 32; lanes 32-63: the same for b
+    const auto s = __builtin_amdgcn_permlane32_swap(a, b, false, false);
+    return s[0] + s[1];
+}
+
+__device__ __forceinline__ uint32_t swap_add16(uint32_t a, uint32_t b) {
+    // within each 32-lane half: lanes 0-15 a, lanes 16-31 b, summed over
+    // lanes l and l + 16
+    const auto s = __builtin_amdgcn_permlane16_swap(a, b, false, false);
+    return s[0] + s[1];
+}
+
+__device__ __forceinline__ uint32_t row16_sum(uint32_t v) {
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x128, 0xF, 0xF, false);  // row_ror:8
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x124, 0xF, 0xF, false);  // row_ror:4
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x122, 0xF, 0xF, false);  // row_ror:2
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x121, 0xF, 0xF, false);  // row_ror:1
+    return v;
+}
+
+__device__ __forceinline__ double readlane_f64(double v, int lane) {
+    const uint64_t b = (uint64_t)__double_as_longlong(v);
+    const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)b, lane);
+    const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(b >> 32), lane);
+    return __longlong_as_double((int64_t)(((uint64_t)hi << 32) | lo));
+}
+
+// ln_requant_fast with the zero point, the 1/2 and a 512 offset folded into
+// the addend; returns Y + 512.
+__device__ __forceinline__ int ln_requant_rows(double A, double B, int xh, uint32_t hi_mask,
+                                               uint32_t m_add, double c, int lo, int hi) {
+    const uint32_t hiA = (uint32_t)((uint64_t)__double_as_longlong(A) >> 32);
+    const double At = __longlong_as_double((int64_t)((uint64_t)(hiA & hi_mask) << 32));
+    const double M = __longlong_as_double((int64_t)((uint64_t)((hiA & 0x7FF00000u) + m_add) << 32));
+    const double Bc = ((B + M) - M) + c;
+    const double v = fma(At, (double)xh, Bc);
+    int q;
+    asm("v_cvt_i32_f64 %0, %1" : "=v"(q) : "v"(v));
+    asm("v_med3_i32 %0, %1, %2, %3" : "=v"(q) : "v"(q), "s"(lo), "v"(hi));
+    return q;
+}
+
+// Rows r0 .. r0 + nr - 1 of the lane's dwords (zeros elsewhere; nr may be 0).
+template <int W>
+__device__ __forceinline__ void load_rows(uint32_t (&xv)[kRowBatch][W], const uint32_t* x32,
+                                          int64_t r0, int nr, int nd, int lane,
+                                          const bool (&ok)[W]) {
+#pragma unroll
+    for (int j = 0; j < kRowBatch; ++j) {
+        const uint32_t* xr = x32 + (r0 + (j < nr ? j : 0)) * nd + lane;
+#pragma unroll
+        for (int w = 0; w < W; ++w)
+            xv[j][w] = (j < nr && ok[w]) ? __builtin_nontemporal_load(xr + 64 * w) : 0u;
+    }
+}
+
+// Workgroup size: 1024 (one per CU, 4 waves per SIMD within 128 VGPRs), or
+// 512 for W = 4, whose registers exceed that budget.
+constexpr int rows_block(int W) { return W >= 4 ? 512 : 1024; }
+
+template <int W>
+__global__ __launch_bounds__(rows_block(W)) void ln_rows_kernel(LnArgs a) {
+    extern __shared__ double smem[];
+    double2* s_gb = reinterpret_cast<double2*>(smem);        // (gs, bs) at [b][dword]
+    uint4* s_pk = reinterpret_cast<uint4*>(s_gb + a.C);      // per dword, see below
+    const int nd = a.C >> 2;
+    const int lane = threadIdx.x & 63;
+    const uint32_t* x32 = reinterpret_cast<const uint32_t*>(a.x);
+    uint32_t* y32 = reinterpret_cast<uint32_t*>(a.y);
+
+    // Contiguous run of rows of this wavefront.  Wavefronts are numbered
+    // across workgroups first, so that the ones with an extra row (the
+    // remainder of T / nw) spread over all CUs.
+    constexpr int kWaves = rows_block(W) / 64;
+    const int64_t nw = (int64_t)gridDim.x * kWaves;
+    const int64_t gw = (int64_t)(threadIdx.x >> 6) * gridDim.x + blockIdx.x;
+    const int64_t base = a.T / nw, rem = a.T % nw;
+    int64_t r0 = gw * base + min(gw, rem);
+    const int64_t r1 = r0 + base + (gw < rem ? 1 : 0);
+    bool ok[W];
+#pragma unroll
+    for (int w = 0; w < W; ++w) ok[w] = lane + 64 * w < nd;
+
+    // The first batch is requested before the set-up, which it does not need.
+    uint32_t xv[kRowBatch][W];
+    int nr = (int)min<int64_t>(kRowBatch, r1 - r0);
+    load_rows<W>(xv, x32, r0, nr, nd, lane, ok);
+
+    // Set-up, one thread per dword (4 channels): gs = gamma / s_out and
+    // bs = beta / s_out in binary64, and packed per-dword constants with
+    // u = zp_in + 128:
+    //   s_pk[2 dw]     = i16 pairs of 2^alpha (channels 0,1 and 2,3),
+    //                    i16 pairs of -u 2^alpha (same order)
+    //   s_pk[2 dw + 1] = bytes of 2^alpha, sum of -u 2^alpha, and the largest
+    //                    and smallest high word of |gs| over the 4 channels
+    const int u = a.zp_in + 128;
+    for (int dw = threadIdx.x; dw < nd; dw += blockDim.x) {
+        uint32_t mulp[2] = {0, 0}, zmp[2] = {0, 0}, mulb = 0, m1p = 0, ghi = 0, glo = 0x7FF00000u;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            const int c = 4 * dw + b;
+            const double gs = (double)a.gamma[c] / (double)a.s_out;
+            s_gb[b * nd + dw] = double2{gs, (double)a.beta[c] / (double)a.s_out};
+            const int sh = min((int)a.alpha[c], a.K);
+            const uint32_t zm = (uint32_t)(-u) << sh;
+            mulb |= (1u << sh) << (8 * b);
+            mulp[b >> 1] |= (1u << sh) << (16 * (b & 1));
+            zmp[b >> 1] |= (zm & 0xFFFFu) << (16 * (b & 1));
+            m1p += zm;
+            const uint32_t h = (uint32_t)((uint64_t)__double_as_longlong(gs) >> 32) & 0x7FFFFFFFu;
+            ghi = max(ghi, h);
+            glo = min(glo, h);
+        }
+        s_pk[2 * dw] = uint4{mulp[0], mulp[1], zmp[0], zmp[1]};
+        s_pk[2 * dw + 1] = uint4{mulb, m1p, ghi, glo};
+    }
+    __syncthreads();
+    if (nr <= 0) return;
+
+    uint32_t mulp[2 * W], zmp[2 * W], mulb[W];
+    uint32_t m1init = 0, ghi = 0, glo = 0x7FF00000u;
+#pragma unroll
+    for (int w = 0; w < W; ++w) {
+        const int dw = ok[w] ? lane + 64 * w : 0;
+        const uint4 p = s_pk[2 * dw];
+        const uint4 q = s_pk[2 * dw + 1];
+        mulp[2 * w] = ok[w] ? p.x : 0u;
+        mulp[2 * w + 1] = ok[w] ? p.y : 0u;
+        zmp[2 * w] = ok[w] ? p.z : 0u;
+        zmp[2 * w + 1] = ok[w] ? p.w : 0u;
+        mulb[w] = ok[w] ? q.x : 0u;
+        m1init += ok[w] ? q.y : 0u;
+        ghi = ok[w] ? max(ghi, q.z) : ghi;
+        glo = ok[w] ? min(glo, q.w) : glo;
+    }
+    // Bounds on |gs| over the lane's channels from the high words alone
+    // (|gs| <= gmaxl, |gs| >= gminl; a row whose factors come that close to a
+    // bound of the fast range takes the general path).  Zero or subnormal
+    // gs (high word 0) always takes the general path.
+    const double gmaxl = __longlong_as_double((int64_t)(((uint64_t)ghi << 32) | 0xFFFFFFFFu));
+    const double gminl = __longlong_as_double((int64_t)((uint64_t)glo << 32));
+    const bool zerol = glo == 0;
+
+    const int qlo = -(1 << (a.bits - 1));
+    const int qhi = (1 << (a.bits - 1)) - 1;
+    const uint32_t hi_mask = ~((1u << (21 - a.bits)) - 1u);
+    // one scalar, so that the exponent add stays one instruction
+    const uint32_t m_add = __builtin_amdgcn_readfirstlane(((uint32_t)(53 - a.bits) << 20) | 0x80000u);
+    const double amax = ldexp(1.0, a.bits), amin = ldexp(1.0, a.bits - 31);
+    const double cadd = (double)a.zp_out + 512.5;
+    const int lo512 = qlo + 512, hi512 = qhi + 512;
+
+    for (;;) {
+        uint32_t hp[kRowBatch][2 * W];
+        uint32_t m1[kRowBatch], m2[kRowBatch];
+#pragma unroll
+        for (int j = 0; j < kRowBatch; ++j) {
+            m1[j] = m1init;
+            m2[j] = 0;
+#pragma unroll
+            for (int w = 0; w < W; ++w) {
+                const uint32_t xu = xv[j][w] ^ 0x80808080u;
+                const uint32_t p0 = __builtin_amdgcn_perm(xu, xu, 0x0C010C00u);
+                const uint32_t p1 = __builtin_amdgcn_perm(xu, xu, 0x0C030C02u);
+                const short2_t h0 = __builtin_bit_cast(short2_t, p0) * __builtin_bit_cast(short2_t, mulp[2 * w]) +
+                                    __builtin_bit_cast(short2_t, zmp[2 * w]);
+                const short2_t h1 = __builtin_bit_cast(short2_t, p1) * __builtin_bit_cast(short2_t, mulp[2 * w + 1]) +
+                                    __builtin_bit_cast(short2_t, zmp[2 * w + 1]);
+                m1[j] = __builtin_amdgcn_udot4(xu, mulb[w], m1[j], false);
+                m2[j] = (uint32_t)__builtin_amdgcn_sdot2(h0, h0, (int)m2[j], false);
+                m2[j] = (uint32_t)__builtin_amdgcn_sdot2(h1, h1, (int)m2[j], false);
+                hp[j][2 * w] = __builtin_bit_cast(uint32_t, h0);
+                hp[j][2 * w + 1] = __builtin_bit_cast(uint32_t, h1);
+            }
+        }
+        // lane group j (lanes 16 j .. 16 j + 15) ends with row j's totals
+        const uint32_t t1 = row16_sum(swap_add16(swap_add32(m1[0], m1[2]), swap_add32(m1[1], m1[3])));
+        const uint32_t t2 = row16_sum(swap_add16(swap_add32(m2[0], m2[2]), swap_add32(m2[1], m2[3])));
+        double r, m;
+        row_factors((int64_t)(int32_t)t1, (int64_t)t2, a.C, r, m);
+
+#pragma unroll
+        for (int j = 0; j < kRowBatch; ++j) {
+            if (j >= nr) break;
+            const double rj = readlane_f64(r, 16 * j);
+            const double mj = readlane_f64(m, 16 * j);
+            uint32_t* yr = y32 + (r0 + j) * nd + lane;
+            const bool lane_fits = !zerol && gmaxl * rj < amax && gminl * rj >= amin;
+            if (rj > 0.0 && __ballot(!lane_fits) == 0) {
+#pragma unroll
+                for (int w = 0; w < W; ++w) {
+                    int q[4];
+#pragma unroll
+                    for (int b = 0; b < 4; ++b) {
+                        const uint32_t hw = hp[j][2 * w + (b >> 1)];
+                        const int xh = (b & 1) ? (int)hw >> 16 : (int)(int16_t)(hw & 0xFFFFu);
+                        const double2 gb = s_gb[b * nd + (ok[w] ? lane + 64 * w : 0)];
+                        const double A = gb.x * rj;
+                        const double B = gb.y - gb.x * mj;
+                        q[b] = ln_requant_rows(A, B, xh, hi_mask, m_add, cadd, lo512, hi512);
+                    }
+                    const uint32_t lo = __builtin_amdgcn_perm((uint32_t)q[1], (uint32_t)q[0], 0x0C0C0400u);
+                    const uint32_t hi = __builtin_amdgcn_perm((uint32_t)q[3], (uint32_t)q[2], 0x0C0C0400u);
+                    const uint32_t pack = __builtin_amdgcn_perm(hi, lo, 0x05040100u);
+                    if (ok[w]) __builtin_nontemporal_store(pack, yr + 64 * w);
+                    // one dword at a time: the f64 temporaries of all 4 W
+                    // elements would not fit the register budget
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            } else {
+                // rare (factors out of the fast range): element by element,
+                // the row's bytes read again
+                const int8_t* xrow = a.x + (r0 + j) * a.C;
+                int8_t* yrow = a.y + (r0 + j) * a.C;
+#pragma unroll 1
+                for (int c = lane; c < a.C; c += 64) {
+                    const int xh = ((int)xrow[c] - a.zp_in) * (1 << min((int)a.alpha[c], a.K));
+                    const double2 gb = s_gb[(c & 3) * nd + (c >> 2)];
+                    const double A = gb.x * rj;
+                    const double B = gb.y - gb.x * mj;
+                    yrow[c] = (int8_t)ln_requant(A, B, xh, a.bits, a.zp_out, qlo, qhi);
+                }
+            }
+        }
+        // next batch (loaded after the output: requested earlier it would
+        // stay live beside the packed X^ and spill)
+        r0 += kRowBatch;
+        nr = (int)min<int64_t>(kRowBatch, r1 - r0);
+        if (nr <= 0) break;
+        load_rows<W>(xv, x32, r0, nr, nd, lane, ok);
+    }
+}
+
+template <int W>
+hipError_t launch_rows(const LnArgs& a, hipStream_t stream) {
+    // about three rows per wavefront or more, at most one workgroup of 16
+    // wavefronts per CU
+    constexpr int kWaves = rows_block(W) / 64;
+    const int64_t waves = (a.T + 2) / 3;
+    const int64_t blocks = std::min<int64_t>((waves + kWaves - 1) / kWaves, 256 * 16 / kWaves);
+    const size_t lds = (size_t)a.C * 2 * sizeof(double) + (size_t)(a.C / 4) * 2 * sizeof(uint4);
+    launch_kernel(ln_rows_kernel<W>, dim3((unsigned)blocks), dim3(rows_block(W)), lds, stream, a);
+    return hipGetLastError();
+}
+
 template <int W>
 hipError_t launch_fast(const LnArgs& a, int lshift, bool wide, hipStream_t stream) {
     const int R = 64 >> lshift;
@@ -321,6 +597,18 @@ hipError_t launch_ptf_layernorm(const LnArgs& a, hipStream_t stream) {
     const bool aligned = ((reinterpret_cast<uintptr_t>(a.x) | reinterpret_cast<uintptr_t>(a.y)) & 3) == 0;
     // Lanes per row L and dwords per lane W: least padding, then the most
     // lanes per row (fewest registers, highest occupancy).
+    const int nd = a.C / 4;
+    const bool narrow = (double)a.C * 65025.0 * (double)(1 << (2 * a.K)) < 4294967296.0;
+    // Row-batch kernel for 256 <= C <= 1024 (up to 4 dwords per lane without
+    // spills) when the sums of squares fit 32 bits.
+    if (aligned && a.C % 4 == 0 && nd >= 64 && nd <= 256 && narrow) {
+        switch ((nd + 63) / 64) {
+            case 1: return launch_rows<1>(a, stream);
+            case 2: return launch_rows<2>(a, stream);
+            case 3: return launch_rows<3>(a, stream);
+            default: return launch_rows<4>(a, stream);
+        }
+    }
     int best_l = -1, best_w = 0, best_waste = 1 << 30;
     if (aligned && a.C % 4 == 0) {
         for (int l = 6; l >= 0; --l) {

@@ -56,7 +56,10 @@ def _ln_ref(orc, d, **over):
 
 
 LN_SHAPES = [(1, 192), (7, 96), (197, 192), (333, 384), (64, 768), (100, 1024), (37, 100),
-             (9, 13), (5, 2048), (3, 4096), (2, 8192), (65, 4), (3, 1), (70, 2000)]
+             (9, 13), (5, 2048), (3, 4096), (2, 8192), (65, 4), (3, 1), (70, 2000),
+             # row-batch kernel (256 <= C <= 1024): one row, partial batches,
+             # several batches per wavefront, idle lanes in the last dword
+             (1, 768), (5, 256), (4099, 260), (20000, 256), (9001, 1020), (16400, 512)]
 
 
 @pytest.mark.parametrize("T,C", LN_SHAPES)
@@ -101,6 +104,23 @@ def test_ln_edge_rows(fq, orc):
     for s_out in (d["s_out"], 1e-6, 1e3, 0.5):
         over = dict(x_q=x, gamma=gamma, beta=beta, s_out=s_out)
         assert np.array_equal(_ln_gpu(fq, d, **over), _ln_ref(orc, d, **over)), s_out
+
+
+def test_ln_mixed_fast_and_general_rows(fq, orc):
+    """Rows whose factors leave the fast range (near-constant rows: tiny
+    variance, huge 1/sigma) between ordinary rows, so that batches of four
+    rows mix both output paths."""
+    say("ln mixed rows")
+    d = W.ln_inputs(4099, 768, seed=12)
+    x = d["x_q"].copy()
+    rng = np.random.default_rng(12)
+    unshifted = np.flatnonzero(np.minimum(d["alpha"], d["K"]) == 0)
+    assert unshifted.size > 0
+    for i in rng.choice(4099, size=300, replace=False):
+        x[i] = d["zp_in"]
+        x[i, int(rng.choice(unshifted))] += 1 if d["zp_in"] < 127 else -1
+    over = dict(x_q=x)
+    assert np.array_equal(_ln_gpu(fq, d, **over), _ln_ref(orc, d, **over))
 
 
 @pytest.mark.parametrize("cfg", W.CONFIGS, ids=lambda c: c.name)
