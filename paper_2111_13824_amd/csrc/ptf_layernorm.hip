@@ -414,27 +414,38 @@ __global__ __launch_bounds__(rows_block(W)) void ln_rows_kernel(LnArgs a) {
 #pragma unroll
     for (int w = 0; w < W; ++w) ok[w] = lane + 64 * w < nd;
 
-    // The first batch is requested before the set-up, which it does not need.
-    uint32_t xv[kRowBatch][W];
-    int nr = (int)min<int64_t>(kRowBatch, r1 - r0);
-    load_rows<W>(xv, x32, r0, nr, nd, lane, ok);
-
-    // Set-up, one thread per dword (4 channels): gs = gamma / s_out and
-    // bs = beta / s_out in binary64, and packed per-dword constants with
-    // u = zp_in + 128:
+    // Set-up, one thread per dword (4 channels; nd <= 256 <= blockDim): its
+    // loads go first, then the first batch of rows, so that the per-channel
+    // factors are computed while the rows stream in.
+    //   gs = gamma / s_out, bs = beta / s_out (binary64), and per-dword
+    //   constants with u = zp_in + 128:
     //   s_pk[2 dw]     = i16 pairs of 2^alpha (channels 0,1 and 2,3),
     //                    i16 pairs of -u 2^alpha (same order)
     //   s_pk[2 dw + 1] = bytes of 2^alpha, sum of -u 2^alpha, and the largest
     //                    and smallest high word of |gs| over the 4 channels
+    const int sdw = threadIdx.x;
+    float sg[4], sb[4];
+    int sa[4];
+    if (sdw < nd) {
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            sg[b] = a.gamma[4 * sdw + b];
+            sb[b] = a.beta[4 * sdw + b];
+            sa[b] = a.alpha[4 * sdw + b];
+        }
+    }
+    uint32_t xv[kRowBatch][W];
+    int nr = (int)min<int64_t>(kRowBatch, r1 - r0);
+    load_rows<W>(xv, x32, r0, nr, nd, lane, ok);
+
     const int u = a.zp_in + 128;
-    for (int dw = threadIdx.x; dw < nd; dw += blockDim.x) {
+    if (sdw < nd) {
         uint32_t mulp[2] = {0, 0}, zmp[2] = {0, 0}, mulb = 0, m1p = 0, ghi = 0, glo = 0x7FF00000u;
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
-            const int c = 4 * dw + b;
-            const double gs = (double)a.gamma[c] / (double)a.s_out;
-            s_gb[b * nd + dw] = double2{gs, (double)a.beta[c] / (double)a.s_out};
-            const int sh = min((int)a.alpha[c], a.K);
+            const double gs = (double)sg[b] / (double)a.s_out;
+            s_gb[b * nd + sdw] = double2{gs, (double)sb[b] / (double)a.s_out};
+            const int sh = min(sa[b], a.K);
             const uint32_t zm = (uint32_t)(-u) << sh;
             mulb |= (1u << sh) << (8 * b);
             mulp[b >> 1] |= (1u << sh) << (16 * (b & 1));
@@ -444,8 +455,8 @@ __global__ __launch_bounds__(rows_block(W)) void ln_rows_kernel(LnArgs a) {
             ghi = max(ghi, h);
             glo = min(glo, h);
         }
-        s_pk[2 * dw] = uint4{mulp[0], mulp[1], zmp[0], zmp[1]};
-        s_pk[2 * dw + 1] = uint4{mulb, m1p, ghi, glo};
+        s_pk[2 * sdw] = uint4{mulp[0], mulp[1], zmp[0], zmp[1]};
+        s_pk[2 * sdw + 1] = uint4{mulb, m1p, ghi, glo};
     }
     __syncthreads();
     if (nr <= 0) return;
