@@ -67,7 +67,12 @@ _SIGS = {
     "oracle_lis_attn_v_shift": [_P, _I32, _P, _I32, _I64, _I32, _I32, _I32, _I32, _P],
     "oracle_lis_attention_head": [_P, _P, _I32, _I64, _I32, _I32, _F32, _I32, _I32, _P, _I32,
                                   _I32, _P, _P, _I32],
+    "oracle_requant_dyadic_int8": [_P, _I64, _F32, _F32, _I32, _I32, _P],
 }
+
+# Rows per block of the alpha search's error sums (the oracle's reading of
+# the summation order of eq. 11).
+PTF_ERR_BLOCK = 64
 
 
 def lib() -> ctypes.CDLL:
@@ -144,6 +149,19 @@ def ptf_quantize(x: np.ndarray, s: float, zp: int, alpha: np.ndarray, b: int = 8
     _check(lib().oracle_ptf_quantize(_ptr(x), T, C, s, zp, _ptr(alpha), b, _ptr(q)),
            "ptf_quantize")
     return q
+
+
+# ---- Dyadic requantization ----------------------------------------------------
+
+def requant_dyadic_int8(q: np.ndarray, s_in: float, s_out: float, zp_out: int,
+                        bits: int = 8) -> np.ndarray:
+    """int32 accumulator of scale s_in -> b-bit activation of scale s_out in the
+    int8 container (value - 2^(b-1)), through the 31-bit dyadic form of s_in/s_out."""
+    q = np.ascontiguousarray(q, dtype=np.int32)
+    y = np.empty(q.shape, dtype=np.int8)
+    _check(lib().oracle_requant_dyadic_int8(_ptr(q), q.size, s_in, s_out, zp_out, bits, _ptr(y)),
+           "requant_dyadic_int8")
+    return y
 
 
 # ---- Supplement A.1: integer LayerNorm --------------------------------------

@@ -119,15 +119,25 @@ int oracle_ptf_alpha(const double* x, int64_t T, int32_t C, double s, int32_t zp
          * finest grid always wins.  The error is measured on the quantizer that
          * is actually used, eq. (8) with its zp and clip.  Ties go to the
          * smallest alpha. */
+        /* READING: the paper does not fix the order of the sum over t.  The
+         * squared errors are summed in blocks of ORACLE_PTF_ERR_BLOCK
+         * consecutive rows (in order within a block), and the block sums are
+         * added in block order, so that a parallel implementation can
+         * reproduce the same sums, and so the same argmin, exactly. */
         int32_t best = 0;
         double best_err = INFINITY;
         for (int32_t a = 0; a <= K; ++a) {
             const double step = ldexp(1.0, a) * s;
             double err = 0.0;
-            for (int64_t t = 0; t < T; ++t) {
-                const double xv = x[t * C + c];
-                const double deq = (ptf_q(xv, s, zp, a, levels) - (double)zp) * step;
-                err += (xv - deq) * (xv - deq);
+            for (int64_t t0 = 0; t0 < T; t0 += ORACLE_PTF_ERR_BLOCK) {
+                const int64_t t1 = t0 + ORACLE_PTF_ERR_BLOCK < T ? t0 + ORACLE_PTF_ERR_BLOCK : T;
+                double part = 0.0;
+                for (int64_t t = t0; t < t1; ++t) {
+                    const double xv = x[t * C + c];
+                    const double deq = (ptf_q(xv, s, zp, a, levels) - (double)zp) * step;
+                    part += (xv - deq) * (xv - deq);
+                }
+                err += part;
             }
             if (err < best_err) {
                 best_err = err;
@@ -147,6 +157,48 @@ int oracle_ptf_quantize(const double* x, int64_t T, int32_t C, double s, int32_t
     for (int64_t t = 0; t < T; ++t)
         for (int32_t c = 0; c < C; ++c)
             q[t * C + c] = (int32_t)ptf_q(x[t * C + c], s, zp, alpha[c], levels);
+    return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Dyadic requantization of an int32 accumulator to a b-bit activation        */
+/* ------------------------------------------------------------------------ */
+
+/* The integer-only requantization of the LayerNorm output in Supplement A.1
+ * (a real multiplier replaced by N2 / 2^N1, then a rounding shift), applied
+ * to an accumulator of scale s_in, e.g. the BitShift product of Sec. 3.3
+ * (scale s_V / 2^N), to give the next layer's b-bit input of scale s_out.
+ * READING: the precision of N2 for this step is not given; N2 keeps 31
+ * significant bits of M = s_in / s_out, i.e.
+ *   N1 = clamp(31 - e, 0, 62) with M = f 2^e, f in [0.5, 1),
+ *   N2 = min(floor(M 2^N1), 2^31 - 1),
+ *   y  = clip(floor((N2 q + 2^(N1-1)) / 2^N1) + zp_out, 0, 2^b - 1)
+ * (round half up, as for the LayerNorm output). */
+int oracle_requant_dyadic_int8(const int32_t* q, int64_t n, float s_in, float s_out,
+                               int32_t zp_out, int32_t bits, int8_t* y) {
+    if (n < 0 || bits < 2 || bits > 8 || !(s_in > 0.0f) || !(s_out > 0.0f)) return ORACLE_ERR_ARG;
+    if (n == 0) return ORACLE_OK;
+    if (!q || !y) return ORACLE_ERR_ARG;
+    const int64_t half = (int64_t)1 << (bits - 1);
+    const int64_t levels = ((int64_t)1 << bits) - 1;
+    const int64_t zp = (int64_t)zp_out + half;      /* container -> paper grid */
+    if (zp < 0 || zp > levels) return ORACLE_ERR_ARG;
+
+    const double M = (double)s_in / (double)s_out;
+    int e = 0;
+    (void)frexp(M, &e);
+    int64_t N1 = 31 - (int64_t)e;
+    N1 = clip_i64(N1, 0, 62);
+    double n2 = floor(ldexp(M, (int)N1));
+    if (n2 > 2147483647.0) n2 = 2147483647.0;
+    const int64_t N2 = (int64_t)n2;
+    for (int64_t i = 0; i < n; ++i) {
+        const __int128 prod = (__int128)N2 * (__int128)q[i];
+        const __int128 w = N1 > 0 ? (prod + ((__int128)1 << (N1 - 1))) >> N1 : prod;
+        const __int128 yu = w + zp;
+        const int64_t yc = yu < 0 ? 0 : (yu > levels ? levels : (int64_t)yu);
+        y[i] = (int8_t)(yc - half);
+    }
     return ORACLE_OK;
 }
 

@@ -48,12 +48,22 @@ int oracle_minmax_quantize(const double* x, int64_t n, double s, int32_t zp, int
 /* Layer-wise s (eq. 9) and zp (eq. 10) over a row-major [T, C] tensor. */
 int oracle_ptf_params(const double* x, int64_t T, int32_t C, int32_t b, int32_t K,
                       double* s, int32_t* zp);
-/* Per-channel alpha by the argmin of eq. (11) over {0..K}. */
+/* Per-channel alpha by the argmin of eq. (11) over {0..K}; each channel's
+ * squared errors are summed in blocks of ORACLE_PTF_ERR_BLOCK rows. */
+#define ORACLE_PTF_ERR_BLOCK 64
 int oracle_ptf_alpha(const double* x, int64_t T, int32_t C, double s, int32_t zp,
                      int32_t b, int32_t K, uint8_t* alpha);
 /* X_Q = clip(round(X / (2^alpha_c s)) + zp, 0, 2^b - 1) (eq. 8), unsigned grid. */
 int oracle_ptf_quantize(const double* x, int64_t T, int32_t C, double s, int32_t zp,
                         const uint8_t* alpha, int32_t b, int32_t* q);
+
+/* ---- Dyadic requantization (the integer form of Supplement A.1) ------ */
+
+/* y = clip(round((N2 / 2^N1) q) + zp_out) with N2 / 2^N1 the 31-bit dyadic
+ * form of s_in / s_out; y and zp_out in the int8 container of b-bit values
+ * (value - 2^(b-1)).  bits in [2, 8]. */
+int oracle_requant_dyadic_int8(const int32_t* q, int64_t n, float s_in, float s_out,
+                               int32_t zp_out, int32_t bits, int8_t* y);
 
 /* ---- Supplement A.1: integer-only PTF LayerNorm ---------------------- */
 

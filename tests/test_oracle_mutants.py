@@ -49,6 +49,15 @@ MUTANTS = [
     ("ptf_scale_times_2K", "(mx - mn) / levels / two_K", "(mx - mn) / levels * two_K"),
     ("ptf_quant_neg_alpha", "x / (ldexp(1.0, alpha) * s)", "x / (ldexp(1.0, -alpha) * s)"),
     ("minmax_zp_sign", "round_nearest(-l / *s)", "round_nearest(l / *s)"),
+    ("alpha_tail_block_dropped", "t0 < T; t0 += ORACLE_PTF_ERR_BLOCK",
+     "t0 + ORACLE_PTF_ERR_BLOCK <= T; t0 += ORACLE_PTF_ERR_BLOCK"),
+    ("alpha_deq_zp_dropped", "(ptf_q(xv, s, zp, a, levels) - (double)zp) * step",
+     "ptf_q(xv, s, zp, a, levels) * step"),
+    ("alpha_argmax", "if (err < best_err) {", "if (err > best_err || a == 0) {"),
+    ("requant_precision_16", "int64_t N1 = 31 - (int64_t)e;", "int64_t N1 = 16 - (int64_t)e;"),
+    ("requant_round_down", "(prod + ((__int128)1 << (N1 - 1))) >> N1", "prod >> N1"),
+    ("requant_zp_dropped", "const __int128 yu = w + zp;", "const __int128 yu = w + half;"),
+    ("requant_inverse_scale", "(double)s_in / (double)s_out", "(double)s_out / (double)s_in"),
 ]
 
 

@@ -349,6 +349,117 @@ def test_ptf_alpha_search_outliers(orc):
     assert np.all(np.diff(alpha[np.argsort(rng_c)].astype(int)) >= -1)
 
 
+def _exact_ptf_errors(x, s, zp, K, b=8):
+    """Exact rational squared errors of eq. (11) per channel and alpha: the
+    quantized value from the exact quotient (half to even), then the exact
+    residual.  Returns (errors [C][K+1], set of (c, alpha) whose quotient is
+    within 2^-40 of a rounding tie, where a double quotient may round the
+    other way)."""
+    from fractions import Fraction as F
+    levels = 2 ** b - 1
+    S = F(s)
+    T, C = x.shape
+    err = [[F(0)] * (K + 1) for _ in range(C)]
+    fragile = set()
+    for c in range(C):
+        for a in range(K + 1):
+            step = S * 2 ** a
+            tot = F(0)
+            for t in range(T):
+                xv = F(float(x[t, c]))
+                r = xv / step
+                fl = r.numerator // r.denominator
+                frac = r - fl
+                if abs(frac - F(1, 2)) < F(1, 2 ** 40):
+                    fragile.add((c, a))
+                q = fl + (1 if frac > F(1, 2) or (frac == F(1, 2) and fl % 2 == 1) else 0)
+                q = min(max(q + zp, 0), levels)
+                tot += (xv - (q - zp) * step) ** 2
+            err[c][a] = tot
+    return err, fragile
+
+
+def test_ptf_alpha_matches_exact_argmin(orc):
+    """The alpha search against exact rational arithmetic: wherever the exact
+    errors of the best and the runner-up differ by more than 1e-9 relative, the
+    oracle's double sums in 64-row blocks cannot reorder them and its argmin
+    must be the exact one.  T = 150 leaves a partial last block; channel 0 has
+    all its information in that block, channel 1 is all zeros (every alpha
+    exact: the tie goes to alpha = 0)."""
+    rng = np.random.default_rng(41)
+    T, C, K = 150, 12, 3
+    x = (rng.standard_normal((T, C)) * np.exp(rng.uniform(np.log(0.05), np.log(2.5), C))).astype(np.float32)
+    x[:, 4] *= 40.0
+    x[:128, 0] = 0.0
+    x[128:, 0] = rng.uniform(-30, 30, T - 128).astype(np.float32)
+    x[:, 1] = 0.0
+    xd = x.astype(np.float64)
+    s, zp = orc.ptf_params(xd, b=8, K=K)
+    alpha = orc.ptf_alpha(xd, s, zp, b=8, K=K)
+    err, fragile = _exact_ptf_errors(x, s, zp, K)
+    assert alpha[1] == 0
+    checked = 0
+    for c in range(C):
+        order = sorted(range(K + 1), key=lambda a: (err[c][a], a))
+        best, second = order[0], order[1]
+        if any((c, a) in fragile for a in range(K + 1)):
+            continue
+        gap = err[c][second] - err[c][best]
+        if gap == 0 or gap > 1e-9 * max(err[c][second], 1e-300):
+            assert alpha[c] == best, (c, [float(e) for e in err[c]])
+            checked += 1
+    assert checked >= C - 1
+    assert alpha[0] != 0          # decided by the partial last block alone
+
+
+# ---------------------------------------------------------------------------
+# Dyadic requantization
+# ---------------------------------------------------------------------------
+
+def _round_half_up(fr):
+    return (fr + Fraction(1, 2)).numerator // (fr + Fraction(1, 2)).denominator
+
+
+def test_requant_power_of_two_is_exact(orc):
+    """A power-of-two multiplier has an exact dyadic form: the output is the
+    exact q 2^k rounded half up, plus zp, clipped to the b-bit grid."""
+    q = np.arange(-70000, 70000, 7, dtype=np.int32)
+    for k in (-12, -5, -1, 0, 1, 3):
+        for bits, zp in ((8, 0), (8, -100), (8, 127), (4, -3), (2, 1)):
+            y = orc.requant_dyadic_int8(q, float(2.0 ** k), 1.0, zp, bits)
+            half, levels = 2 ** (bits - 1), 2 ** bits - 1
+            ref = [min(max(_round_half_up(Fraction(int(v)) * Fraction(2) ** k) + zp + half, 0), levels) - half
+                   for v in q]
+            assert np.array_equal(y.astype(np.int64), np.array(ref)), (k, bits, zp)
+
+
+def test_requant_matches_exact_product_within_31_bits(orc):
+    """For any multiplier M = s_in / s_out, the output equals round-half-up of
+    the exact q M wherever q M + 1/2 is farther than |q| M 2^-30 (the bound of
+    a 31-bit truncation of M) from an integer, and is never more than one
+    step from it.  q is drawn so that q M covers the output range."""
+    rng = np.random.default_rng(43)
+    for s_in, s_out in ((0.02 / 32768, 0.013), (3.0e-7, 0.5), (1.0, 3.0), (7.0, 0.001)):
+        s_in32, s_out32 = np.float32(s_in), np.float32(s_out)
+        M = Fraction(float(s_in32)) / Fraction(float(s_out32))
+        span = rng.uniform(-300.0, 300.0, size=3000) / float(M)
+        q = np.clip(np.rint(span), -(2 ** 31), 2 ** 31 - 1).astype(np.int64).astype(np.int32)
+        q[:4] = [0, 1, -1, 2 ** 31 - 1]
+        for zp in (0, -17):
+            y = orc.requant_dyadic_int8(q, float(s_in32), float(s_out32), zp).astype(np.int64)
+            n_exact = 0
+            for v, got in zip(q, y):
+                exact = Fraction(int(v)) * M
+                r = _round_half_up(exact)
+                ref = min(max(r + zp + 128, 0), 255) - 128
+                assert abs(got - ref) <= 1
+                f = exact + Fraction(1, 2) - r          # in [0, 1)
+                if min(f, 1 - f) > abs(int(v)) * M * Fraction(1, 2 ** 30):
+                    assert got == ref, (s_in, s_out, int(v))
+                    n_exact += 1
+            assert n_exact > 0.99 * len(q)
+
+
 # ---------------------------------------------------------------------------
 # Integer LayerNorm with PTF (Supplement A.1)
 # ---------------------------------------------------------------------------
