@@ -26,6 +26,7 @@
 #ifndef FQVIT_H
 #define FQVIT_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -53,7 +54,9 @@ int32_t fq_version(void);
  * launched by the next entry-point call made on the calling thread: `start`
  * then records that kernel's start and `stop` its end (hipExtLaunchKernel
  * semantics), so hipEventElapsedTime gives the kernel's own duration with no
- * extra packets on the stream.  Every entry point launches at most one kernel.
+ * extra packets on the stream.  Every other entry point launches one kernel.
+ * ptf_calibrate, which launches four kernels, records `start` on the first and
+ * `stop` on the last, so the interval covers the whole calibration.
  * The events are consumed by that next call whatever it returns; a call that
  * enqueues nothing (empty tensors, failed validation) leaves them unrecorded.
  * Always returns FQ_OK.
@@ -148,6 +151,70 @@ fq_status lis_attention_head(const int32_t* logits, const int32_t* bias, int32_t
                              int64_t G, int32_t Lq, int32_t Lk, float s_logit, int32_t bits,
                              int32_t exp_n, const int8_t* v, int32_t zp_v, int32_t d,
                              int32_t* out, uint8_t* codes_out, int32_t ld_codes, void* stream);
+
+/*
+ * PTF calibration (Sec. 3.2): the layer-wise scale and zero point of eq. (9),
+ * (10) from the minimum and maximum of x, then each channel's power-of-two
+ * factor alpha_c by the argmin of eq. (11) over {0 .. K}, the squared error of
+ * the quantizer of eq. (8) itself (its zero point and clip included).
+ *
+ *   x          [T, C] float activations (finite), T in [0, 2^24 - 256].
+ *   bits       b in [2, 8]; K in [0, 7] (the paper uses 3).
+ *   s          device double (out): s = (max - min) / (2^b - 1) / 2^K.
+ *   zp         device int32 (out), container form: clip(rint(-min / (2^K s)),
+ *              0, 2^b - 1) - 2^(b-1).
+ *   alpha      [C] uint8 (out).
+ *   workspace  device scratch of at least fq_ptf_calibrate_workspace_bytes(T,
+ *              C, K) bytes, owned by the caller; its contents on entry do not
+ *              matter and on return are unspecified.
+ * Every operation is rounded in binary64 as written; each channel's squared
+ * errors are summed in blocks of 64 consecutive rows, in order, and the block
+ * sums added in order, so alpha is a pure function of x.  Ties go to the
+ * smallest alpha.  A tensor whose maximum equals its minimum gets s = 0, the
+ * zero point 0 of the paper's grid and alpha = 0.  T = 0 enqueues nothing and
+ * leaves the outputs untouched.
+ * Errors: FQ_ERR_NULL, FQ_ERR_SHAPE (T outside [0, 2^24 - 256], C outside
+ * [1, 8192]), FQ_ERR_PARAM (bits, K, or a workspace that is too small).
+ */
+size_t fq_ptf_calibrate_workspace_bytes(int64_t T, int32_t C, int32_t K);
+fq_status ptf_calibrate(const float* x, int64_t T, int32_t C, int32_t bits, int32_t K, double* s,
+                        int32_t* zp, uint8_t* alpha, void* workspace, size_t workspace_bytes,
+                        void* stream);
+
+/*
+ * PTF quantizer (Sec. 3.2, eq. 8): X_Q = clip(rint(x / (2^alpha_c s)) + zp,
+ * 0, 2^b - 1), in binary64, stored in the int8 container.
+ *
+ *   x      [T, C] float; s, zp: device scalars as written by ptf_calibrate
+ *          (zp in container form); alpha [C] uint8; bits b in [2, 8].
+ *   x_q    [T, C] int8 container output (the input of ptf_layernorm_int8).
+ * s <= 0 (a degenerate calibration) stores zp everywhere.
+ * Errors: FQ_ERR_NULL, FQ_ERR_SHAPE (T < 0, C outside [1, 8192]),
+ * FQ_ERR_PARAM (bits).
+ */
+fq_status ptf_quantize_int8(const float* x, int64_t T, int32_t C, const double* s,
+                            const int32_t* zp, const uint8_t* alpha, int32_t bits, int8_t* x_q,
+                            void* stream);
+
+/*
+ * Dyadic requantization of an int32 accumulator to a b-bit activation, the
+ * integer-only form of Supplement A.1 (a real multiplier replaced by
+ * N2 / 2^N1 and a rounding shift), e.g. for the BitShift Attn x V output of
+ * lis_attention_head (scale s_V / 2^(2^b - 1)) feeding the next layer.
+ *
+ *   q       [n] int32 with scale s_in.
+ *   s_in, s_out  positive finite scales; zp_out the output zero point,
+ *           container form.  bits b in [2, 8].
+ *   y       [n] int8 container output.
+ * With M = s_in / s_out in binary64, M = f 2^e (f in [0.5, 1)),
+ * N1 = clamp(31 - e, 0, 62), N2 = min(floor(M 2^N1), 2^31 - 1):
+ * y = clip(floor((N2 q + 2^(N1-1)) / 2^N1) + zp_out) (no half term when
+ * N1 = 0), exact in 64-bit integers.
+ * Errors: FQ_ERR_NULL, FQ_ERR_SHAPE (n < 0), FQ_ERR_PARAM (bits, a scale or
+ * zp_out out of range).
+ */
+fq_status requant_dyadic_int8(const int32_t* q, int64_t n, float s_in, float s_out,
+                              int32_t zp_out, int32_t bits, int8_t* y, void* stream);
 
 #ifdef __cplusplus
 }

@@ -26,6 +26,9 @@ SIGNATURES = {
     "lis_attn_v_shift": [_P, _I32, _P, _I32, _I64, _I32, _I32, _I32, _I32, _P, _P],
     "lis_attention_head": [_P, _P, _I32, _I64, _I32, _I32, _F32, _I32, _I32, _P, _I32, _I32, _P,
                            _P, _I32, _P],
+    "ptf_calibrate": [_P, _I64, _I32, _I32, _I32, _P, _P, _P, _P, ctypes.c_size_t, _P],
+    "ptf_quantize_int8": [_P, _I64, _I32, _P, _P, _P, _I32, _P, _P],
+    "requant_dyadic_int8": [_P, _I64, _F32, _F32, _I32, _I32, _P, _P],
 }
 
 
@@ -56,6 +59,8 @@ def lib() -> ctypes.CDLL:
         L.fq_version.restype = ctypes.c_int32
         L.fq_time_next_call.argtypes = [_P, _P]
         L.fq_time_next_call.restype = ctypes.c_int32
+        L.fq_ptf_calibrate_workspace_bytes.argtypes = [_I64, _I32, _I32]
+        L.fq_ptf_calibrate_workspace_bytes.restype = ctypes.c_size_t
         _lib = L
     return _lib
 
@@ -222,3 +227,59 @@ def lis_attention_head(logits, v, s_logit: float, bits: int = 4, exp_n: int = 20
             _dev_ptr(out, torch.int32, "out", 3),
             _dev_ptr(codes_out, torch.uint8, "codes_out", 3), ld, _stream(stream, logits))
     return _invoke("lis_attention_head", args, (logits, bias, v, out, codes_out), prepare, out)
+
+
+def ptf_calibrate_workspace_bytes(T: int, C: int, K: int = 3) -> int:
+    """Bytes of device scratch that ptf_calibrate needs (0 for invalid sizes)."""
+    return int(lib().fq_ptf_calibrate_workspace_bytes(T, C, K))
+
+
+def ptf_calibrate(x, bits: int = 8, K: int = 3, s=None, zp=None, alpha=None, workspace=None,
+                  stream=None, prepare: bool = False):
+    """PTF calibration of a float [T, C] tensor: returns (s, zp, alpha) as device
+    tensors (float64 [1], int32 [1] in container form, uint8 [C]).  The
+    workspace is allocated here with torch when not given."""
+    import torch
+    T, C = x.shape
+    dev = x.device
+    s = torch.empty(1, dtype=torch.float64, device=dev) if s is None else s
+    zp = torch.empty(1, dtype=torch.int32, device=dev) if zp is None else zp
+    alpha = torch.empty(C, dtype=torch.uint8, device=dev) if alpha is None else alpha
+    need = ptf_calibrate_workspace_bytes(T, C, K) if T > 0 else 0
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    args = (_dev_ptr(x, torch.float32, "x", 2), T, C, bits, K,
+            _dev_ptr(s, torch.float64, "s", 1), _dev_ptr(zp, torch.int32, "zp", 1),
+            _dev_ptr(alpha, torch.uint8, "alpha", 1), _dev_ptr(workspace, torch.uint8, "workspace", 1),
+            workspace.numel(), _stream(stream, x))
+    return _invoke("ptf_calibrate", args, (x, s, zp, alpha, workspace), prepare, (s, zp, alpha))
+
+
+def ptf_quantize_int8(x, s, zp, alpha, bits: int = 8, x_q=None, stream=None,
+                      prepare: bool = False):
+    """PTF quantization of a float [T, C] tensor with device scalars s, zp (as
+    returned by ptf_calibrate) and alpha [C]; returns (or fills) int8 [T, C]."""
+    import torch
+    T, C = x.shape
+    if x_q is None:
+        x_q = torch.empty((T, C), dtype=torch.int8, device=x.device)
+    if alpha.shape != (C,) or x_q.shape != (T, C):
+        raise ValueError("alpha must be [C] and x_q [T, C]")
+    args = (_dev_ptr(x, torch.float32, "x", 2), T, C, _dev_ptr(s, torch.float64, "s", 1),
+            _dev_ptr(zp, torch.int32, "zp", 1), _dev_ptr(alpha, torch.uint8, "alpha", 1), bits,
+            _dev_ptr(x_q, torch.int8, "x_q", 2), _stream(stream, x))
+    return _invoke("ptf_quantize_int8", args, (x, s, zp, alpha, x_q), prepare, x_q)
+
+
+def requant_dyadic_int8(q, s_in: float, s_out: float, zp_out: int, bits: int = 8, y=None,
+                        stream=None, prepare: bool = False):
+    """Dyadic requantization of an int32 tensor (any shape, contiguous) to the
+    int8 container; returns (or fills) int8 of the same shape."""
+    import torch
+    if y is None:
+        y = torch.empty(q.shape, dtype=torch.int8, device=q.device)
+    if y.shape != q.shape:
+        raise ValueError("y must have the shape of q")
+    args = (_dev_ptr(q, torch.int32, "q"), q.numel(), s_in, s_out, zp_out, bits,
+            _dev_ptr(y, torch.int8, "y"), _stream(stream, q))
+    return _invoke("requant_dyadic_int8", args, (q, y), prepare, y)

@@ -14,6 +14,9 @@ namespace {
 constexpr int32_t kMaxC = 8192;
 constexpr int32_t kMaxLk = 4096;
 constexpr int32_t kMaxD = 256;
+// The alpha search's grid has one y index per 4 blocks of 64 rows: at most
+// 65535 of them.
+constexpr int64_t kMaxCalibT = ((int64_t)1 << 24) - 256;
 
 fq_status from_hip(hipError_t e) { return e == hipSuccess ? FQ_OK : FQ_ERR_HIP; }
 
@@ -78,6 +81,10 @@ bool grid_fits(int64_t G, int32_t Lq, int32_t rows_per_block) {
 }  // namespace
 
 const fqvit::LaunchEvents& fqvit::launch_events() { return t_events; }
+void fqvit::set_launch_events(hipEvent_t start, hipEvent_t stop) {
+    t_events.start = start;
+    t_events.stop = stop;
+}
 
 extern "C" {
 
@@ -185,6 +192,59 @@ fq_status lis_attention_head(const int32_t* logits, const int32_t* bias, int32_t
     a.codes = codes_out;
     a.ld_codes = codes_out ? ld_codes : 0;
     return from_hip(fqvit::launch_lis(a, (hipStream_t)stream));
+}
+
+size_t fq_ptf_calibrate_workspace_bytes(int64_t T, int32_t C, int32_t K) {
+    if (T < 1 || T > kMaxCalibT || C < 1 || C > kMaxC || K < 0 || K > 7) return 0;
+    return fqvit::ptf_calibrate_workspace_bytes(T, C, K);
+}
+
+fq_status ptf_calibrate(const float* x, int64_t T, int32_t C, int32_t bits, int32_t K, double* s,
+                        int32_t* zp, uint8_t* alpha, void* workspace, size_t workspace_bytes,
+                        void* stream) {
+    ConsumeEvents consume;
+    if (T < 0 || T > kMaxCalibT || C < 1 || C > kMaxC) return FQ_ERR_SHAPE;
+    if (bits < 2 || bits > 8 || K < 0 || K > 7) return FQ_ERR_PARAM;
+    if (T == 0) return FQ_OK;
+    if (!x || !s || !zp || !alpha || !workspace) return FQ_ERR_NULL;
+    if (workspace_bytes < fqvit::ptf_calibrate_workspace_bytes(T, C, K)) return FQ_ERR_PARAM;
+    fqvit::PtfCalibArgs a{x, T, C, bits, K, s, zp, alpha, workspace};
+    return from_hip(fqvit::launch_ptf_calibrate(a, (hipStream_t)stream));
+}
+
+fq_status ptf_quantize_int8(const float* x, int64_t T, int32_t C, const double* s,
+                            const int32_t* zp, const uint8_t* alpha, int32_t bits, int8_t* x_q,
+                            void* stream) {
+    ConsumeEvents consume;
+    if (T < 0 || C < 1 || C > kMaxC) return FQ_ERR_SHAPE;
+    if (bits < 2 || bits > 8) return FQ_ERR_PARAM;
+    if (T == 0) return FQ_OK;
+    if (!x || !s || !zp || !alpha || !x_q) return FQ_ERR_NULL;
+    fqvit::PtfQuantArgs a{x, T, C, s, zp, alpha, bits, x_q};
+    return from_hip(fqvit::launch_ptf_quantize(a, (hipStream_t)stream));
+}
+
+fq_status requant_dyadic_int8(const int32_t* q, int64_t n, float s_in, float s_out,
+                              int32_t zp_out, int32_t bits, int8_t* y, void* stream) {
+    ConsumeEvents consume;
+    if (n < 0) return FQ_ERR_SHAPE;
+    if (bits < 2 || bits > 8) return FQ_ERR_PARAM;
+    if (!(s_in > 0.0f) || !std::isfinite(s_in) || !(s_out > 0.0f) || !std::isfinite(s_out))
+        return FQ_ERR_PARAM;
+    const int32_t half = 1 << (bits - 1);
+    if (zp_out < -half || zp_out >= half) return FQ_ERR_PARAM;
+    if (n == 0) return FQ_OK;
+    if (!q || !y) return FQ_ERR_NULL;
+    // N2 / 2^N1: the 31-bit dyadic form of M = s_in / s_out.
+    const double M = (double)s_in / (double)s_out;
+    int e = 0;
+    (void)std::frexp(M, &e);
+    int64_t N1 = 31 - (int64_t)e;
+    N1 = N1 < 0 ? 0 : (N1 > 62 ? 62 : N1);
+    double n2 = std::floor(std::ldexp(M, (int)N1));
+    if (n2 > 2147483647.0) n2 = 2147483647.0;
+    fqvit::RequantArgs a{q, n, (int64_t)n2, (int32_t)N1, zp_out, bits, y};
+    return from_hip(fqvit::launch_requant(a, (hipStream_t)stream));
 }
 
 }  // extern "C"

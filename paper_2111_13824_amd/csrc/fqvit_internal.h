@@ -15,6 +15,9 @@ struct LaunchEvents {
     hipEvent_t stop = nullptr;
 };
 const LaunchEvents& launch_events();
+// Replaces the current call's events (for entry points that launch several
+// kernels: the start event goes on the first, the stop event on the last).
+void set_launch_events(hipEvent_t start, hipEvent_t stop);
 
 // Every kernel launch of the library goes through here so that the events, if
 // any, record the kernel's own start and end.
@@ -105,5 +108,50 @@ struct AvArgs {
 };
 
 hipError_t launch_attn_v_shift(const AvArgs& a, hipStream_t stream);
+
+// ---------------------------------------------------------------------------
+// PTF calibration / quantization and dyadic requantization
+// ---------------------------------------------------------------------------
+
+constexpr int kPtfErrBlock = 64;     // rows per block of the alpha-search error sums
+constexpr int kMinmaxParts = 1024;   // at most this many min/max partials
+
+struct PtfCalibArgs {
+    const float* x;         // [T, C]
+    int64_t T;
+    int32_t C, bits, K;
+    double* s;              // device scalar out
+    int32_t* zp;            // device scalar out (container form)
+    uint8_t* alpha;         // [C] out
+    void* workspace;        // ptf_calibrate_workspace_bytes(T, C, K) bytes
+};
+
+size_t ptf_calibrate_workspace_bytes(int64_t T, int32_t C, int32_t K);
+hipError_t launch_ptf_calibrate(const PtfCalibArgs& a, hipStream_t stream);
+
+struct PtfQuantArgs {
+    const float* x;         // [T, C]
+    int64_t T;
+    int32_t C;
+    const double* s;        // device scalar
+    const int32_t* zp;      // device scalar (container form)
+    const uint8_t* alpha;   // [C]
+    int32_t bits;
+    int8_t* y;              // [T, C]
+};
+
+hipError_t launch_ptf_quantize(const PtfQuantArgs& a, hipStream_t stream);
+
+struct RequantArgs {
+    const int32_t* q;
+    int64_t n;
+    int64_t N2;             // in [0, 2^31 - 1]
+    int32_t N1;             // in [0, 62]
+    int32_t zp;             // container form
+    int32_t bits;
+    int8_t* y;
+};
+
+hipError_t launch_requant(const RequantArgs& a, hipStream_t stream);
 
 }  // namespace fqvit

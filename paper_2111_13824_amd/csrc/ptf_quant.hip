@@ -1,0 +1,323 @@
+// PTF calibration and quantization (Sec. 3.2, eq. 8-11) and the dyadic
+// requantization of an int32 accumulator (the integer form of Supplement A.1)
+// for gfx950.
+//
+// Calibration runs four kernels:
+//   1. minmax_partial  per-workgroup minimum and maximum of x;
+//   2. params          the layer-wise scale s = (max - min) / (2^b - 1) / 2^K
+//                      and zero point zp = clip(rint(-min / (2^K s)), 0, 2^b - 1)
+//                      in binary64 (eq. 9, 10), each operation rounded once;
+//   3. alpha_partial   for every channel c and block of 64 consecutive rows, the
+//                      squared errors of the K + 1 candidate grids summed in row
+//                      order (eq. 11 with its zero point and clip);
+//   4. alpha_final     per channel, the block sums added in block order and the
+//                      argmin over alpha (the smallest alpha on ties).
+// Steps 3 and 4 reproduce the blocked summation order exactly, so the argmin
+// is a pure function of x.  x / (2^alpha s) is computed as ldexp(x / s,
+// -alpha): scaling by a power of two commutes with the rounding of the
+// quotient, which never leaves the normal range for binary32 inputs.
+#include <cmath>
+
+#include "fqvit_internal.h"
+
+namespace fqvit {
+namespace {
+
+constexpr int kBlock = 256;
+
+typedef float vf4 __attribute__((ext_vector_type(4)));
+typedef int vi4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float wave_min(float v) {
+    for (int off = 32; off >= 1; off >>= 1) v = fminf(v, __shfl_xor(v, off, 64));
+    return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+    for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
+    return v;
+}
+
+// part[2 b], part[2 b + 1] = minimum and maximum of workgroup b's elements.
+__global__ __launch_bounds__(kBlock) void minmax_partial_kernel(const float* x, int64_t n,
+                                                                int vec4, float* part) {
+    float mn = INFINITY, mx = -INFINITY;
+    const int64_t tid = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    if (vec4) {
+        const vf4* x4 = reinterpret_cast<const vf4*>(x);
+        for (int64_t i = tid; i < n / 4; i += stride) {
+            const vf4 v = __builtin_nontemporal_load(x4 + i);
+            mn = fminf(fminf(mn, v.x), fminf(v.y, fminf(v.z, v.w)));
+            mx = fmaxf(fmaxf(mx, v.x), fmaxf(v.y, fmaxf(v.z, v.w)));
+        }
+        for (int64_t i = (n / 4) * 4 + tid; i < n; i += stride) {
+            mn = fminf(mn, x[i]);
+            mx = fmaxf(mx, x[i]);
+        }
+    } else {
+        for (int64_t i = tid; i < n; i += stride) {
+            mn = fminf(mn, x[i]);
+            mx = fmaxf(mx, x[i]);
+        }
+    }
+    __shared__ float s_mn[kBlock / 64], s_mx[kBlock / 64];
+    mn = wave_min(mn);
+    mx = wave_max(mx);
+    if ((threadIdx.x & 63) == 0) {
+        s_mn[threadIdx.x >> 6] = mn;
+        s_mx[threadIdx.x >> 6] = mx;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < kBlock / 64; ++w) {
+            mn = fminf(mn, s_mn[w]);
+            mx = fmaxf(mx, s_mx[w]);
+        }
+        part[2 * blockIdx.x] = mn;
+        part[2 * blockIdx.x + 1] = mx;
+    }
+}
+
+// One workgroup: the overall minimum and maximum, then s and zp (container
+// form) as in eq. (9), (10).  A tensor with max == min (or a non-finite
+// range) gets s = 0 and the zero point 0 of the paper's grid.
+__global__ __launch_bounds__(kBlock) void params_kernel(const float* part, int nparts, int bits,
+                                                        int K, double* s_out, int32_t* zp_out) {
+    float mn = INFINITY, mx = -INFINITY;
+    for (int i = threadIdx.x; i < nparts; i += kBlock) {
+        mn = fminf(mn, part[2 * i]);
+        mx = fmaxf(mx, part[2 * i + 1]);
+    }
+    __shared__ float s_mn[kBlock / 64], s_mx[kBlock / 64];
+    mn = wave_min(mn);
+    mx = wave_max(mx);
+    if ((threadIdx.x & 63) == 0) {
+        s_mn[threadIdx.x >> 6] = mn;
+        s_mx[threadIdx.x >> 6] = mx;
+    }
+    __syncthreads();
+    if (threadIdx.x != 0) return;
+    for (int w = 1; w < kBlock / 64; ++w) {
+        mn = fminf(mn, s_mn[w]);
+        mx = fmaxf(mx, s_mx[w]);
+    }
+    const double levels = (double)((1 << bits) - 1);
+    const double two_K = ldexp(1.0, K);
+    const double s = ((double)mx - (double)mn) / levels / two_K;
+    const int half = 1 << (bits - 1);
+    if (!(s > 0.0) || !isfinite(s)) {
+        *s_out = 0.0;
+        *zp_out = -half;
+        return;
+    }
+    const double z = fmin(fmax(rint(-(double)mn / (two_K * s)), 0.0), levels);
+    *s_out = s;
+    *zp_out = (int32_t)z - half;
+}
+
+// Workgroup (cx, ky): 64 channels cx*64 .. cx*64 + 63 (one per lane), four
+// row blocks 4 ky .. 4 ky + 3 (one per wavefront).  part[(a nb + k) C + c] =
+// sum over the rows of block k, in order, of (x - deq_a(x))^2.
+template <int KMAX>
+__global__ __launch_bounds__(kBlock) void alpha_partial_kernel(const float* x, int64_t T, int C,
+                                                               int K, int bits,
+                                                               const double* s_ptr,
+                                                               const int32_t* zp_ptr,
+                                                               int64_t nb, double* part) {
+    const int c = blockIdx.x * 64 + (threadIdx.x & 63);
+    const int64_t k = (int64_t)blockIdx.y * 4 + (threadIdx.x >> 6);
+    if (c >= C || k >= nb) return;
+    const double s = *s_ptr;
+    if (!(s > 0.0)) return;
+    const double zp = (double)(*zp_ptr + (1 << (bits - 1)));
+    const double levels = (double)((1 << bits) - 1);
+    double acc[KMAX + 1];
+#pragma unroll
+    for (int a = 0; a <= KMAX; ++a) acc[a] = 0.0;
+    const int64_t t0 = k * kPtfErrBlock;
+    const int64_t t1 = min<int64_t>(t0 + kPtfErrBlock, T);
+    const float* xc = x + c;
+    for (int64_t t = t0; t < t1; ++t) {
+        const double xv = (double)xc[t * C];
+        const double q0 = xv / s;
+#pragma unroll
+        for (int a = 0; a <= KMAX; ++a) {
+            if (a > K) break;
+            const double step = ldexp(s, a);
+            const double q = fmin(fmax(rint(ldexp(q0, -a)) + zp, 0.0), levels);
+            const double deq = (q - zp) * step;
+            const double e = xv - deq;
+            acc[a] = acc[a] + e * e;
+        }
+    }
+#pragma unroll
+    for (int a = 0; a <= KMAX; ++a)
+        if (a <= K) part[((int64_t)a * nb + k) * C + c] = acc[a];
+}
+
+// One thread per channel: block sums added in block order, argmin over alpha
+// with ties to the smallest.
+__global__ __launch_bounds__(kBlock) void alpha_final_kernel(const double* part, int C, int K,
+                                                             int64_t nb, const double* s_ptr,
+                                                             uint8_t* alpha) {
+    const int c = blockIdx.x * kBlock + threadIdx.x;
+    if (c >= C) return;
+    if (!(*s_ptr > 0.0)) {
+        alpha[c] = 0;
+        return;
+    }
+    int best = 0;
+    double best_err = INFINITY;
+    for (int a = 0; a <= K; ++a) {
+        double err = 0.0;
+        const double* p = part + (int64_t)a * nb * C + c;
+        for (int64_t k = 0; k < nb; ++k) err = err + p[k * C];
+        if (err < best_err) {
+            best_err = err;
+            best = a;
+        }
+    }
+    alpha[c] = (uint8_t)best;
+}
+
+// X_Q = clip(rint(x / (2^alpha_c s)) + zp, 0, 2^b - 1) (eq. 8), stored in the
+// int8 container.  A thread covers four consecutive channels of one row.
+// s <= 0 (a degenerate calibration) stores the zero point.
+__device__ __forceinline__ int ptf_q(float x, double s, double zp, double levels, int a) {
+    const double q = fmin(fmax(rint(ldexp((double)x / s, -a)) + zp, 0.0), levels);
+    return (int)q;
+}
+
+__global__ __launch_bounds__(kBlock) void quantize_kernel(const float* x, int64_t T, int C,
+                                                          const double* s_ptr,
+                                                          const int32_t* zp_ptr,
+                                                          const uint8_t* alpha, int bits,
+                                                          int vec4, int8_t* y) {
+    const double s = *s_ptr;
+    const int half = 1 << (bits - 1);
+    const int zpc = *zp_ptr;
+    const double zp = (double)(zpc + half);
+    const double levels = (double)((1 << bits) - 1);
+    const int cq = (C + 3) >> 2;
+    const int64_t total = T * (int64_t)cq;
+    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * kBlock) {
+        const int64_t t = i / cq;
+        const int c0 = (int)(i - t * cq) * 4;
+        const int64_t off = t * C + c0;
+        if (vec4) {
+            const vf4 v = __builtin_nontemporal_load(reinterpret_cast<const vf4*>(x + off));
+            int q[4];
+            const float xv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+            for (int b = 0; b < 4; ++b)
+                q[b] = s > 0.0 ? ptf_q(xv[b], s, zp, levels, alpha[c0 + b]) - half : zpc;
+            const uint32_t pack = ((uint32_t)q[0] & 0xFFu) | (((uint32_t)q[1] & 0xFFu) << 8) |
+                                  (((uint32_t)q[2] & 0xFFu) << 16) | ((uint32_t)q[3] << 24);
+            __builtin_nontemporal_store(pack, reinterpret_cast<uint32_t*>(y + off));
+        } else {
+            for (int b = 0; b < 4 && c0 + b < C; ++b)
+                y[off + b] = (int8_t)(s > 0.0 ? ptf_q(x[off + b], s, zp, levels, alpha[c0 + b]) - half
+                                               : zpc);
+        }
+    }
+}
+
+// y = clip(((N2 q + 2^(N1-1)) >> N1) + zp, 0, 2^b - 1) in the int8 container;
+// four elements per thread when aligned.
+__device__ __forceinline__ int requant_one(int32_t q, int64_t N2, int N1, int64_t zp, int64_t hi,
+                                           int half) {
+    const int64_t prod = N2 * (int64_t)q;
+    const int64_t w = N1 > 0 ? (prod + ((int64_t)1 << (N1 - 1))) >> N1 : prod;
+    const int64_t yu = w + zp;
+    const int64_t yc = yu < 0 ? 0 : (yu > hi ? hi : yu);
+    return (int)yc - half;
+}
+
+__global__ __launch_bounds__(kBlock) void requant_kernel(const int32_t* q, int64_t n, int64_t N2,
+                                                         int N1, int zp_c, int bits, int vec4,
+                                                         int8_t* y) {
+    const int half = 1 << (bits - 1);
+    const int64_t zp = zp_c + half;
+    const int64_t hi = (1 << bits) - 1;
+    const int64_t tid = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    if (vec4) {
+        const vi4* q4 = reinterpret_cast<const vi4*>(q);
+        uint32_t* y4 = reinterpret_cast<uint32_t*>(y);
+        for (int64_t i = tid; i < n / 4; i += stride) {
+            const vi4 v = __builtin_nontemporal_load(q4 + i);
+            const uint32_t p = ((uint32_t)requant_one(v.x, N2, N1, zp, hi, half) & 0xFFu) |
+                               (((uint32_t)requant_one(v.y, N2, N1, zp, hi, half) & 0xFFu) << 8) |
+                               (((uint32_t)requant_one(v.z, N2, N1, zp, hi, half) & 0xFFu) << 16) |
+                               ((uint32_t)requant_one(v.w, N2, N1, zp, hi, half) << 24);
+            __builtin_nontemporal_store(p, y4 + i);
+        }
+        for (int64_t i = (n / 4) * 4 + tid; i < n; i += stride)
+            y[i] = (int8_t)requant_one(q[i], N2, N1, zp, hi, half);
+    } else {
+        for (int64_t i = tid; i < n; i += stride)
+            y[i] = (int8_t)requant_one(q[i], N2, N1, zp, hi, half);
+    }
+}
+
+unsigned grid_for(int64_t work, int64_t per_block, int64_t cap) {
+    const int64_t b = (work + per_block - 1) / per_block;
+    return (unsigned)std::max<int64_t>(1, std::min<int64_t>(b, cap));
+}
+
+}  // namespace
+
+size_t ptf_calibrate_workspace_bytes(int64_t T, int32_t C, int32_t K) {
+    const int64_t nb = (T + kPtfErrBlock - 1) / kPtfErrBlock;
+    return (size_t)kMinmaxParts * 2 * sizeof(float) + (size_t)(K + 1) * nb * C * sizeof(double);
+}
+
+hipError_t launch_ptf_calibrate(const PtfCalibArgs& a, hipStream_t stream) {
+    const int64_t n = a.T * (int64_t)a.C;
+    float* mm = reinterpret_cast<float*>(a.workspace);
+    double* part = reinterpret_cast<double*>(mm + 2 * kMinmaxParts);
+    const int vec4 = ((reinterpret_cast<uintptr_t>(a.x) & 15) == 0) ? 1 : 0;
+    const unsigned nb1 = grid_for(n, (int64_t)kBlock * 16, kMinmaxParts);
+    const LaunchEvents ev = launch_events();
+    // the caller's events bracket the whole sequence: start on the first
+    // kernel, stop on the last
+    set_launch_events(ev.start, nullptr);
+    launch_kernel(minmax_partial_kernel, dim3(nb1), dim3(kBlock), 0, stream, a.x, n, vec4, mm);
+    set_launch_events(nullptr, nullptr);
+    launch_kernel(params_kernel, dim3(1), dim3(kBlock), 0, stream, (const float*)mm, (int)nb1,
+                  a.bits, a.K, a.s, a.zp);
+    const int64_t nb = (a.T + kPtfErrBlock - 1) / kPtfErrBlock;
+    const dim3 g3((unsigned)((a.C + 63) / 64), (unsigned)((nb + 3) / 4));
+    launch_kernel(alpha_partial_kernel<7>, g3, dim3(kBlock), 0, stream, a.x, a.T, a.C, a.K, a.bits,
+                  (const double*)a.s, (const int32_t*)a.zp, nb, part);
+    set_launch_events(nullptr, ev.stop);
+    launch_kernel(alpha_final_kernel, dim3((unsigned)((a.C + kBlock - 1) / kBlock)), dim3(kBlock), 0,
+                  stream, (const double*)part, a.C, a.K, nb, (const double*)a.s, a.alpha);
+    set_launch_events(nullptr, nullptr);
+    return hipGetLastError();
+}
+
+hipError_t launch_ptf_quantize(const PtfQuantArgs& a, hipStream_t stream) {
+    const int vec4 = (a.C % 4 == 0 && (reinterpret_cast<uintptr_t>(a.x) & 15) == 0 &&
+                      (reinterpret_cast<uintptr_t>(a.y) & 3) == 0)
+                         ? 1
+                         : 0;
+    const int64_t work = a.T * (int64_t)((a.C + 3) / 4);
+    launch_kernel(quantize_kernel, dim3(grid_for(work, kBlock * 4, 8192)), dim3(kBlock), 0, stream,
+                  a.x, a.T, a.C, a.s, a.zp, a.alpha, a.bits, vec4, a.y);
+    return hipGetLastError();
+}
+
+hipError_t launch_requant(const RequantArgs& a, hipStream_t stream) {
+    const int vec4 = ((reinterpret_cast<uintptr_t>(a.q) & 15) == 0 &&
+                      (reinterpret_cast<uintptr_t>(a.y) & 3) == 0)
+                         ? 1
+                         : 0;
+    launch_kernel(requant_kernel, dim3(grid_for(a.n, kBlock * 16, 8192)), dim3(kBlock), 0, stream,
+                  a.q, a.n, a.N2, a.N1, a.zp, a.bits, vec4, a.y);
+    return hipGetLastError();
+}
+
+}  // namespace fqvit

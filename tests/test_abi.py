@@ -33,7 +33,8 @@ def test_header_symbols_exported(lib):
     names = _declared_functions()
     assert set(names) >= {"ptf_layernorm_int8", "lis_softmax_log4", "lis_attn_v_shift",
                           "lis_attention_head", "fq_status_str", "fq_version",
-                          "fq_time_next_call"}
+                          "fq_time_next_call", "ptf_calibrate", "fq_ptf_calibrate_workspace_bytes",
+                          "ptf_quantize_int8", "requant_dyadic_int8"}
     for n in names:
         assert hasattr(lib, n), f"{n} declared in fqvit.h but not exported"
     # the binding exposes the compute entry points under the same names
@@ -171,3 +172,72 @@ def test_binding_requires_library(monkeypatch):
     monkeypatch.setattr(B, "LIB_PATH", "/nonexistent/libfqvit.so")
     with pytest.raises(RuntimeError, match="missing"):
         B.lib()
+
+
+def test_calibrate_workspace_size(lib):
+    f = B.ptf_calibrate_workspace_bytes
+    assert f(0, 768, 3) == 0 and f(10, 0, 3) == 0 and f(10, 768, 8) == 0
+    assert f(12608, 768, 3) == 1024 * 8 + 4 * 197 * 768 * 8
+    assert f(64, 5, 0) == 1024 * 8 + 1 * 1 * 5 * 8
+    assert f(65, 5, 7) == 1024 * 8 + 8 * 2 * 5 * 8
+
+
+def test_calibrate_validation(lib):
+    f = lib.ptf_calibrate
+    need = B.ptf_calibrate_workspace_bytes(100, 16, 3)
+    args = dict(x=1, T=100, C=16, bits=8, K=3, s=1, zp=1, alpha=1, ws=1, wsb=need)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return f(a["x"], a["T"], a["C"], a["bits"], a["K"], a["s"], a["zp"], a["alpha"], a["ws"],
+                 a["wsb"], NULL)
+
+    assert call(T=-1) == B.FQ_ERR_SHAPE
+    assert call(T=(1 << 24) - 255) == B.FQ_ERR_SHAPE
+    assert call(C=0) == B.FQ_ERR_SHAPE
+    assert call(C=8193) == B.FQ_ERR_SHAPE
+    assert call(bits=1) == B.FQ_ERR_PARAM
+    assert call(bits=9) == B.FQ_ERR_PARAM
+    assert call(K=8) == B.FQ_ERR_PARAM
+    assert call(wsb=need - 1) == B.FQ_ERR_PARAM
+    for k in ("x", "s", "zp", "alpha", "ws"):
+        assert call(**{k: None}) == B.FQ_ERR_NULL
+    assert call(T=0, x=None, s=None) == B.FQ_OK      # empty: nothing enqueued
+
+
+def test_quantize_validation(lib):
+    f = lib.ptf_quantize_int8
+    args = dict(x=1, T=10, C=16, s=1, zp=1, alpha=1, bits=8, y=1)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return f(a["x"], a["T"], a["C"], a["s"], a["zp"], a["alpha"], a["bits"], a["y"], NULL)
+
+    assert call(T=-1) == B.FQ_ERR_SHAPE
+    assert call(C=0) == B.FQ_ERR_SHAPE
+    assert call(bits=1) == B.FQ_ERR_PARAM
+    assert call(bits=9) == B.FQ_ERR_PARAM
+    for k in ("x", "s", "zp", "alpha", "y"):
+        assert call(**{k: None}) == B.FQ_ERR_NULL
+    assert call(T=0, x=None) == B.FQ_OK
+
+
+def test_requant_validation(lib):
+    f = lib.requant_dyadic_int8
+    args = dict(q=1, n=10, si=0.5, so=0.25, zp=0, bits=8, y=1)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return f(a["q"], a["n"], a["si"], a["so"], a["zp"], a["bits"], a["y"], NULL)
+
+    assert call(n=-1) == B.FQ_ERR_SHAPE
+    assert call(bits=1) == B.FQ_ERR_PARAM
+    assert call(bits=9) == B.FQ_ERR_PARAM
+    for k, v in (("si", 0.0), ("si", float("nan")), ("so", -1.0), ("so", float("inf"))):
+        assert call(**{k: v}) == B.FQ_ERR_PARAM
+    assert call(zp=128) == B.FQ_ERR_PARAM
+    assert call(bits=4, zp=8) == B.FQ_ERR_PARAM
+    assert call(bits=4, zp=-9) == B.FQ_ERR_PARAM
+    assert call(q=None) == B.FQ_ERR_NULL
+    assert call(y=None) == B.FQ_ERR_NULL
+    assert call(n=0, q=None, y=None) == B.FQ_OK
