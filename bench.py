@@ -132,6 +132,8 @@ def parse():
     p.add_argument("--warmup", type=int, default=50)
     p.add_argument("--config", default="vit_base16_224_b64")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-extras", action="store_true",
+                   help="skip the timing of the calibration / quantization / requantization ops")
     p.add_argument("--copy-calibration", action="store_true",
                    help="after the timed steps, run COPY_REPS device copies of COPY_BYTES "
                         "(the known-size kernel that scales the traffic counters)")
@@ -169,6 +171,54 @@ def cpu_baseline(cfg, inp, min_s=10.0, max_steps=12):
             "sample": f"{reps} complete steps of {cfg.name} (PTF-LayerNorm {cfg.T}x{cfg.channels}"
                       f" + LIS attention {cfg.G}x{cfg.Lq}x{cfg.Lk}, d={cfg.d}), single thread,"
                       f" {dt:.1f} s"}
+
+
+def extras(cfg, inp, out, fq, torch, reps=24, n_sets=8):
+    """Kernel times of the operations on either side of the hot path, on the
+    same workload: PTF calibration and quantization of the LayerNorm input
+    (float32 [T, C]) and the dyadic requantization of the head's int32 output.
+    Each is timed with the library's own kernel events (calibration: first to
+    last of its four kernels) over `n_sets` rotated inputs."""
+    import numpy as np
+    dev = torch.device("cuda:0")
+    x0 = torch.from_numpy(inp["ln"]["x_float"].astype(np.float32)).to(dev)
+    xs = [x0] + [torch.roll(x0, shifts=i, dims=0) for i in range(1, n_sets)]
+    T, C = x0.shape
+    ws = torch.empty(fq.ptf_calibrate_workspace_bytes(T, C, 3), dtype=torch.uint8, device=dev)
+    s = torch.empty(1, dtype=torch.float64, device=dev)
+    zp = torch.empty(1, dtype=torch.int32, device=dev)
+    alpha = torch.empty(C, dtype=torch.uint8, device=dev)
+    xq = torch.empty((T, C), dtype=torch.int8, device=dev)
+    outs = [out] + [out.clone() for _ in range(1, n_sets)]
+    y8 = torch.empty(out.shape, dtype=torch.int8, device=dev)
+    calls = {
+        "ptf_calibrate": [fq.ptf_calibrate(x, 8, 3, s, zp, alpha, ws, prepare=True) for x in xs],
+        "ptf_quantize_int8": [fq.ptf_quantize_int8(x, s, zp, alpha, 8, xq, prepare=True) for x in xs],
+        "requant_dyadic_int8": [fq.requant_dyadic_int8(o, 0.02 / 32768, 0.011, -3, 8, y8, prepare=True)
+                                for o in outs],
+    }
+    n_el = T * C
+    nbytes = {"ptf_calibrate": 2 * 4 * n_el + C,          # x read twice (min/max, then alpha)
+              "ptf_quantize_int8": 4 * n_el + n_el,       # float in, int8 out
+              "requant_dyadic_int8": 5 * out.numel()}     # int32 in, int8 out
+    time_next = fq.binding.lib().fq_time_next_call
+    res = {}
+    for name, cs in calls.items():
+        for c in cs:
+            c()
+        torch.cuda.synchronize()
+        ev = HipEvents(reps)
+        for i in range(reps):
+            time_next(*ev.pairs[i])
+            cs[i % n_sets]()
+        torch.cuda.synchronize()
+        us = sum(ev.elapsed_ms(i) for i in range(reps)) / reps * 1e3
+        ev.close()
+        gbs = nbytes[name] / (us * 1e-6) / 1e9
+        res[name] = {"us": us, "algorithmic_bytes": nbytes[name], "gbs": gbs,
+                     "hbm_frac": gbs / HBM_PEAK_GBS}
+    res["shapes"] = f"x float32 [{T}, {C}], K = 3, b = 8; requant of int32 {list(out.shape)}"
+    return res
 
 
 class HipEvents:
@@ -340,6 +390,8 @@ def main():
         },
         "wall_s_timed": wall,
     }
+    if not args.no_extras:
+        result["extras"] = extras(cfg, inp, sets[0]["out"], fq, torch)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(cfg, inp)
     print(json.dumps(result), flush=True)

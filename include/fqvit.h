@@ -158,7 +158,7 @@ fq_status lis_attention_head(const int32_t* logits, const int32_t* bias, int32_t
  * factor alpha_c by the argmin of eq. (11) over {0 .. K}, the squared error of
  * the quantizer of eq. (8) itself (its zero point and clip included).
  *
- *   x          [T, C] float activations (finite), T in [0, 2^24 - 256].
+ *   x          [T, C] float activations (finite), T in [0, 65535 * 64].
  *   bits       b in [2, 8]; K in [0, 7] (the paper uses 3).
  *   s          device double (out): s = (max - min) / (2^b - 1) / 2^K.
  *   zp         device int32 (out), container form: clip(rint(-min / (2^K s)),
@@ -173,7 +173,7 @@ fq_status lis_attention_head(const int32_t* logits, const int32_t* bias, int32_t
  * smallest alpha.  A tensor whose maximum equals its minimum gets s = 0, the
  * zero point 0 of the paper's grid and alpha = 0.  T = 0 enqueues nothing and
  * leaves the outputs untouched.
- * Errors: FQ_ERR_NULL, FQ_ERR_SHAPE (T outside [0, 2^24 - 256], C outside
+ * Errors: FQ_ERR_NULL, FQ_ERR_SHAPE (T outside [0, 65535 * 64], C outside
  * [1, 8192]), FQ_ERR_PARAM (bits, K, or a workspace that is too small).
  */
 size_t fq_ptf_calibrate_workspace_bytes(int64_t T, int32_t C, int32_t K);

@@ -14,9 +14,9 @@ namespace {
 constexpr int32_t kMaxC = 8192;
 constexpr int32_t kMaxLk = 4096;
 constexpr int32_t kMaxD = 256;
-// The alpha search's grid has one y index per 4 blocks of 64 rows: at most
+// The alpha search's grid has one y index per block of 64 rows: at most
 // 65535 of them.
-constexpr int64_t kMaxCalibT = ((int64_t)1 << 24) - 256;
+constexpr int64_t kMaxCalibT = (int64_t)65535 * 64;
 
 fq_status from_hip(hipError_t e) { return e == hipSuccess ? FQ_OK : FQ_ERR_HIP; }
 

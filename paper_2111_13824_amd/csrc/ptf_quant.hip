@@ -4,15 +4,15 @@
 //
 // Calibration runs four kernels:
 //   1. minmax_partial  per-workgroup minimum and maximum of x;
-//   2. params          the layer-wise scale s = (max - min) / (2^b - 1) / 2^K
+//   2. alpha_partial   the layer-wise scale s = (max - min) / (2^b - 1) / 2^K
 //                      and zero point zp = clip(rint(-min / (2^K s)), 0, 2^b - 1)
-//                      in binary64 (eq. 9, 10), each operation rounded once;
-//   3. alpha_partial   for every channel c and block of 64 consecutive rows, the
-//                      squared errors of the K + 1 candidate grids summed in row
-//                      order (eq. 11 with its zero point and clip);
-//   4. alpha_final     per channel, the block sums added in block order and the
-//                      argmin over alpha (the smallest alpha on ties).
-// Steps 3 and 4 reproduce the blocked summation order exactly, so the argmin
+//                      in binary64 (eq. 9, 10), each operation rounded once,
+//                      then for every channel c and block of 64 consecutive
+//                      rows the squared errors of the K + 1 candidate grids
+//                      summed in row order (eq. 11 with its zero point and clip);
+//   3. alpha_sum       per channel and alpha, the block sums added in block order;
+//   4. alpha_argmin    per channel, the argmin over alpha (the smallest on ties).
+// Steps 2 and 3 reproduce the blocked summation order exactly, so the argmin
 // is a pure function of x.  x / (2^alpha s) is computed as ldexp(x / s,
 // -alpha): scaling by a power of two commutes with the rounding of the
 // quotient, which never leaves the normal range for binary32 inputs.
@@ -79,11 +79,12 @@ __global__ __launch_bounds__(kBlock) void minmax_partial_kernel(const float* x, 
     }
 }
 
-// One workgroup: the overall minimum and maximum, then s and zp (container
-// form) as in eq. (9), (10).  A tensor with max == min (or a non-finite
-// range) gets s = 0 and the zero point 0 of the paper's grid.
-__global__ __launch_bounds__(kBlock) void params_kernel(const float* part, int nparts, int bits,
-                                                        int K, double* s_out, int32_t* zp_out) {
+// The overall minimum and maximum from the min/max partials (every thread of
+// the workgroup gets them), then s and zp (container form) as in eq. (9),
+// (10).  A tensor with max == min (or a non-finite range) gets s = 0 and the
+// zero point 0 of the paper's grid.
+__device__ void calib_params(const float* part, int nparts, int bits, int K, double& s_out,
+                             int32_t& zp_out) {
     float mn = INFINITY, mx = -INFINITY;
     for (int i = threadIdx.x; i < nparts; i += kBlock) {
         mn = fminf(mn, part[2 * i]);
@@ -97,7 +98,8 @@ __global__ __launch_bounds__(kBlock) void params_kernel(const float* part, int n
         s_mx[threadIdx.x >> 6] = mx;
     }
     __syncthreads();
-    if (threadIdx.x != 0) return;
+    mn = s_mn[0];
+    mx = s_mx[0];
     for (int w = 1; w < kBlock / 64; ++w) {
         mn = fminf(mn, s_mn[w]);
         mx = fmaxf(mx, s_mx[w]);
@@ -107,60 +109,121 @@ __global__ __launch_bounds__(kBlock) void params_kernel(const float* part, int n
     const double s = ((double)mx - (double)mn) / levels / two_K;
     const int half = 1 << (bits - 1);
     if (!(s > 0.0) || !isfinite(s)) {
-        *s_out = 0.0;
-        *zp_out = -half;
+        s_out = 0.0;
+        zp_out = -half;
         return;
     }
     const double z = fmin(fmax(rint(-(double)mn / (two_K * s)), 0.0), levels);
-    *s_out = s;
-    *zp_out = (int32_t)z - half;
+    s_out = s;
+    zp_out = (int32_t)z - half;
 }
 
-// Workgroup (cx, ky): 64 channels cx*64 .. cx*64 + 63 (one per lane), four
-// row blocks 4 ky .. 4 ky + 3 (one per wavefront).  part[(a nb + k) C + c] =
-// sum over the rows of block k, in order, of (x - deq_a(x))^2.
-template <int KMAX>
+// Workgroup (cx, k): channels cx*64 .. cx*64 + 63 (one per lane) and the
+// rows of block k; wavefront w computes the terms (x - deq_a(x))^2 of rows
+// 16 w .. 16 w + 15 of the block.  Each candidate's terms go through LDS and
+// one wavefront then adds that candidate's 64 terms in row order:
+// part[(a nb + k) C + c] = ((0 + term_0) + term_1) + ...  Every
+// workgroup derives s and zp from the min/max partials; workgroup (0, 0)
+// also stores them.
+constexpr int kRowsPerWave = kPtfErrBlock / (kBlock / 64);
+
+template <int K>
 __global__ __launch_bounds__(kBlock) void alpha_partial_kernel(const float* x, int64_t T, int C,
-                                                               int K, int bits,
-                                                               const double* s_ptr,
-                                                               const int32_t* zp_ptr,
-                                                               int64_t nb, double* part) {
-    const int c = blockIdx.x * 64 + (threadIdx.x & 63);
-    const int64_t k = (int64_t)blockIdx.y * 4 + (threadIdx.x >> 6);
-    if (c >= C || k >= nb) return;
-    const double s = *s_ptr;
-    if (!(s > 0.0)) return;
-    const double zp = (double)(*zp_ptr + (1 << (bits - 1)));
-    const double levels = (double)((1 << bits) - 1);
-    double acc[KMAX + 1];
-#pragma unroll
-    for (int a = 0; a <= KMAX; ++a) acc[a] = 0.0;
+                                                               int bits, const float* mm,
+                                                               int nparts, double* s_store,
+                                                               int32_t* zp_store, int64_t nb,
+                                                               double* part) {
+    __shared__ double term[kPtfErrBlock][64];      // 32 KB: one candidate at a time
+    double s;
+    int32_t zpc;
+    calib_params(mm, nparts, bits, K, s, zpc);
+    if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) {
+        *s_store = s;
+        *zp_store = zpc;
+    }
+    if (!(s > 0.0)) return;                        // uniform over the grid
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int c = blockIdx.x * 64 + lane;
+    const int64_t k = blockIdx.y;
     const int64_t t0 = k * kPtfErrBlock;
-    const int64_t t1 = min<int64_t>(t0 + kPtfErrBlock, T);
-    const float* xc = x + c;
-    for (int64_t t = t0; t < t1; ++t) {
-        const double xv = (double)xc[t * C];
-        const double q0 = xv / s;
+    const int nt = (int)min<int64_t>(kPtfErrBlock, T - t0);   // rows in this block
+    const int r0 = wave * kRowsPerWave;
+    const double zp = (double)(zpc + (1 << (bits - 1)));
+    const double levels = (double)((1 << bits) - 1);
+
+    double xv[kRowsPerWave], q0[kRowsPerWave];
 #pragma unroll
-        for (int a = 0; a <= KMAX; ++a) {
-            if (a > K) break;
-            const double step = ldexp(s, a);
-            const double q = fmin(fmax(rint(ldexp(q0, -a)) + zp, 0.0), levels);
-            const double deq = (q - zp) * step;
-            const double e = xv - deq;
-            acc[a] = acc[a] + e * e;
-        }
+    for (int i = 0; i < kRowsPerWave; ++i) {
+        const bool ok = c < C && r0 + i < nt;
+        xv[i] = ok ? (double)x[(t0 + r0 + i) * C + c] : 0.0;
     }
 #pragma unroll
-    for (int a = 0; a <= KMAX; ++a)
-        if (a <= K) part[((int64_t)a * nb + k) * C + c] = acc[a];
+    for (int i = 0; i < kRowsPerWave; ++i) q0[i] = xv[i] / s;
+
+#pragma unroll
+    for (int a = 0; a <= K; ++a) {
+        const double step = ldexp(s, a);
+#pragma unroll
+        for (int i = 0; i < kRowsPerWave; ++i) {
+            const double q = fmin(fmax(rint(ldexp(q0[i], -a)) + zp, 0.0), levels);
+            const double deq = (q - zp) * step;
+            const double e = xv[i] - deq;
+            term[r0 + i][lane] = e * e;
+        }
+        __syncthreads();
+        if (wave == (a & 3)) {      // the summing wavefront rotates with a
+            double acc = 0.0;
+            for (int r = 0; r < nt; ++r) acc = acc + term[r][lane];
+            if (c < C) part[((int64_t)a * nb + k) * C + c] = acc;
+        }
+        __syncthreads();
+    }
 }
 
-// One thread per channel: block sums added in block order, argmin over alpha
-// with ties to the smallest.
-__global__ __launch_bounds__(kBlock) void alpha_final_kernel(const double* part, int C, int K,
-                                                             int64_t nb, const double* s_ptr,
-                                                             uint8_t* alpha) {
+// Workgroup (cx, a): channels cx*64 .. cx*64 + 63, candidate alpha = a.  The
+// block sums are staged in LDS, up to kSumChunk blocks at a time (loaded by
+// the whole workgroup), and each channel's lane of wavefront 0 adds them in
+// block order: err[a C + c] = ((0 + part_0) + part_1) + ...
+constexpr int kSumChunk = 128;   // 64 KB of LDS per pass
+
+__global__ __launch_bounds__(kBlock) void alpha_sum_kernel(const double* part, int C, int64_t nb,
+                                                           const double* s_ptr, double* err) {
+    extern __shared__ double tile[];   // [kSumChunk][64]
+    const int c0 = blockIdx.x * 64;
+    const int a = blockIdx.y;
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    if (!(*s_ptr > 0.0)) return;
+    const double* p = part + (int64_t)a * nb * C + c0;
+    double acc = 0.0;
+    constexpr int kPerThread = kSumChunk / (kBlock / 64);
+    for (int64_t k0 = 0; k0 < nb; k0 += kSumChunk) {
+        const int nk = (int)min<int64_t>(kSumChunk, nb - k0);
+        // all of this thread's loads first, then the LDS stores
+        double v[kPerThread];
+#pragma unroll
+        for (int i = 0; i < kPerThread; ++i) {
+            const int r = wave + i * (kBlock / 64);
+            v[i] = (r < nk && c0 + lane < C) ? p[(k0 + r) * C + lane] : 0.0;
+        }
+#pragma unroll
+        for (int i = 0; i < kPerThread; ++i) {
+            const int r = wave + i * (kBlock / 64);
+            if (r < nk) tile[r * 64 + lane] = v[i];
+        }
+        __syncthreads();
+        if (wave == 0)
+            for (int r = 0; r < nk; ++r) acc = acc + tile[r * 64 + lane];
+        __syncthreads();
+    }
+    if (wave == 0 && c0 + lane < C) err[(int64_t)a * C + c0 + lane] = acc;
+}
+
+// One thread per channel: argmin over alpha with ties to the smallest.
+__global__ __launch_bounds__(kBlock) void alpha_argmin_kernel(const double* err, int C, int K,
+                                                              const double* s_ptr,
+                                                              uint8_t* alpha) {
     const int c = blockIdx.x * kBlock + threadIdx.x;
     if (c >= C) return;
     if (!(*s_ptr > 0.0)) {
@@ -170,11 +233,9 @@ __global__ __launch_bounds__(kBlock) void alpha_final_kernel(const double* part,
     int best = 0;
     double best_err = INFINITY;
     for (int a = 0; a <= K; ++a) {
-        double err = 0.0;
-        const double* p = part + (int64_t)a * nb * C + c;
-        for (int64_t k = 0; k < nb; ++k) err = err + p[k * C];
-        if (err < best_err) {
-            best_err = err;
+        const double e = err[(int64_t)a * C + c];
+        if (e < best_err) {
+            best_err = e;
             best = a;
         }
     }
@@ -271,7 +332,15 @@ unsigned grid_for(int64_t work, int64_t per_block, int64_t cap) {
 
 size_t ptf_calibrate_workspace_bytes(int64_t T, int32_t C, int32_t K) {
     const int64_t nb = (T + kPtfErrBlock - 1) / kPtfErrBlock;
-    return (size_t)kMinmaxParts * 2 * sizeof(float) + (size_t)(K + 1) * nb * C * sizeof(double);
+    return (size_t)kMinmaxParts * 2 * sizeof(float) + (size_t)(K + 1) * nb * C * sizeof(double) +
+           (size_t)(K + 1) * C * sizeof(double);
+}
+
+template <int K>
+void launch_alpha_partial(const PtfCalibArgs& a, dim3 grid, const float* mm, int nparts,
+                          int64_t nb, double* part, hipStream_t stream) {
+    launch_kernel(alpha_partial_kernel<K>, grid, dim3(kBlock), 0, stream, a.x, a.T, a.C, a.bits,
+                  mm, nparts, a.s, a.zp, nb, part);
 }
 
 hipError_t launch_ptf_calibrate(const PtfCalibArgs& a, hipStream_t stream) {
@@ -286,15 +355,25 @@ hipError_t launch_ptf_calibrate(const PtfCalibArgs& a, hipStream_t stream) {
     set_launch_events(ev.start, nullptr);
     launch_kernel(minmax_partial_kernel, dim3(nb1), dim3(kBlock), 0, stream, a.x, n, vec4, mm);
     set_launch_events(nullptr, nullptr);
-    launch_kernel(params_kernel, dim3(1), dim3(kBlock), 0, stream, (const float*)mm, (int)nb1,
-                  a.bits, a.K, a.s, a.zp);
     const int64_t nb = (a.T + kPtfErrBlock - 1) / kPtfErrBlock;
-    const dim3 g3((unsigned)((a.C + 63) / 64), (unsigned)((nb + 3) / 4));
-    launch_kernel(alpha_partial_kernel<7>, g3, dim3(kBlock), 0, stream, a.x, a.T, a.C, a.K, a.bits,
-                  (const double*)a.s, (const int32_t*)a.zp, nb, part);
+    const dim3 g3((unsigned)((a.C + 63) / 64), (unsigned)nb);
+    switch (a.K) {
+        case 0: launch_alpha_partial<0>(a, g3, mm, (int)nb1, nb, part, stream); break;
+        case 1: launch_alpha_partial<1>(a, g3, mm, (int)nb1, nb, part, stream); break;
+        case 2: launch_alpha_partial<2>(a, g3, mm, (int)nb1, nb, part, stream); break;
+        case 3: launch_alpha_partial<3>(a, g3, mm, (int)nb1, nb, part, stream); break;
+        case 4: launch_alpha_partial<4>(a, g3, mm, (int)nb1, nb, part, stream); break;
+        case 5: launch_alpha_partial<5>(a, g3, mm, (int)nb1, nb, part, stream); break;
+        case 6: launch_alpha_partial<6>(a, g3, mm, (int)nb1, nb, part, stream); break;
+        default: launch_alpha_partial<7>(a, g3, mm, (int)nb1, nb, part, stream); break;
+    }
+    double* err = part + (int64_t)(a.K + 1) * nb * a.C;
+    launch_kernel(alpha_sum_kernel, dim3((unsigned)((a.C + 63) / 64), (unsigned)(a.K + 1)),
+                  dim3(kBlock), (size_t)kSumChunk * 64 * sizeof(double), stream,
+                  (const double*)part, a.C, nb, (const double*)a.s, err);
     set_launch_events(nullptr, ev.stop);
-    launch_kernel(alpha_final_kernel, dim3((unsigned)((a.C + kBlock - 1) / kBlock)), dim3(kBlock), 0,
-                  stream, (const double*)part, a.C, a.K, nb, (const double*)a.s, a.alpha);
+    launch_kernel(alpha_argmin_kernel, dim3((unsigned)((a.C + kBlock - 1) / kBlock)), dim3(kBlock), 0,
+                  stream, (const double*)err, a.C, a.K, (const double*)a.s, a.alpha);
     set_launch_events(nullptr, nullptr);
     return hipGetLastError();
 }

@@ -177,9 +177,10 @@ def test_binding_requires_library(monkeypatch):
 def test_calibrate_workspace_size(lib):
     f = B.ptf_calibrate_workspace_bytes
     assert f(0, 768, 3) == 0 and f(10, 0, 3) == 0 and f(10, 768, 8) == 0
-    assert f(12608, 768, 3) == 1024 * 8 + 4 * 197 * 768 * 8
-    assert f(64, 5, 0) == 1024 * 8 + 1 * 1 * 5 * 8
-    assert f(65, 5, 7) == 1024 * 8 + 8 * 2 * 5 * 8
+    # min/max partials, per-block error sums, per-channel error totals
+    assert f(12608, 768, 3) == 1024 * 8 + 4 * 197 * 768 * 8 + 4 * 768 * 8
+    assert f(64, 5, 0) == 1024 * 8 + 1 * 1 * 5 * 8 + 1 * 5 * 8
+    assert f(65, 5, 7) == 1024 * 8 + 8 * 2 * 5 * 8 + 8 * 5 * 8
 
 
 def test_calibrate_validation(lib):
@@ -193,7 +194,7 @@ def test_calibrate_validation(lib):
                  a["wsb"], NULL)
 
     assert call(T=-1) == B.FQ_ERR_SHAPE
-    assert call(T=(1 << 24) - 255) == B.FQ_ERR_SHAPE
+    assert call(T=65535 * 64 + 1) == B.FQ_ERR_SHAPE
     assert call(C=0) == B.FQ_ERR_SHAPE
     assert call(C=8193) == B.FQ_ERR_SHAPE
     assert call(bits=1) == B.FQ_ERR_PARAM
