@@ -68,6 +68,9 @@ _SIGS = {
     "oracle_lis_attention_head": [_P, _P, _I32, _I64, _I32, _I32, _F32, _I32, _I32, _P, _I32,
                                   _I32, _P, _P, _I32],
     "oracle_requant_dyadic_int8": [_P, _I64, _F32, _F32, _I32, _I32, _P],
+    "oracle_qk_logits": [_P, _P, _I32, _I32, _I64, _I32, _I32, _I32, _P],
+    "oracle_lis_attention_qk": [_P, _P, _I32, _I32, _I32, _P, _I32, _I64, _I32, _I32, _F32, _I32,
+                                _I32, _P, _I32, _I32, _P],
 }
 
 # Rows per block of the alpha search's error sums (the oracle's reading of
@@ -265,3 +268,36 @@ def lis_attention_head(logits, v, s_logit, bits=4, exp_n=20, zp_v=0, bias=None,
                                            exp_n, _ptr(v), zp_v, d, _ptr(out), _ptr(codes), ld),
            "lis_attention_head")
     return (out, codes) if want_codes else out
+
+
+# ---- Sec. 3.3, Fig. 4: integer-only MSA from int8 Q and K --------------------
+
+def qk_logits(q, k, zp_q=0, zp_k=0) -> np.ndarray:
+    """int32 logits [G, Lq, Lk] = (q - zp_q)(k - zp_k)^T per unit, exact."""
+    q = np.ascontiguousarray(q, dtype=np.int8)
+    k = np.ascontiguousarray(k, dtype=np.int8)
+    G, Lq, dk = q.shape
+    Lk = k.shape[1]
+    out = np.empty((G, Lq, Lk), dtype=np.int32)
+    _check(lib().oracle_qk_logits(_ptr(q), _ptr(k), zp_q, zp_k, G, Lq, Lk, dk, _ptr(out)),
+           "qk_logits")
+    return out
+
+
+def lis_attention_qk(q, k, v, s_logit, zp_q=0, zp_k=0, bits=4, exp_n=20, zp_v=0, bias=None):
+    """int8 Q K^T, Log-Int-Softmax and BitShift Attn x V; returns int32 [G, Lq, d]."""
+    q = np.ascontiguousarray(q, dtype=np.int8)
+    k = np.ascontiguousarray(k, dtype=np.int8)
+    v = np.ascontiguousarray(v, dtype=np.int8)
+    G, Lq, dk = q.shape
+    Lk = k.shape[1]
+    d = v.shape[2]
+    Hb = 0
+    if bias is not None:
+        bias = np.ascontiguousarray(bias, dtype=np.int32)
+        Hb = bias.shape[0]
+    out = np.empty((G, Lq, d), dtype=np.int32)
+    _check(lib().oracle_lis_attention_qk(_ptr(q), _ptr(k), zp_q, zp_k, dk, _ptr(bias), Hb, G, Lq,
+                                         Lk, s_logit, bits, exp_n, _ptr(v), zp_v, d, _ptr(out)),
+           "lis_attention_qk")
+    return out

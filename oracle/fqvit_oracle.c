@@ -519,3 +519,49 @@ int oracle_lis_attention_head(const int32_t* logits, const int32_t* bias, int32_
     free(tmp);
     return rc;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Integer-only MSA (Sec. 3.3, its Fig. 4): int8 Q K^T, then LIS and BitShift */
+/* ------------------------------------------------------------------------ */
+
+/* The attention logits of the integer-only dataflow: the MinMax-quantized
+ * MatMul of Sec. 3.1 (its int GEMMs for MatMul) between the query and key
+ * activations, exact in integers:
+ *   logit[g,i,j] = sum_c (q[g,i,c] - zp_q) (k[g,j,c] - zp_k)
+ * with q, k and the zero points in the int8 container (the offset 2^(b-1)
+ * cancels in each difference).  Its scale, s_q s_k (with any 1/sqrt(dk) of
+ * the softmax folded in), is the s_logit of Log-Int-Softmax, which follows
+ * together with the BitShift product as in oracle_lis_attention_head. */
+int oracle_qk_logits(const int8_t* q, const int8_t* k, int32_t zp_q, int32_t zp_k, int64_t G,
+                     int32_t Lq, int32_t Lk, int32_t dk, int32_t* logits) {
+    if (G < 0 || Lq < 0 || Lk < 1 || dk < 1) return ORACLE_ERR_ARG;
+    if (zp_q < -128 || zp_q > 127 || zp_k < -128 || zp_k > 127) return ORACLE_ERR_ARG;
+    for (int64_t g = 0; g < G; ++g)
+        for (int32_t i = 0; i < Lq; ++i)
+            for (int32_t j = 0; j < Lk; ++j) {
+                int64_t acc = 0;
+                const int8_t* qi = q + (g * Lq + i) * (int64_t)dk;
+                const int8_t* kj = k + (g * Lk + j) * (int64_t)dk;
+                for (int32_t c = 0; c < dk; ++c)
+                    acc += ((int64_t)qi[c] - zp_q) * ((int64_t)kj[c] - zp_k);
+                if (acc > INT32_MAX || acc < INT32_MIN) return ORACLE_ERR_RANGE;
+                logits[(g * Lq + i) * (int64_t)Lk + j] = (int32_t)acc;
+            }
+    return ORACLE_OK;
+}
+
+int oracle_lis_attention_qk(const int8_t* q, const int8_t* k, int32_t zp_q, int32_t zp_k,
+                            int32_t dk, const int32_t* bias, int32_t Hb, int64_t G, int32_t Lq,
+                            int32_t Lk, float s_logit, int32_t bits, int32_t exp_n,
+                            const int8_t* v, int32_t zp_v, int32_t d, int32_t* out) {
+    if (G < 0 || Lq < 0 || Lk < 1 || dk < 1) return ORACLE_ERR_ARG;
+    if (G == 0 || Lq == 0) return ORACLE_OK;
+    int32_t* logits = (int32_t*)malloc(sizeof(int32_t) * (size_t)(G * Lq) * (size_t)Lk);
+    if (!logits) return ORACLE_ERR_ARG;
+    int rc = oracle_qk_logits(q, k, zp_q, zp_k, G, Lq, Lk, dk, logits);
+    if (rc == ORACLE_OK)
+        rc = oracle_lis_attention_head(logits, bias, Hb, G, Lq, Lk, s_logit, bits, exp_n, v, zp_v,
+                                       d, out, NULL, 0);
+    free(logits);
+    return rc;
+}

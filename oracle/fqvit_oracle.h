@@ -123,6 +123,18 @@ int oracle_lis_attention_head(const int32_t* logits, const int32_t* bias, int32_
                               int32_t exp_n, const int8_t* v, int32_t zp_v, int32_t d,
                               int32_t* out, uint8_t* codes_out, int32_t ld_codes);
 
+/* ---- Sec. 3.3, Fig. 4: integer-only MSA from int8 Q and K ------------- */
+
+/* logits[g,i,j] = sum_c (q[g,i,c] - zp_q)(k[g,j,c] - zp_k); q: [G, Lq, dk],
+ * k: [G, Lk, dk] int8 containers, zero points in container form. */
+int oracle_qk_logits(const int8_t* q, const int8_t* k, int32_t zp_q, int32_t zp_k, int64_t G,
+                     int32_t Lq, int32_t Lk, int32_t dk, int32_t* logits);
+/* oracle_qk_logits, then oracle_lis_attention_head on those logits. */
+int oracle_lis_attention_qk(const int8_t* q, const int8_t* k, int32_t zp_q, int32_t zp_k,
+                            int32_t dk, const int32_t* bias, int32_t Hb, int64_t G, int32_t Lq,
+                            int32_t Lk, float s_logit, int32_t bits, int32_t exp_n,
+                            const int8_t* v, int32_t zp_v, int32_t d, int32_t* out);
+
 #ifdef __cplusplus
 }
 #endif

@@ -58,6 +58,9 @@ MUTANTS = [
     ("requant_round_down", "(prod + ((__int128)1 << (N1 - 1))) >> N1", "prod >> N1"),
     ("requant_zp_dropped", "const __int128 yu = w + zp;", "const __int128 yu = w + half;"),
     ("requant_inverse_scale", "(double)s_in / (double)s_out", "(double)s_out / (double)s_in"),
+    ("qk_zero_point_sign", "((int64_t)qi[c] - zp_q)", "((int64_t)qi[c] + zp_q)"),
+    ("qk_zp_k_dropped", "((int64_t)kj[c] - zp_k)", "((int64_t)kj[c])"),
+    ("qk_k_transposed", "k + (g * Lk + j) * (int64_t)dk", "k + (g * Lk + j)"),
 ]
 
 

@@ -413,6 +413,45 @@ def test_ptf_alpha_matches_exact_argmin(orc):
 
 
 # ---------------------------------------------------------------------------
+# Integer Q K^T (Sec. 3.1 int MatMul feeding Sec. 3.3)
+# ---------------------------------------------------------------------------
+
+def test_qk_logits_is_integer_matmul(orc):
+    """A textbook special case: the logits are the batched int64 matrix product
+    of the zero-point-centred operands (numpy), for every zero point pair."""
+    rng = np.random.default_rng(51)
+    q = rng.integers(-128, 128, size=(3, 17, 64)).astype(np.int8)
+    k = rng.integers(-128, 128, size=(3, 29, 64)).astype(np.int8)
+    for zq, zk in ((0, 0), (5, -7), (-128, 127)):
+        ref = np.matmul(q.astype(np.int64) - zq, np.swapaxes(k.astype(np.int64) - zk, 1, 2))
+        assert np.array_equal(orc.qk_logits(q, k, zq, zk).astype(np.int64), ref)
+
+
+def test_qk_logits_zero_point_shift_invariance(orc):
+    """Moving the container grid (values and zero point by the same amount)
+    leaves the logits unchanged; q = zp_q gives zero logits."""
+    rng = np.random.default_rng(52)
+    q = rng.integers(-100, 100, size=(2, 9, 32)).astype(np.int8)
+    k = rng.integers(-100, 100, size=(2, 11, 32)).astype(np.int8)
+    base = orc.qk_logits(q, k, 3, -4)
+    assert np.array_equal(orc.qk_logits((q + 20).astype(np.int8), k, 23, -4), base)
+    assert np.array_equal(orc.qk_logits(q, (k - 20).astype(np.int8), 3, -24), base)
+    assert not orc.qk_logits(np.full_like(q, 7), k, 7, -4).any()
+
+
+def test_qk_head_is_logits_then_head(orc):
+    """The integer-only MSA from Q, K equals the logits followed by the fused
+    Log-Int-Softmax / BitShift head."""
+    rng = np.random.default_rng(53)
+    q = rng.integers(-128, 128, size=(2, 13, 64)).astype(np.int8)
+    k = rng.integers(-128, 128, size=(2, 21, 64)).astype(np.int8)
+    v = rng.integers(-127, 128, size=(2, 21, 16)).astype(np.int8)
+    s = 1.0 / 1800.0
+    out = orc.lis_attention_qk(q, k, v, s, zp_q=2, zp_k=-3)
+    assert np.array_equal(out, orc.lis_attention_head(orc.qk_logits(q, k, 2, -3), v, s))
+
+
+# ---------------------------------------------------------------------------
 # Dyadic requantization
 # ---------------------------------------------------------------------------
 
