@@ -153,6 +153,30 @@ fq_status lis_attention_head(const int32_t* logits, const int32_t* bias, int32_t
                              int32_t* out, uint8_t* codes_out, int32_t ld_codes, void* stream);
 
 /*
+ * Integer-only multi-head self-attention from int8 queries and keys: the
+ * MinMax-quantized MatMul of Sec. 3.1 between Q and K (an integer GEMM),
+ * Log-Int-Softmax and the BitShift Attn x V of Sec. 3.3 (the dataflow of its
+ * Fig. 4), with the logits and codes kept on chip:
+ *   logit[g,i,j] = sum_c (q[g,i,c] - zp_q)(k[g,j,c] - zp_k) (+ bias),
+ * then exactly lis_attention_head on those logits.
+ *
+ *   q       [G, Lq, dk] int8 container, 16-byte aligned; zp_q in [-128, 127].
+ *   k       [G, Lk, dk] int8 container, 16-byte aligned; zp_k in [-128, 127].
+ *   dk      32 or 64.
+ *   bias, Hb, s_logit, bits, exp_n, v, zp_v, out: as in lis_attention_head;
+ *           s_logit is the scale of the logits (s_q s_k, with any 1/sqrt(dk)
+ *           of the softmax folded in).
+ * Supported: Lk in [1, 224], d in [1, 64].
+ * Errors: FQ_ERR_NULL, FQ_ERR_SHAPE (sizes, dk, or bias with Hb < 1),
+ * FQ_ERR_PARAM (zero points, bits, exp_n, s_logit, or misaligned q / k),
+ * FQ_ERR_HEADROOM.
+ */
+fq_status lis_attention_qk(const int8_t* q, const int8_t* k, int32_t zp_q, int32_t zp_k,
+                           int32_t dk, const int32_t* bias, int32_t Hb, int64_t G, int32_t Lq,
+                           int32_t Lk, float s_logit, int32_t bits, int32_t exp_n,
+                           const int8_t* v, int32_t zp_v, int32_t d, int32_t* out, void* stream);
+
+/*
  * PTF calibration (Sec. 3.2): the layer-wise scale and zero point of eq. (9),
  * (10) from the minimum and maximum of x, then each channel's power-of-two
  * factor alpha_c by the argmin of eq. (11) over {0 .. K}, the squared error of

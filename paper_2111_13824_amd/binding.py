@@ -26,6 +26,8 @@ SIGNATURES = {
     "lis_attn_v_shift": [_P, _I32, _P, _I32, _I64, _I32, _I32, _I32, _I32, _P, _P],
     "lis_attention_head": [_P, _P, _I32, _I64, _I32, _I32, _F32, _I32, _I32, _P, _I32, _I32, _P,
                            _P, _I32, _P],
+    "lis_attention_qk": [_P, _P, _I32, _I32, _I32, _P, _I32, _I64, _I32, _I32, _F32, _I32, _I32,
+                         _P, _I32, _I32, _P, _P],
     "ptf_calibrate": [_P, _I64, _I32, _I32, _I32, _P, _P, _P, _P, ctypes.c_size_t, _P],
     "ptf_quantize_int8": [_P, _I64, _I32, _P, _P, _P, _I32, _P, _P],
     "requant_dyadic_int8": [_P, _I64, _F32, _F32, _I32, _I32, _P, _P],
@@ -283,3 +285,24 @@ def requant_dyadic_int8(q, s_in: float, s_out: float, zp_out: int, bits: int = 8
     args = (_dev_ptr(q, torch.int32, "q"), q.numel(), s_in, s_out, zp_out, bits,
             _dev_ptr(y, torch.int8, "y"), _stream(stream, q))
     return _invoke("requant_dyadic_int8", args, (q, y), prepare, y)
+
+
+def lis_attention_qk(q, k, v, s_logit: float, zp_q: int = 0, zp_k: int = 0, bits: int = 4,
+                     exp_n: int = 20, zp_v: int = 0, bias=None, out=None, stream=None,
+                     prepare: bool = False):
+    """Integer-only attention from int8 q [G, Lq, dk], k [G, Lk, dk] and
+    v [G, Lk, d]; returns (or fills) int32 [G, Lq, d]."""
+    import torch
+    G, Lq, dk = q.shape
+    Lk = k.shape[1]
+    d = v.shape[2]
+    if k.shape != (G, Lk, dk) or v.shape[:2] != (G, Lk):
+        raise ValueError("k must be [G, Lk, dk] and v [G, Lk, d]")
+    if out is None:
+        out = torch.empty((G, Lq, d), dtype=torch.int32, device=q.device)
+    Hb = bias.shape[0] if bias is not None else 0
+    args = (_dev_ptr(q, torch.int8, "q", 3), _dev_ptr(k, torch.int8, "k", 3), zp_q, zp_k, dk,
+            _dev_ptr(bias, torch.int32, "bias", 3), Hb, G, Lq, Lk, s_logit, bits, exp_n,
+            _dev_ptr(v, torch.int8, "v", 3), zp_v, d, _dev_ptr(out, torch.int32, "out", 3),
+            _stream(stream, q))
+    return _invoke("lis_attention_qk", args, (q, k, v, bias, out), prepare, out)

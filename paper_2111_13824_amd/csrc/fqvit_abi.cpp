@@ -194,6 +194,38 @@ fq_status lis_attention_head(const int32_t* logits, const int32_t* bias, int32_t
     return from_hip(fqvit::launch_lis(a, (hipStream_t)stream));
 }
 
+fq_status lis_attention_qk(const int8_t* q, const int8_t* k, int32_t zp_q, int32_t zp_k,
+                           int32_t dk, const int32_t* bias, int32_t Hb, int64_t G, int32_t Lq,
+                           int32_t Lk, float s_logit, int32_t bits, int32_t exp_n,
+                           const int8_t* v, int32_t zp_v, int32_t d, int32_t* out, void* stream) {
+    ConsumeEvents consume;
+    if (G < 0 || G > 0x7FFFFFFF || Lq < 0 || Lk < 1 || Lk > fqvit::kQkMaxLk || d < 1 || d > 64 ||
+        (dk != 32 && dk != 64) || (bias && Hb < 1))
+        return FQ_ERR_SHAPE;
+    if (zp_q < -128 || zp_q > 127 || zp_k < -128 || zp_k > 127 || zp_v < -128 || zp_v > 127)
+        return FQ_ERR_PARAM;
+    fqvit::LisConsts kc;
+    const fq_status st = lis_constants(s_logit, bits, exp_n, Lk, &kc);
+    if (st != FQ_OK) return st;
+    if (G == 0 || Lq == 0) return FQ_OK;
+    if (!q || !k || !v || !out) return FQ_ERR_NULL;
+    if (((reinterpret_cast<uintptr_t>(q) | reinterpret_cast<uintptr_t>(k)) & 15) != 0)
+        return FQ_ERR_PARAM;
+    fqvit::LisArgs a{};
+    a.bias = bias;
+    a.Hb = bias ? Hb : 1;
+    a.G = G;
+    a.Lq = Lq;
+    a.Lk = Lk;
+    a.k = kc;
+    a.v = v;
+    a.zp_v = zp_v;
+    a.d = d;
+    a.out = out;
+    const fqvit::QkInput in{q, k, zp_q, zp_k, dk};
+    return from_hip(fqvit::launch_lis_qk(a, in, (hipStream_t)stream));
+}
+
 size_t fq_ptf_calibrate_workspace_bytes(int64_t T, int32_t C, int32_t K) {
     if (T < 1 || T > kMaxCalibT || C < 1 || C > kMaxC || K < 0 || K > 7) return 0;
     return fqvit::ptf_calibrate_workspace_bytes(T, C, K);

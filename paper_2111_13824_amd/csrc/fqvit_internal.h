@@ -96,6 +96,19 @@ struct LisArgs {
 
 hipError_t launch_lis(const LisArgs& a, hipStream_t stream);
 
+// Integer-only attention from int8 Q and K (logits computed on chip; the
+// logits / codes fields of LisArgs are unused).
+struct QkInput {
+    const int8_t* q;        // [G, Lq, dk]
+    const int8_t* k;        // [G, Lk, dk]
+    int32_t zp_q, zp_k;     // container form
+    int32_t dk;             // 32 or 64
+};
+
+constexpr int kQkMaxLk = 224;   // keys per unit (7 chunks of 32)
+
+hipError_t launch_lis_qk(const LisArgs& a, const QkInput& in, hipStream_t stream);
+
 struct AvArgs {
     const uint8_t* codes;
     int32_t ld_codes;

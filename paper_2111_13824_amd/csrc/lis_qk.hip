@@ -1,0 +1,31 @@
+// Host side of the integer-only attention from int8 Q and K (kernel in
+// lis_qk_kernel.h): launch geometry and LDS of one workgroup per unit.
+#include "lis_qk_kernel.h"
+
+namespace fqvit {
+
+hipError_t launch_lis_qk(const LisArgs& a, const QkInput& in, hipStream_t stream) {
+    using namespace lis;
+    const int nc = (a.Lk + 31) / 32;
+    int dt = 2;
+    while (16 * dt < a.d) dt <<= 1;
+    LisLaunch p{};
+    p.ntiles = (a.Lq + 15) / 16;
+    p.dpad = 16 * dt;
+    p.ncg = dt;
+    p.kb = 32 * nc;
+    p.ld = p.kb + 8;
+    p.vec_ok = (a.d % 16 == 0) && ((reinterpret_cast<uintptr_t>(a.v) & 15) == 0);
+    p.vt_bytes = p.dpad * p.ld * (int)sizeof(uint16_t);
+    p.out_vec = 0;
+    p.n_logits = 0;
+    p.n_bias = a.bias ? (int64_t)a.Hb * a.Lq * a.Lk : 0;
+    const size_t lds = (size_t)p.vt_bytes + (size_t)32 * nc * in.dk + (size_t)32 * nc * sizeof(int32_t);
+    const bool half = a.Lk - 32 * (nc - 1) <= 16;
+    const bool fp = a.k.fp_ok != 0;
+    const QkArgs qa{in.q, in.k, in.zp_q, in.zp_k};
+    if (in.dk == 32) return launch_qk_dk32(nc, dt, half, fp, a, qa, p, lds, stream);
+    return launch_qk_dk64(nc, dt, half, fp, a, qa, p, lds, stream);
+}
+
+}  // namespace fqvit

@@ -34,7 +34,7 @@ def test_header_symbols_exported(lib):
     assert set(names) >= {"ptf_layernorm_int8", "lis_softmax_log4", "lis_attn_v_shift",
                           "lis_attention_head", "fq_status_str", "fq_version",
                           "fq_time_next_call", "ptf_calibrate", "fq_ptf_calibrate_workspace_bytes",
-                          "ptf_quantize_int8", "requant_dyadic_int8"}
+                          "ptf_quantize_int8", "requant_dyadic_int8", "lis_attention_qk"}
     for n in names:
         assert hasattr(lib, n), f"{n} declared in fqvit.h but not exported"
     # the binding exposes the compute entry points under the same names
@@ -242,3 +242,35 @@ def test_requant_validation(lib):
     assert call(q=None) == B.FQ_ERR_NULL
     assert call(y=None) == B.FQ_ERR_NULL
     assert call(n=0, q=None, y=None) == B.FQ_OK
+
+
+def test_qk_validation(lib):
+    f = lib.lis_attention_qk
+    args = dict(q=16, k=16, zq=0, zk=0, dk=64, bias=None, Hb=0, G=2, Lq=5, Lk=7, s=0.001, bits=4,
+                n=20, v=1, zv=0, d=64, out=1)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return f(a["q"], a["k"], a["zq"], a["zk"], a["dk"], a["bias"], a["Hb"], a["G"], a["Lq"],
+                 a["Lk"], a["s"], a["bits"], a["n"], a["v"], a["zv"], a["d"], a["out"], NULL)
+
+    assert call(G=-1) == B.FQ_ERR_SHAPE
+    assert call(Lk=0) == B.FQ_ERR_SHAPE
+    assert call(Lk=225) == B.FQ_ERR_SHAPE
+    assert call(d=65) == B.FQ_ERR_SHAPE
+    assert call(d=0) == B.FQ_ERR_SHAPE
+    assert call(dk=48) == B.FQ_ERR_SHAPE
+    assert call(dk=128) == B.FQ_ERR_SHAPE
+    assert call(bias=16, Hb=0) == B.FQ_ERR_SHAPE
+    assert call(zq=128) == B.FQ_ERR_PARAM
+    assert call(zk=-129) == B.FQ_ERR_PARAM
+    assert call(zv=200) == B.FQ_ERR_PARAM
+    assert call(bits=5) == B.FQ_ERR_PARAM
+    assert call(s=1.0) == B.FQ_ERR_PARAM
+    assert call(n=0) == B.FQ_ERR_PARAM
+    assert call(q=8) == B.FQ_ERR_PARAM           # q not 16-byte aligned
+    assert call(k=24) == B.FQ_ERR_PARAM
+    for key in ("q", "k", "v", "out"):
+        assert call(**{key: None}) == B.FQ_ERR_NULL
+    assert call(G=0, q=None) == B.FQ_OK
+    assert call(Lq=0, out=None) == B.FQ_OK

@@ -176,6 +176,19 @@ def attn_inputs(G: int, Lq: int, Lk: int, d: int, seed: int, heads: int = 1,
                 s_logit=s_logit, bits=LIS_BITS, exp_n=EXP_N)
 
 
+def qk_inputs(G: int, Lq: int, Lk: int, dk: int, d: int, seed: int, sigma: float = 30.0,
+              zp_q: int = 0, zp_k: int = 0, heads: int = 1, bias: bool = False) -> dict:
+    """int8 query and key activations [G, Lq|Lk, dk] (rounded Gaussians of
+    standard deviation `sigma` around their zero points, clipped to int8),
+    int8 V [G, Lk, d] and an optional bias [heads, Lq, Lk]."""
+    _, r_lg, r_v, r_par = _streams(seed)
+    q = np.clip(np.rint(r_lg.standard_normal((G, Lq, dk)) * sigma) + zp_q, -128, 127).astype(np.int8)
+    k = np.clip(np.rint(r_lg.standard_normal((G, Lk, dk)) * sigma) + zp_k, -128, 127).astype(np.int8)
+    v = r_v.integers(-127, 128, size=(G, Lk, d)).astype(np.int8)
+    b = r_par.integers(-64, 65, size=(heads, Lq, Lk)).astype(np.int32) if bias else None
+    return dict(q=q, k=k, v=v, zp_q=zp_q, zp_k=zp_k, bias=b)
+
+
 def config_inputs(cfg: Config, part: str = "all", G: Optional[int] = None,
                   T: Optional[int] = None) -> dict:
     """Inputs of a named config.  ``G`` truncates the attention unit count (the
