@@ -85,7 +85,7 @@ def pmc_summary(fetch_dir, write_dir):
         rows.sort(key=lambda r: int(r["Dispatch_Id"]))
         groups = {"head": [], "ln": [], "copy": []}
         def is_head(name):
-            return "fqvit::lis::" in name
+            return "fqvit::lis::" in name and "lis_qk_kernel" not in name
 
         def is_ln(name):
             return "fqvit::" in name and "ln_" in name
@@ -98,7 +98,8 @@ def pmc_summary(fetch_dir, write_dir):
                 groups["head"].append(v)
             elif is_ln(name):
                 groups["ln"].append(v)
-            elif "copy" in name.lower() and int(r["Dispatch_Id"]) > last_head:
+            elif ("copy" in name.lower() and int(r["Dispatch_Id"]) > last_head
+                  and len(groups["copy"]) < COPY_REPS):
                 groups["copy"].append(v)
         return {k: (sum(v) / len(v) if v else float("nan"), len(v)) for k, v in groups.items()}
 
@@ -191,14 +192,27 @@ def extras(cfg, inp, out, fq, torch, reps=24, n_sets=8):
     xq = torch.empty((T, C), dtype=torch.int8, device=dev)
     outs = [out] + [out.clone() for _ in range(1, n_sets)]
     y8 = torch.empty(out.shape, dtype=torch.int8, device=dev)
+    # integer-only attention from int8 Q, K of the same attention shape: Q and
+    # K rounded Gaussians (sigma 19.6, so the logits at s = 2^-10 have the
+    # spread of the head workload's), V as for the head
+    import workloads as W
+    G, Lq, Lk, dk, d = cfg.G, cfg.Lq, cfg.Lk, cfg.d, cfg.d
+    qks = []
+    for i in range(n_sets):
+        qk_in = W.qk_inputs(G, Lq, Lk, dk, d, seed=100 + i, sigma=19.6)
+        qks.append({key: torch.from_numpy(qk_in[key]).to(dev) for key in ("q", "k", "v")})
+    out_qk = torch.empty((G, Lq, d), dtype=torch.int32, device=dev)
     calls = {
+        "lis_attention_qk": [fq.lis_attention_qk(t["q"], t["k"], t["v"], 2.0 ** -10, out=out_qk,
+                                                 prepare=True) for t in qks],
         "ptf_calibrate": [fq.ptf_calibrate(x, 8, 3, s, zp, alpha, ws, prepare=True) for x in xs],
         "ptf_quantize_int8": [fq.ptf_quantize_int8(x, s, zp, alpha, 8, xq, prepare=True) for x in xs],
         "requant_dyadic_int8": [fq.requant_dyadic_int8(o, 0.02 / 32768, 0.011, -3, 8, y8, prepare=True)
                                 for o in outs],
     }
     n_el = T * C
-    nbytes = {"ptf_calibrate": 2 * 4 * n_el + C,          # x read twice (min/max, then alpha)
+    nbytes = {"lis_attention_qk": G * (Lq * dk + Lk * dk + Lk * d + 4 * Lq * d),
+              "ptf_calibrate": 2 * 4 * n_el + C,          # x read twice (min/max, then alpha)
               "ptf_quantize_int8": 4 * n_el + n_el,       # float in, int8 out
               "requant_dyadic_int8": 5 * out.numel()}     # int32 in, int8 out
     time_next = fq.binding.lib().fq_time_next_call
@@ -217,7 +231,9 @@ def extras(cfg, inp, out, fq, torch, reps=24, n_sets=8):
         gbs = nbytes[name] / (us * 1e-6) / 1e9
         res[name] = {"us": us, "algorithmic_bytes": nbytes[name], "gbs": gbs,
                      "hbm_frac": gbs / HBM_PEAK_GBS}
-    res["shapes"] = f"x float32 [{T}, {C}], K = 3, b = 8; requant of int32 {list(out.shape)}"
+    res["shapes"] = (f"x float32 [{T}, {C}], K = 3, b = 8; requant of int32 {list(out.shape)};"
+                     f" qk: q [{G}, {Lq}, {dk}], k [{G}, {Lk}, {dk}], v [{G}, {Lk}, {d}] int8,"
+                     f" s_logit 2^-10")
     return res
 
 

@@ -17,7 +17,8 @@
 // With zero points (int8 containers; the 2^(b-1) offset cancels):
 //   sum_c (q - zq)(k - zk) = S - zk sum_c q - zq sum_c k + dk zq zk,
 // S = sum_c q k from the MFMA; the per-key term zq sum_c k is computed once per
-// unit, the per-query term zk sum_c q - dk zq zk once per tile.  All sums are
+// unit (stored negated), the per-query term zk sum_c q - dk zq zk once per
+// tile, and each logit is one three-operand add.  All sums are
 // exact in int32 (|logit| <= dk 255^2 < 2^24 for dk <= 256).
 #pragma once
 
@@ -88,7 +89,7 @@ __global__ __launch_bounds__(kBlock, 3) void lis_qk_kernel(LisArgs a, QkArgs qa,
             s = __builtin_amdgcn_sdot4(v.z, 0x01010101, s, false);
             s = __builtin_amdgcn_sdot4(v.w, 0x01010101, s, false);
         }
-        ck[j] = qa.zq * s;
+        ck[j] = -(qa.zq * s);        // stored negated: one three-operand add per logit
     }
     __syncthreads();
 
@@ -120,8 +121,7 @@ __global__ __launch_bounds__(kBlock, 3) void lis_qk_kernel(LisArgs a, QkArgs qa,
         }
         sq += __shfl_xor(sq, 16, 64);
         sq += __shfl_xor(sq, 32, 64);
-        const int cq = qa.zk * sq - dkzz;
-        const int32_t* brow = bplane ? bplane + (int64_t)i * a.Lk : nullptr;
+        const int ncq = dkzz - qa.zk * sq;   // minus the per-query term
 
         // logits of this tile in the Log-Int-Softmax lane layout
         int lg[NC][8];
@@ -152,14 +152,23 @@ __global__ __launch_bounds__(kBlock, 3) void lis_qk_kernel(LisArgs a, QkArgs qa,
                 const i32x4v cv = *reinterpret_cast<const i32x4v*>(ck + j0);
 #pragma unroll
                 for (int t = 0; t < 4; ++t) {
-                    const int j = j0 + t;
-                    int v = s[t] - cq - cv[t];
-                    if (brow && j < a.Lk) v += brow[j];
-                    lg[c][4 * h + t] = j < a.Lk ? v : INT_MIN;
+                    const int v = s[t] + ncq + cv[t];
+                    // only the last chunk can hold keys past Lk
+                    lg[c][4 * h + t] = (c < NC - 1 || j0 + t < a.Lk) ? v : INT_MIN;
                 }
             }
         }
-
+        if (bplane) {   // uniform: the bias of the lane's row, in a pass of its own
+            const int32_t* brow = bplane + (int64_t)i * a.Lk;
+#pragma unroll
+            for (int c = 0; c < NC; ++c) {
+#pragma unroll
+                for (int t = 0; t < 8; ++t) {
+                    const int j = 32 * c + 4 * kg + (t < 4 ? t : 12 + t);
+                    if (c < NC - 1 || j < a.Lk) lg[c][t] += brow[j];
+                }
+            }
+        }
         uint32_t zb[NC][2];
         const RowState st = tile_iexp<NC, FP, NT>(lg, zb, k);
         f32x4 acc[DTMAX];
