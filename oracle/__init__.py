@@ -201,12 +201,15 @@ def ilog2(q: int) -> int:
     return lib().oracle_ilog2(int(q))
 
 
-def codes_ld(Lk: int) -> int:
-    return (Lk + 1) // 2
+def codes_ld(Lk: int, bits: int = 4) -> int:
+    return (Lk + 1) // 2 if bits <= 4 else Lk
 
 
-def unpack_codes(packed: np.ndarray, Lk: int) -> np.ndarray:
-    """[..., ld] packed nibbles -> [..., Lk] codes (even key in the low nibble)."""
+def unpack_codes(packed: np.ndarray, Lk: int, bits: int = 4) -> np.ndarray:
+    """[..., ld] stored codes -> [..., Lk] codes: nibbles (even key in the low
+    nibble) for bits <= 4, one byte per code above."""
+    if bits > 4:
+        return packed[..., :Lk]
     lo = packed & 15
     hi = packed >> 4
     out = np.stack([lo, hi], axis=-1).reshape(*packed.shape[:-1], packed.shape[-1] * 2)
@@ -216,7 +219,7 @@ def unpack_codes(packed: np.ndarray, Lk: int) -> np.ndarray:
 def lis_softmax_log4(logits, s_logit, bits=4, exp_n=20, bias=None, ld_codes=None) -> np.ndarray:
     logits = np.ascontiguousarray(logits, dtype=np.int32)
     G, Lq, Lk = logits.shape
-    ld = codes_ld(Lk) if ld_codes is None else ld_codes
+    ld = codes_ld(Lk, bits) if ld_codes is None else ld_codes
     Hb = 0
     if bias is not None:
         bias = np.ascontiguousarray(bias, dtype=np.int32)

@@ -366,10 +366,15 @@ int32_t oracle_ilog2(uint64_t q) {
 
 static int lis_check(int64_t G, int32_t Lq, int32_t Lk, int32_t bits, int32_t exp_n,
                      float s_logit) {
-    if (G < 0 || Lq < 0 || Lk < 1 || bits < 1 || bits > 4 || exp_n < 1 || exp_n > 30 ||
+    if (G < 0 || Lq < 0 || Lk < 1 || bits < 1 || bits > 8 || exp_n < 1 || exp_n > 30 ||
         !(s_logit > 0.0f))
         return ORACLE_ERR_ARG;
     return ORACLE_OK;
+}
+
+/* Bytes per row of stored codes: two per byte up to 4 bits, else one per byte. */
+static int32_t codes_row_bytes(int32_t Lk, int32_t bits) {
+    return bits <= 4 ? (Lk + 1) / 2 : Lk;
 }
 
 /* One row of Log-Int-Softmax: Attn_Q for every key.  v holds logits + bias. */
@@ -406,7 +411,7 @@ int oracle_lis_softmax_log4(const int32_t* logits, int64_t G, int32_t Lq, int32_
                             const int32_t* bias, int32_t Hb, float s_logit, int32_t bits,
                             int32_t exp_n, uint8_t* codes, int32_t ld_codes) {
     if (lis_check(G, Lq, Lk, bits, exp_n, s_logit) != ORACLE_OK) return ORACLE_ERR_ARG;
-    if (ld_codes < (Lk + 1) / 2) return ORACLE_ERR_ARG;
+    if (ld_codes < codes_row_bytes(Lk, bits)) return ORACLE_ERR_ARG;
     if (bias && Hb < 1) return ORACLE_ERR_ARG;
     if (G == 0 || Lq == 0) return ORACLE_OK;
     if (!logits || !codes) return ORACLE_ERR_ARG;
@@ -429,12 +434,17 @@ int oracle_lis_softmax_log4(const int32_t* logits, int64_t G, int32_t Lq, int32_
             const int32_t* bq = bias ? bias + ((g % Hb) * Lq + i) * (int64_t)Lk : NULL;
             for (int32_t j = 0; j < Lk; ++j) v[j] = (int64_t)q[j] + (bq ? bq[j] : 0);
             lis_row(v, Lk, &k, bits, e, code);
-            /* READING (storage): 4-bit codes, two per byte, even key in the low nibble. */
+            /* READING (storage): codes of up to 4 bits two per byte, even key in
+             * the low nibble; wider codes (Sec. 3.3 allows any b) one per byte. */
             uint8_t* out = codes + (g * Lq + i) * (int64_t)ld_codes;
-            for (int32_t j = 0; j < Lk; j += 2) {
-                const int32_t lo = code[j];
-                const int32_t hi = (j + 1 < Lk) ? code[j + 1] : 0;
-                out[j / 2] = (uint8_t)(lo | (hi << 4));
+            if (bits <= 4) {
+                for (int32_t j = 0; j < Lk; j += 2) {
+                    const int32_t lo = code[j];
+                    const int32_t hi = (j + 1 < Lk) ? code[j + 1] : 0;
+                    out[j / 2] = (uint8_t)(lo | (hi << 4));
+                }
+            } else {
+                for (int32_t j = 0; j < Lk; ++j) out[j] = (uint8_t)code[j];
             }
         }
     }
@@ -504,7 +514,8 @@ int oracle_lis_attention_head(const int32_t* logits, const int32_t* bias, int32_
                               int64_t G, int32_t Lq, int32_t Lk, float s_logit, int32_t bits,
                               int32_t exp_n, const int8_t* v, int32_t zp_v, int32_t d,
                               int32_t* out, uint8_t* codes_out, int32_t ld_codes) {
-    if (lis_check(G, Lq, Lk, bits, exp_n, s_logit) != ORACLE_OK || d < 1) return ORACLE_ERR_ARG;
+    if (lis_check(G, Lq, Lk, bits, exp_n, s_logit) != ORACLE_OK || d < 1 || bits > 4)
+        return ORACLE_ERR_ARG;
     const int32_t ld = (Lk + 1) / 2;
     if (codes_out && ld_codes < ld) return ORACLE_ERR_ARG;
     if (G == 0 || Lq == 0) return ORACLE_OK;

@@ -96,9 +96,10 @@ int64_t oracle_iexp(int64_t q, const oracle_iexp_consts* k, int64_t* z_out, int6
 int32_t oracle_ilog2(uint64_t q);
 
 /* logits: [G, Lq, Lk] int32; bias: nullable [Hb, Lq, Lk] int32, unit g uses head g % Hb.
- * codes: Attn_Q in [0, 2^bits - 1], two per byte (even key in the low nibble),
- * row stride ld_codes >= ceil(Lk / 2) bytes; bytes past ceil(Lk/2) are not written.
- * bits in [1, 4]. */
+ * codes: Attn_Q in [0, 2^bits - 1]; for bits <= 4 two per byte (even key in the
+ * low nibble), row stride ld_codes >= ceil(Lk / 2) bytes; for bits in [5, 8] one
+ * per byte, ld_codes >= Lk.  Bytes past the row's codes are not written.
+ * bits in [1, 8]. */
 int oracle_lis_softmax_log4(const int32_t* logits, int64_t G, int32_t Lq, int32_t Lk,
                             const int32_t* bias, int32_t Hb, float s_logit, int32_t bits,
                             int32_t exp_n, uint8_t* codes, int32_t ld_codes);

@@ -61,6 +61,7 @@ MUTANTS = [
     ("qk_zero_point_sign", "((int64_t)qi[c] - zp_q)", "((int64_t)qi[c] + zp_q)"),
     ("qk_zp_k_dropped", "((int64_t)kj[c] - zp_k)", "((int64_t)kj[c])"),
     ("qk_k_transposed", "k + (g * Lk + j) * (int64_t)dk", "k + (g * Lk + j)"),
+    ("wide_codes_truncated", "out[j] = (uint8_t)code[j];", "out[j] = (uint8_t)(code[j] & 15);"),
 ]
 
 

@@ -250,6 +250,30 @@ def test_lis_lower_bits_clip(orc):
         assert np.array_equal(cb, np.minimum(c4, 2 ** bits - 1))
 
 
+def test_lis_wide_codes_exact(orc):
+    """Codes of 5 to 8 bits (one per byte): exact rational q_rev = round(sum/e)
+    (ties up) through the closed form of I-Log2, clipped at 2^b - 1; below 15
+    they agree with the 4-bit codes, and rows wide enough in spread reach codes
+    above 15.  Bytes past Lk in a wider row stride are left alone."""
+    a = W.attn_inputs(2, 12, 41, 8, seed=13, heads=2, sigma=(6.0, 9.0))
+    c4 = _codes_and_e(orc, a["logits"])
+    seen_wide = False
+    for bits in (5, 6, 8):
+        stored = orc.lis_softmax_log4(a["logits"], S, bits=bits, ld_codes=44)
+        assert np.all(stored[..., 41:] == 0)
+        cb = orc.unpack_codes(stored, 41, bits)
+        assert np.array_equal(np.minimum(cb, 15), c4)
+        for g in range(2):
+            for i in range(12):
+                e, _ = orc.lis_row_exp(a["logits"][g, i], S)
+                tot = int(e.astype(object).sum())
+                for j in range(41):
+                    q_rev = math.floor(Fraction(tot, int(e[j])) + Fraction(1, 2))
+                    assert cb[g, i, j] == min(ilog2_closed_form(q_rev), 2 ** bits - 1)
+        seen_wide |= bool((cb > 15).any())
+    assert seen_wide
+
+
 def test_lis_packing_layout(orc):
     """Two codes per byte, even key in the low nibble; bytes past ceil(Lk/2) in a
     wider row stride are left alone; an odd tail's high nibble is zero."""
