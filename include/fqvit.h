@@ -103,18 +103,20 @@ fq_status ptf_layernorm_int8(const int8_t* x_q, int64_t T, int32_t C, int32_t zp
  *   bias    NULL or [Hb, Lq, Lk] int32 added to the logits of unit g from
  *           head g % Hb before the row maximum (Swin relative-position bias).
  *   s_logit in [1e-4, 0.5].
- *   bits    code width b in [1, 4]; codes are Attn_Q in [0, 2^b - 1] and the
+ *   bits    code width b in [1, 8]; codes are Attn_Q in [0, 2^b - 1] and the
  *           LIS output of the paper is N - Attn_Q with N = 2^b - 1, scale 2^-N.
  *   exp_n   I-Exp clamp depth n in [1, 30]: inputs below n q_ln2 are clamped.
- *   codes   [G, Lq, ld_codes] uint8 output, two codes per byte, the even key
- *           in the low nibble; an odd row's last high nibble is 0; bytes at
- *           and beyond ceil(Lk/2) in each row are not written.
+ *   codes   [G, Lq, ld_codes] uint8 output.  b <= 4: two codes per byte, the
+ *           even key in the low nibble, an odd row's last high nibble 0, bytes
+ *           at and beyond ceil(Lk/2) in each row not written.  b >= 5: one
+ *           code per byte, bytes at and beyond Lk not written.
  * Per row: t_j = v_j - max v, e_j = I-Exp(t_j) with q_ln2 = floor(-ln2/s),
  * q_b = floor(1.353/s), q_c = floor(0.344/((0.3585 s) s)) in IEEE double,
  * S = sum e_j, Attn_Q_j = min(I-Log2(floor((2S + e_j) / (2 e_j))), 2^b - 1).
  * Errors: FQ_ERR_NULL (logits or codes NULL with G Lq > 0), FQ_ERR_SHAPE
- * (G or Lq < 0, Lk outside [1, 4096], ld_codes < ceil(Lk/2), Hb < 1 with a
- * bias), FQ_ERR_PARAM (bits, exp_n or s_logit out of range), FQ_ERR_HEADROOM
+ * (G or Lq < 0, Lk outside [1, 4096], ld_codes below ceil(Lk/2) for b <= 4 or
+ * Lk for b >= 5, Hb < 1 with a bias), FQ_ERR_PARAM (bits, exp_n or s_logit
+ * out of range), FQ_ERR_HEADROOM
  * ((2 Lk + 1) (q_b^2 + q_c) 2^n >= 2^63).
  * Precondition (not checked): |logit + bias| < 2^30.
  */
@@ -144,8 +146,8 @@ fq_status lis_attn_v_shift(const uint8_t* codes, int32_t ld_codes, const int8_t*
  * Fused Log-Int-Softmax and BitShift Attn x V, the integer-only attention of
  * Sec. 3.3 (the MSA dataflow of its Fig. 4): the same results as
  * lis_softmax_log4 followed by lis_attn_v_shift, with the codes kept on chip.
- * Arguments as in those two calls; d in [1, 256]; codes_out is NULL or a
- * [G, Lq, ld_codes] buffer that also receives the codes.
+ * Arguments as in those two calls (bits in [1, 4]); d in [1, 256]; codes_out
+ * is NULL or a [G, Lq, ld_codes] buffer that also receives the codes.
  */
 fq_status lis_attention_head(const int32_t* logits, const int32_t* bias, int32_t Hb,
                              int64_t G, int32_t Lq, int32_t Lk, float s_logit, int32_t bits,
@@ -163,7 +165,8 @@ fq_status lis_attention_head(const int32_t* logits, const int32_t* bias, int32_t
  *   q       [G, Lq, dk] int8 container, 16-byte aligned; zp_q in [-128, 127].
  *   k       [G, Lk, dk] int8 container, 16-byte aligned; zp_k in [-128, 127].
  *   dk      32 or 64.
- *   bias, Hb, s_logit, bits, exp_n, v, zp_v, out: as in lis_attention_head;
+ *   bias, Hb, s_logit, bits (in [1, 4]), exp_n, v, zp_v, out: as in
+ *           lis_attention_head;
  *           s_logit is the scale of the logits (s_q s_k, with any 1/sqrt(dk)
  *           of the softmax folded in).
  * Supported: Lk in [1, 224], d in [1, 64].

@@ -161,17 +161,19 @@ def ptf_layernorm_int8(x_q, zp_in: int, alpha, K: int, gamma, beta, s_out: float
     return _invoke("ptf_layernorm_int8", args, (x_q, alpha, gamma, beta, y_q), prepare, y_q)
 
 
-def codes_ld(Lk: int) -> int:
-    return (Lk + 1) // 2
+def codes_ld(Lk: int, bits: int = 4) -> int:
+    """Bytes per row of stored codes: two per byte up to 4 bits, else one."""
+    return (Lk + 1) // 2 if bits <= 4 else Lk
 
 
 def lis_softmax_log4(logits, s_logit: float, bits: int = 4, exp_n: int = 20, bias=None,
                      codes=None, stream=None, prepare: bool = False):
-    """Packed 4-bit Log-Int-Softmax codes [G, Lq, ld] of int32 logits [G, Lq, Lk]."""
+    """Log-Int-Softmax codes [G, Lq, ld] of int32 logits [G, Lq, Lk]: packed two
+    per byte for bits <= 4, one per byte for bits in [5, 8]."""
     import torch
     G, Lq, Lk = logits.shape
     if codes is None:
-        codes = torch.zeros((G, Lq, codes_ld(Lk)), dtype=torch.uint8, device=logits.device)
+        codes = torch.zeros((G, Lq, codes_ld(Lk, bits)), dtype=torch.uint8, device=logits.device)
     if codes.dim() != 3 or codes.shape[:2] != (G, Lq):
         raise ValueError("codes must be [G, Lq, ld_codes]")
     Hb = 0

@@ -32,7 +32,7 @@ struct ConsumeEvents {
 fq_status lis_constants(float s_logit, int32_t bits, int32_t n, int32_t Lk,
                         fqvit::LisConsts* k) {
     if (!(s_logit >= 1e-4f && s_logit <= 0.5f)) return FQ_ERR_PARAM;
-    if (bits < 1 || bits > 4 || n < 1 || n > 30) return FQ_ERR_PARAM;
+    if (bits < 1 || bits > 8 || n < 1 || n > 30) return FQ_ERR_PARAM;
     const double s = (double)s_logit;
     const double q_ln2 = std::floor(-0.69314718055994530942 / s);   // floor(-ln2 / s)
     const double q_b = std::floor(1.353 / s);                       // floor(b / s)
@@ -128,7 +128,9 @@ fq_status lis_softmax_log4(const int32_t* logits, int64_t G, int32_t Lq, int32_t
                            const int32_t* bias, int32_t Hb, float s_logit, int32_t bits,
                            int32_t exp_n, uint8_t* codes, int32_t ld_codes, void* stream) {
     ConsumeEvents consume;
-    if (G < 0 || Lq < 0 || Lk < 1 || Lk > kMaxLk || ld_codes < (Lk + 1) / 2 || (bias && Hb < 1) ||
+    // codes of up to 4 bits two per byte, wider codes one per byte
+    const int32_t row_bytes = (bits >= 5 && bits <= 8) ? Lk : (Lk + 1) / 2;
+    if (G < 0 || Lq < 0 || Lk < 1 || Lk > kMaxLk || ld_codes < row_bytes || (bias && Hb < 1) ||
         !grid_fits(G, Lq, 64))
         return FQ_ERR_SHAPE;
     fqvit::LisConsts k;
@@ -172,6 +174,7 @@ fq_status lis_attention_head(const int32_t* logits, const int32_t* bias, int32_t
         (codes_out && ld_codes < (Lk + 1) / 2) || !grid_fits(G, Lq, 64))
         return FQ_ERR_SHAPE;
     if (zp_v < -128 || zp_v > 127) return FQ_ERR_PARAM;
+    if (bits > 4) return FQ_ERR_PARAM;   // the BitShift product shifts by at most 15
     fqvit::LisConsts k;
     const fq_status st = lis_constants(s_logit, bits, exp_n, Lk, &k);
     if (st != FQ_OK) return st;
@@ -204,6 +207,7 @@ fq_status lis_attention_qk(const int8_t* q, const int8_t* k, int32_t zp_q, int32
         return FQ_ERR_SHAPE;
     if (zp_q < -128 || zp_q > 127 || zp_k < -128 || zp_k > 127 || zp_v < -128 || zp_v > 127)
         return FQ_ERR_PARAM;
+    if (bits > 4) return FQ_ERR_PARAM;   // the BitShift product shifts by at most 15
     fqvit::LisConsts kc;
     const fq_status st = lis_constants(s_logit, bits, exp_n, Lk, &kc);
     if (st != FQ_OK) return st;

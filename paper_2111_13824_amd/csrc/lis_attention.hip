@@ -60,7 +60,6 @@ __global__ __launch_bounds__(kBlock) void lis_kernel_stream(LisArgs a, LisLaunch
     }
     const RowSum rs = row_sum(sum, k);
 
-    const int nbytes = (Lk + 1) >> 1;
     const bool row_ok = (i0 + r) < a.Lq;
     uint8_t* crow = a.codes ? a.codes + (g * a.Lq + i) * (int64_t)a.ld_codes : nullptr;
     constexpr int DTMAX = 16;
@@ -91,7 +90,7 @@ __global__ __launch_bounds__(kBlock) void lis_kernel_stream(LisArgs a, LisLaunch
             code[t] = valid ? cd : 0;
             pbits[t] = valid ? (uint32_t)(ptop - (cd << 7)) : 0u;
         }
-        if (crow && row_ok) store_codes(crow, nbytes, c, kg, code);
+        if (crow && row_ok) store_codes_row(crow, Lk, k.top, c, kg, code);
         if (FUSED) {
             u32x4 av;
             av.x = pbits[0] | (pbits[1] << 16);

@@ -238,6 +238,23 @@ __device__ __forceinline__ void store_codes(uint8_t* crow, int nbytes, int c, in
     if (b1 + 1 < nbytes) crow[b1 + 1] = v3;
 }
 
+// Store the 8 codes of lane (r, kg) in chunk c of a row: nibbles for codes of
+// up to 4 bits (top <= 15), else one byte per code (keys past Lk skipped).
+__device__ __forceinline__ void store_codes_row(uint8_t* crow, int Lk, int top, int c, int kg,
+                                                const int (&code)[8]) {
+    if (top > 15) {
+        const int k0 = 32 * c + 4 * kg;
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+            if (k0 + t < Lk) crow[k0 + t] = (uint8_t)code[t];
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+            if (k0 + 16 + t < Lk) crow[k0 + 16 + t] = (uint8_t)code[4 + t];
+    } else {
+        store_codes(crow, (Lk + 1) >> 1, c, kg, code);
+    }
+}
+
 // Keys of V^T per LDS stage for a padded head dimension dpad: at most 40 KB of
 // LDS per workgroup so that several workgroups share a CU.
 constexpr int vt_stage_keys(int dpad) { return (40960 / (2 * dpad) - 8) / 32 * 32; }
@@ -676,12 +693,11 @@ __device__ __forceinline__ void unit_tile(int (&cur)[NC][8], int (&nxt)[NC][8], 
     } else {
         const int i = i0 + r;
         uint8_t* crow = a.codes + (g * a.Lq + min(i, a.Lq - 1)) * (int64_t)a.ld_codes;
-        const int nbytes = (a.Lk + 1) >> 1;
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
             int code[8];
             chunk_codes<NC, true, NT>(code, cur, zb, st, k, c);
-            if (i < a.Lq) store_codes(crow, nbytes, c, kg, code);
+            if (i < a.Lq) store_codes_row(crow, a.Lk, k.top, c, kg, code);
             if (PF + c < NC) load_one_chunk<NC, HALF>(nxt, rn, PF + c, kg, a.Lk);
             __builtin_amdgcn_sched_barrier(0);
         }
@@ -774,7 +790,6 @@ __global__ __launch_bounds__(kBlock, lis_waves_per_simd(NC)) void lis_kernel(Lis
     if (FUSED) __syncthreads();   // V^T is visible
     if (!MULTI && !active) return;
 
-    const int nbytes = (Lk + 1) >> 1;
     const bool row_ok = (i0 + r) < a.Lq;
     uint8_t* crow = FUSED ? nullptr : a.codes + (g * a.Lq + i) * (int64_t)a.ld_codes;
     f32x4 acc[DTMAX];
@@ -804,7 +819,7 @@ __global__ __launch_bounds__(kBlock, lis_waves_per_simd(NC)) void lis_kernel(Lis
         } else {
             int code[8];
             chunk_codes<NC, FP, 8>(code, lg, zb, st, k, c);
-            if (row_ok) store_codes(crow, nbytes, c, kg, code);
+            if (row_ok) store_codes_row(crow, Lk, k.top, c, kg, code);
         }
     }
 

@@ -114,7 +114,8 @@ def test_lis_validation(lib):
     assert call(G=-1) == B.FQ_ERR_SHAPE
     assert call(bias=1, Hb=0) == B.FQ_ERR_SHAPE
     assert call(bits=0) == B.FQ_ERR_PARAM
-    assert call(bits=5) == B.FQ_ERR_PARAM
+    assert call(bits=9) == B.FQ_ERR_PARAM
+    assert call(bits=5, ld=4) == B.FQ_ERR_SHAPE      # one byte per code above 4 bits
     assert call(n=0) == B.FQ_ERR_PARAM
     assert call(n=31) == B.FQ_ERR_PARAM
     assert call(s=0.6) == B.FQ_ERR_PARAM

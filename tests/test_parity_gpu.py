@@ -174,12 +174,35 @@ def test_lis_codes_scales(fq, orc, s, n):
     assert np.array_equal(got, orc.lis_softmax_log4(a["logits"], s, exp_n=n))
 
 
-@pytest.mark.parametrize("bits", [1, 2, 3, 4])
+@pytest.mark.parametrize("bits", [1, 2, 3, 4, 5, 6, 7, 8])
 def test_lis_codes_bits(fq, orc, bits):
     say("lis bits", bits)
     a = W.attn_inputs(3, 33, 77, 8, seed=bits)
     got = host(fq.lis_softmax_log4(dev(a["logits"]), S, bits=bits))
     assert np.array_equal(got, orc.lis_softmax_log4(a["logits"], S, bits=bits))
+
+
+@pytest.mark.parametrize("G,Lq,Lk,bits,sigma", [
+    (1024, 17, 197, 8, 9.0),     # unit kernel (enough units for it)
+    (6, 40, 300, 6, 6.0),        # tile kernel
+    (2, 9, 900, 5, 9.0),         # stream kernel (long rows)
+    (1024, 16, 49, 8, 9.0),
+])
+def test_lis_wide_codes_each_kernel(fq, orc, G, Lq, Lk, bits, sigma):
+    """Codes of 5 to 8 bits, one per byte, from every kernel that writes codes,
+    on rows spread enough for codes above 15, in a wider row stride whose extra
+    bytes stay untouched; integer and float paths."""
+    import torch
+    say("lis wide codes", G, Lq, Lk, bits)
+    a = W.attn_inputs(G, Lq, Lk, 8, seed=G + Lk, sigma=(sigma,))
+    for s in (S, 2e-4):
+        codes = torch.full((G, Lq, Lk + 3), 0xAB, dtype=torch.uint8, device="cuda:0")
+        fq.lis_softmax_log4(dev(a["logits"]), s, bits=bits, codes=codes)
+        got = host(codes)
+        ref = orc.lis_softmax_log4(a["logits"], s, bits=bits)
+        assert np.array_equal(got[..., :Lk], ref), s
+        assert np.all(got[..., Lk:] == 0xAB)
+        assert got[..., :Lk].max() > 15
 
 
 def test_lis_codes_bias_and_stride(fq, orc):
