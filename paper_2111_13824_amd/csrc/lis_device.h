@@ -345,20 +345,22 @@ __device__ __forceinline__ float iexp_f(int v, int mx, const LisConsts& k) {
 //     (one v_lshl_add_u64, no carry through a scalar register) has the same
 //     top 12 bits as the exact difference; adding 1/2 to 2S + e changes no
 //     comparison with the integers Y 2^m.
-//   * [2S < 3e] is the sign of the exact fma(e, -3, 2S).
-// The empty asm hides the pattern's origin so that the compiler converts it to
-// binary64 here rather than keeping the conversions of the I-Exp pass (two
-// registers per key) alive across both passes.
-__device__ __forceinline__ int code_f(int ebits, double S2h, double S2, int top) {
+//   * [2S < 3e] is the sign of fma(e, -4, X) = 2S - 3e + 1/2, exact (a
+//     half-integer below 2^52), negative exactly when the integer 2S - 3e is;
+//     -4 is an inline constant and X is dead afterwards, so this is one
+//     v_fmac_f64 into X's registers.
+// The 64-bit add compiles to v_lshl_add_u64 (no carry through a scalar
+// register).  The empty asm hides the pattern's origin so that the compiler
+// converts it to binary64 here rather than keeping the conversions of the
+// I-Exp pass (two registers per key) alive across both passes.
+__device__ __forceinline__ int code_f(int ebits, double S2h, int top) {
     asm volatile("" : "+v"(ebits));
     const double ed = (double)__int_as_float(ebits);
     const double X = S2h + ed;
     const double Y = ed * 1.5;
-    const uint64_t nyb = ~(uint64_t)__double_as_longlong(Y);
-    uint64_t d;
-    asm("v_lshl_add_u64 %0, %1, 0, %2" : "=v"(d) : "v"((uint64_t)__double_as_longlong(X)), "v"(nyb));
+    const uint64_t d = (uint64_t)__double_as_longlong(X) + ~(uint64_t)__double_as_longlong(Y);
     const int m = (int)(d >> 52);
-    const int t = (int)((uint32_t)((uint64_t)__double_as_longlong(fma(ed, -3.0, S2)) >> 32) >> 31);
+    const int t = (int)((uint32_t)((uint64_t)__double_as_longlong(fma(ed, -4.0, X)) >> 32) >> 31);
     return min(m, top) - t;
 }
 
@@ -464,7 +466,7 @@ __device__ __forceinline__ void chunk_codes(int (&code)[8], const int (&lg)[NC][
         }
         int cd;
         if constexpr (FP) {
-            cd = code_f(lg[c][t], st.S2h, st.S2f, k.top);
+            cd = code_f(lg[c][t], st.S2h, k.top);
         } else {
             const uint32_t z = (zb[c][t >> 2] >> (8 * (t & 3))) & 0xFFu;
             cd = lis_code((uint32_t)lg[c][t], z, st.rs, k);
@@ -489,7 +491,7 @@ __device__ __forceinline__ u32x4 chunk_pbits(const int (&lg)[NC][8], const uint3
         }
         int cd;
         if constexpr (FP) {
-            cd = code_f(lg[c][t], st.S2h, st.S2f, k.top);
+            cd = code_f(lg[c][t], st.S2h, k.top);
         } else {
             const uint32_t z = (zb[c][t >> 2] >> (8 * (t & 3))) & 0xFFu;
             cd = lis_code((uint32_t)lg[c][t], z, st.rs, k);

@@ -55,12 +55,13 @@ def test_iexp_float_form_exhaustive(orc, s, n):
 
 def _code_float(S2, e, top):
     """m from bits(2S + e + 1/2) + ~bits(1.5 e) (64-bit wrap), t from the sign
-    of fma(e, -3, 2S), as the kernel computes them."""
+    of fma(e, -4, X) with X = 2S + e + 1/2, as the kernel computes them (the
+    fma is evaluated exactly in extended precision and rounded once)."""
     X = (S2 + 0.5) + e
     Y = e * 1.5
     d = X.view(np.uint64) + ~Y.view(np.uint64)
     m = (d >> np.uint64(52)).astype(np.int64)
-    s3 = (S2.astype(np.longdouble) - 3 * e.astype(np.longdouble)).astype(np.float64)
+    s3 = (X.astype(np.longdouble) - 4 * e.astype(np.longdouble)).astype(np.float64)
     t = (s3.view(np.uint64) >> np.uint64(63)).astype(np.int64)
     return np.minimum(m, top) - t
 
