@@ -488,8 +488,10 @@ __global__ __launch_bounds__(rows_block(W)) void ln_rows_kernel(LnArgs a) {
     const int qlo = -(1 << (a.bits - 1));
     const int qhi = (1 << (a.bits - 1)) - 1;
     const uint32_t hi_mask = ~((1u << (21 - a.bits)) - 1u);
-    // one scalar, so that the exponent add stays one instruction
-    const uint32_t m_add = __builtin_amdgcn_readfirstlane(((uint32_t)(53 - a.bits) << 20) | 0x80000u);
+    // one opaque scalar, so that the exponent add stays one instruction (the
+    // compiler would otherwise split the constant into a subtract and an add)
+    uint32_t m_add = ((uint32_t)(53 - a.bits) << 20) | 0x80000u;
+    asm volatile("" : "+s"(m_add));
     const double amax = ldexp(1.0, a.bits), amin = ldexp(1.0, a.bits - 31);
     const double cadd = (double)a.zp_out + 512.5;
     const int lo512 = qlo + 512, hi512 = qhi + 512;
