@@ -44,8 +44,7 @@ __global__ __launch_bounds__(kBlock) void lis_kernel_stream(LisArgs a, LisLaunch
 #pragma unroll
         for (int t = 0; t < 8; ++t) mx = max(mx, lg[t]);
     }
-    mx = max(mx, __shfl_xor(mx, 16, 64));
-    mx = max(mx, __shfl_xor(mx, 32, 64));
+    mx = row4_max(mx);
 
     uint64_t sum = 0;
     for (int c = 0; c < nc; ++c) {

@@ -30,11 +30,13 @@
 // (m >= 1 always, since 2S >= 2e, and 2S < 3e forces m = 1).  Two exact
 // evaluations of this formula are implemented:
 //   * float path: I-Exp in binary32 (every intermediate is an integer below
-//     2^24) and the code in binary64 (2S + e + 1/2 below 2^52), m being the
-//     difference of the IEEE bit patterns of 2S + e + 1/2 and 1.5 e shifted
-//     right by 52 (both positive, so the pattern difference is the exponent
-//     difference minus a borrow exactly when the mantissa of the quotient
-//     falls below 1);
+//     2^24) and the code from binary64 values (2S + e below 2^52), m being the
+//     difference of the IEEE bit patterns of 2S + e and 1.5 e shifted right
+//     by 52 (both positive, so the pattern difference is the exponent
+//     difference minus a borrow exactly when the significand of the quotient
+//     falls below 1), taken on the patterns shifted right by 27 so that it is
+//     32-bit arithmetic, and [2S < 3e] a binary32 comparison of e with
+//     floor(2S / 3);
 //   * integer path (any scale the host accepts): 24-bit integer I-Exp and
 //     64-bit comparisons.  With Sp = floor(2S / 2^s), W = Sp + qL and Q = 3 qL,
 //     m = floor(log2(W / Q)) + 1 and 2S < 3e is Sp < Q; msb(W) is msb(2S) - s
@@ -70,6 +72,56 @@ __device__ __forceinline__ int64_t xcd_remap(int64_t b, int64_t total) {
 // of lane group kg are contiguous.
 __device__ __forceinline__ int chunk_pos(int j) {
     return ((j & 15) >> 2) * 8 + ((j >> 4) << 2) + (j & 3);
+}
+
+// ---------------------------------------------------------------------------
+// Reductions over the four lanes of a row (l, l ^ 16, l ^ 32, l ^ 48) with the
+// lane-swap instructions (v_permlane32_swap, v_permlane16_swap): they stay in
+// the VALU, where a shuffle would take an LDS round trip.  Swapping a value
+// with itself leaves, per lane, the value of lane l and of its partner in the
+// two results.  The whole wavefront must be active.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int row4_max(int v) {
+    const auto s = __builtin_amdgcn_permlane32_swap((uint32_t)v, (uint32_t)v, false, false);
+    v = max((int)s[0], (int)s[1]);
+    const auto t = __builtin_amdgcn_permlane16_swap((uint32_t)v, (uint32_t)v, false, false);
+    return max((int)t[0], (int)t[1]);
+}
+
+__device__ __forceinline__ int row4_sum(int v) {
+    const auto s = __builtin_amdgcn_permlane32_swap((uint32_t)v, (uint32_t)v, false, false);
+    v = (int)(s[0] + s[1]);
+    const auto t = __builtin_amdgcn_permlane16_swap((uint32_t)v, (uint32_t)v, false, false);
+    return (int)(t[0] + t[1]);
+}
+
+__device__ __forceinline__ uint64_t row4_sum(uint64_t v) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+        const auto sl = h == 0 ? __builtin_amdgcn_permlane32_swap(lo, lo, false, false)
+                               : __builtin_amdgcn_permlane16_swap(lo, lo, false, false);
+        const auto sh = h == 0 ? __builtin_amdgcn_permlane32_swap(hi, hi, false, false)
+                               : __builtin_amdgcn_permlane16_swap(hi, hi, false, false);
+        v = (((uint64_t)sh[0] << 32) | sl[0]) + (((uint64_t)sh[1] << 32) | sl[1]);
+    }
+    return v;
+}
+
+// Exact when every partial sum is (integers below 2^53 here).
+__device__ __forceinline__ double row4_sum(double v) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const uint64_t b = (uint64_t)__double_as_longlong(v);
+        const uint32_t lo = (uint32_t)b, hi = (uint32_t)(b >> 32);
+        const auto sl = h == 0 ? __builtin_amdgcn_permlane32_swap(lo, lo, false, false)
+                               : __builtin_amdgcn_permlane16_swap(lo, lo, false, false);
+        const auto sh = h == 0 ? __builtin_amdgcn_permlane32_swap(hi, hi, false, false)
+                               : __builtin_amdgcn_permlane16_swap(hi, hi, false, false);
+        v = __longlong_as_double((int64_t)(((uint64_t)sh[0] << 32) | sl[0])) +
+            __longlong_as_double((int64_t)(((uint64_t)sh[1] << 32) | sl[1]));
+    }
+    return v;
 }
 
 // ---------------------------------------------------------------------------
@@ -283,8 +335,7 @@ struct RowSum {
 };
 
 __device__ __forceinline__ RowSum row_sum(uint64_t sum, const LisConsts& k) {
-    sum += __shfl_xor(sum, 16, 64);
-    sum += __shfl_xor(sum, 32, 64);
+    sum = row4_sum(sum);
     RowSum rs;
     rs.S2 = sum << 1;
     rs.rc = (63 - __clzll((long long)rs.S2)) - 31 - k.n;
@@ -337,31 +388,78 @@ __device__ __forceinline__ float iexp_f(int v, int mx, const LisConsts& k) {
     return __builtin_ldexpf(qL, k.f_sK - __float_as_int(zb));
 }
 
-// Code of one key from e (its binary32 bit pattern), 2S and 2S + 1/2
-// (binary64; 2S + e + 1/2 < 2^52, so every value below is exact).
-//   * m = floor(log2(X / Y)) with X = 2S + e + 1/2 and Y = 1.5 e: X is a
-//     half-integer and Y 2^m an integer, so X / Y is never a power of two and
-//     the bit-pattern difference bits(X) - bits(Y) - 1 = bits(X) + ~bits(Y)
-//     (one v_lshl_add_u64, no carry through a scalar register) has the same
-//     top 12 bits as the exact difference; adding 1/2 to 2S + e changes no
-//     comparison with the integers Y 2^m.
-//   * [2S < 3e] is the sign of fma(e, -4, X) = 2S - 3e + 1/2, exact (a
-//     half-integer below 2^52), negative exactly when the integer 2S - 3e is;
-//     -4 is an inline constant and X is dead afterwards, so this is one
-//     v_fmac_f64 into X's registers.
-// The 64-bit add compiles to v_lshl_add_u64 (no carry through a scalar
-// register).  The empty asm hides the pattern's origin so that the compiler
-// converts it to binary64 here rather than keeping the conversions of the
-// I-Exp pass (two registers per key) alive across both passes.
-__device__ __forceinline__ int code_f(int ebits, double S2h, int top) {
+// Code of one key on the float path, from e (its binary32 bit pattern) and the
+// row state (2S < 2^52 an integer; every value below is exact).
+//   * m = floor(log2(X / Y)) with X = 2S + e and Y = 1.5 e.  For positive
+//     normal binary64 values, bits(X) - bits(Y) = 2^52 (E_X - E_Y) + (F_X - F_Y),
+//     so its floor quotient by 2^52 is E_X - E_Y, less one exactly when the
+//     significand of X is below that of Y: floor(log2(X / Y)).  X and Y are
+//     taken scaled by 2^-1000 (exact, still normal, biased exponents between
+//     23 and 79): their patterns are then below 2^59, and shifted right by 27
+//     they fit 32 bits.  Y = 3 e / 2 has at most 26 significant bits (e at
+//     most 24), so its pattern is a multiple of 2^27 and
+//         m = floor((floor(bits(X) / 2^27) - bits(Y) / 2^27) / 2^25),
+//     two funnel shifts and a 32-bit difference.
+//   * [2S < 3e] is e > tau, tau the largest binary32 value not above
+//     floor(2S / 3): e is an integer held exactly in binary32.
+// The empty asm hides the pattern's origin so that the compiler converts it
+// to binary64 here rather than keeping the conversions of the I-Exp pass (two
+// registers per key) alive across both passes.
+constexpr double kCodeScale = 0x1p-1000;
+
+struct RowState {
+    double S2s;     // float path: 2S 2^-1000
+    double sc;      // float path: 2^-1000, held in scalar registers (an fma
+                    // cannot take it as a literal)
+    float tau;      // float path: largest binary32 value <= floor(2S / 3)
+    RowSum rs;      // integer path
+};
+
+// floor(bits(v) / 2^27) mod 2^32 of a binary64 value
+__device__ __forceinline__ uint32_t bits_shr27(double v) {
+    const uint64_t b = (uint64_t)__double_as_longlong(v);
+    return __builtin_amdgcn_alignbit((uint32_t)(b >> 32), (uint32_t)b, 27);
+}
+
+// (floor(bits(X 2^-1000) / 2^27), bits(Y 2^-1000) / 2^27) of one key
+__device__ __forceinline__ void code_bits(int ebits, const RowState& st, uint32_t& ax,
+                                          uint32_t& ay, float& e) {
     asm volatile("" : "+v"(ebits));
-    const double ed = (double)__int_as_float(ebits);
-    const double X = S2h + ed;
-    const double Y = ed * 1.5;
-    const uint64_t d = (uint64_t)__double_as_longlong(X) + ~(uint64_t)__double_as_longlong(Y);
-    const int m = (int)(d >> 52);
-    const int t = (int)((uint32_t)((uint64_t)__double_as_longlong(fma(ed, -4.0, X)) >> 32) >> 31);
-    return min(m, top) - t;
+    e = __int_as_float(ebits);
+    const double ed = (double)e;
+    ax = bits_shr27(fma(ed, st.sc, st.S2s));
+    ay = bits_shr27(ed * (1.5 * kCodeScale));
+}
+
+__device__ __forceinline__ int code_f(int ebits, const RowState& st, int top) {
+    uint32_t ax, ay;
+    float e;
+    code_bits(ebits, st, ax, ay, e);
+    const int m = (int)((ax - ay) >> 25);
+    return min(m, top) - (e > st.tau ? 1 : 0);
+}
+
+// top - code for top <= 15: with kr = (top + 1) 2^25 - 1, the saturated
+// difference kr - (ax - ay) = (top - m) 2^25 + (2^25 - 1 - (ax - ay) mod 2^25)
+// has max(top - m, 0) as its quotient by 2^25 (ay + kr stays below 2^32: the
+// biased exponent of Y 2^-1000 is below 80).  min(m, top) - [2S < 3e] is
+// top minus that quotient minus the comparison.
+__device__ __forceinline__ uint32_t code_rev_f(int ebits, const RowState& st, uint32_t kr) {
+    uint32_t ax, ay;
+    float e;
+    code_bits(ebits, st, ax, ay, e);
+    const uint32_t r = __builtin_elementwise_sub_sat(ay + kr, ax) >> 25;
+    return r + (e > st.tau ? 1u : 0u);
+}
+
+// Largest binary32 value <= floor(S2 / 3), S2 an integer below 2^53: the
+// binary64 quotient is S2 / 3 rounded to a grid of at most 1/2, so its floor
+// is floor(S2 / 3); the conversion rounds to nearest and is stepped down when
+// it lands above.
+__device__ __forceinline__ float third_floor_f32(double S2) {
+    const double q = floor(S2 / 3.0);
+    const float f = (float)q;
+    return (double)f > q ? __int_as_float(__float_as_int(f) - 1) : f;
 }
 
 // Wavefronts per SIMD the register allocation aims for: the logits of NC chunks
@@ -383,16 +481,8 @@ __device__ __forceinline__ int tile_max(const int (&lg)[NC][8]) {
 #pragma unroll
         for (int t = 0; t < 8; t += 2) mx = max(mx, max(lg[c][t], lg[c][t + 1]));
     }
-    mx = max(mx, __shfl_xor(mx, 16, 64));
-    mx = max(mx, __shfl_xor(mx, 32, 64));
-    return mx;
+    return row4_max(mx);
 }
-
-struct RowState {
-    double S2f;     // float path: 2S
-    double S2h;     // float path: 2S + 1/2
-    RowSum rs;      // integer path
-};
 
 template <int NC, bool FP, int NT>
 __device__ __forceinline__ RowState tile_iexp(int (&lg)[NC][8], uint32_t (&zb)[NC][2],
@@ -417,10 +507,12 @@ __device__ __forceinline__ RowState tile_iexp(int (&lg)[NC][8], uint32_t (&zb)[N
             __builtin_amdgcn_sched_barrier(0);
         }
         double sum = (part[0] + part[1]) + (part[2] + part[3]);
-        sum += __shfl_xor(sum, 16, 64);
-        sum += __shfl_xor(sum, 32, 64);
-        st.S2f = 2.0 * sum;
-        st.S2h = st.S2f + 0.5;
+        sum = row4_sum(sum);
+        const double S2 = 2.0 * sum;
+        st.S2s = S2 * kCodeScale;
+        st.sc = kCodeScale;
+        asm volatile("" : "+s"(st.sc));
+        st.tau = third_floor_f32(S2);
     } else {
         uint64_t sum = 0;
 #pragma unroll
@@ -466,7 +558,7 @@ __device__ __forceinline__ void chunk_codes(int (&code)[8], const int (&lg)[NC][
         }
         int cd;
         if constexpr (FP) {
-            cd = code_f(lg[c][t], st.S2h, k.top);
+            cd = code_f(lg[c][t], st, k.top);
         } else {
             const uint32_t z = (zb[c][t >> 2] >> (8 * (t & 3))) & 0xFFu;
             cd = lis_code((uint32_t)lg[c][t], z, st.rs, k);
@@ -476,31 +568,43 @@ __device__ __forceinline__ void chunk_codes(int (&code)[8], const int (&lg)[NC][
 }
 
 // bf16 operand of P = 2^(N - code) for chunk c (masked keys 0), as four
-// dwords holding the pairs (t, t + 1).
+// dwords holding the pairs (t, t + 1).  Float path: the bf16 pattern of
+// 2^(N - code) is (127 + N - code) << 7, built from code_rev_f.
 template <int NC, bool FP, int NT>
 __device__ __forceinline__ u32x4 chunk_pbits(const int (&lg)[NC][8], const uint32_t (&zb)[NC][2],
                                              const RowState& st, const LisConsts& k, int c) {
     const bool last = c == NC - 1;
-    const float ptop = (float)(1 << k.top);
-    float P[8];
+    if constexpr (FP) {
+        const uint32_t kr = ((uint32_t)(k.top + 1) << 25) - 1u;
+        uint32_t ex[8];
 #pragma unroll
-    for (int t = 0; t < 8; ++t) {
-        if (last && t >= NT) {
-            P[t] = 0.0f;
-            continue;
+        for (int t = 0; t < 8; ++t) {
+            if (last && t >= NT) {
+                ex[t] = 0;
+                continue;
+            }
+            const uint32_t x = 127u + code_rev_f(lg[c][t], st, kr);
+            ex[t] = (last && lg[c][t] == 0) ? 0u : x;
         }
-        int cd;
-        if constexpr (FP) {
-            cd = code_f(lg[c][t], st.S2h, k.top);
-        } else {
+        return u32x4{(ex[0] | (ex[1] << 16)) << 7, (ex[2] | (ex[3] << 16)) << 7,
+                     (ex[4] | (ex[5] << 16)) << 7, (ex[6] | (ex[7] << 16)) << 7};
+    } else {
+        const float ptop = (float)(1 << k.top);
+        float P[8];
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            if (last && t >= NT) {
+                P[t] = 0.0f;
+                continue;
+            }
             const uint32_t z = (zb[c][t >> 2] >> (8 * (t & 3))) & 0xFFu;
-            cd = lis_code((uint32_t)lg[c][t], z, st.rs, k);
+            const int cd = lis_code((uint32_t)lg[c][t], z, st.rs, k);
+            const float p = __builtin_ldexpf(ptop, -cd);
+            P[t] = (last && lg[c][t] == 0) ? 0.0f : p;
         }
-        const float p = __builtin_ldexpf(ptop, -cd);
-        P[t] = (last && lg[c][t] == 0) ? 0.0f : p;
+        return u32x4{bf16_pair(P[0], P[1]), bf16_pair(P[2], P[3]), bf16_pair(P[4], P[5]),
+                     bf16_pair(P[6], P[7])};
     }
-    return u32x4{bf16_pair(P[0], P[1]), bf16_pair(P[2], P[3]), bf16_pair(P[4], P[5]),
-                 bf16_pair(P[6], P[7])};
 }
 
 // acc[dt] += P x V^T for chunk c (cs: its index inside the current V^T stage).

@@ -119,8 +119,7 @@ __global__ __launch_bounds__(kBlock, 3) void lis_qk_kernel(LisArgs a, QkArgs qa,
             sq = __builtin_amdgcn_sdot4((int)qb8, 0x01010101, sq, false);
             sq = __builtin_amdgcn_sdot4((int)(qb8 >> 32), 0x01010101, sq, false);
         }
-        sq += __shfl_xor(sq, 16, 64);
-        sq += __shfl_xor(sq, 32, 64);
+        sq = row4_sum(sq);
         const int ncq = dkzz - qa.zk * sq;   // minus the per-query term
 
         // logits of this tile in the Log-Int-Softmax lane layout

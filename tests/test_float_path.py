@@ -53,17 +53,50 @@ def test_iexp_float_form_exhaustive(orc, s, n):
     assert np.array_equal(got, ref)
 
 
+SCALE = 2.0 ** -1000
+
+
+def _shr27(v):
+    """floor(bits(v) / 2^27) mod 2^32 (the funnel shift of the two words)."""
+    return (v.view(np.uint64) >> np.uint64(27)) & np.uint64(0xFFFFFFFF)
+
+
+def _third_floor_f32(S2):
+    """Largest binary32 value <= floor(S2 / 3), as the kernel forms it: the
+    binary64 quotient floored, converted to nearest and stepped down when
+    above."""
+    q = np.floor(S2 / 3.0)
+    f = q.astype(np.float32)
+    down = (f.astype(np.float64) > q)
+    f = np.where(down, (f.view(np.int32) - 1).view(np.float32), f)
+    return f.astype(np.float32)
+
+
+def _code_parts(S2, e):
+    """(m, t) as the kernel computes them: m from the funnel-shifted patterns
+    of (2S + e) 2^-1000 and 1.5 e 2^-1000, t = [e > tau]."""
+    X = (S2 * SCALE) + e * SCALE          # one rounding of an exact value
+    Y = e * (1.5 * SCALE)
+    ax, ay = _shr27(X), _shr27(Y)
+    m = (((ax - ay) & np.uint64(0xFFFFFFFF)) >> np.uint64(25)).astype(np.int64)
+    t = (e.astype(np.float32) > _third_floor_f32(S2)).astype(np.int64)
+    return ax, ay, m, t
+
+
 def _code_float(S2, e, top):
-    """m from bits(2S + e + 1/2) + ~bits(1.5 e) (64-bit wrap), t from the sign
-    of fma(e, -4, X) with X = 2S + e + 1/2, as the kernel computes them (the
-    fma is evaluated exactly in extended precision and rounded once)."""
-    X = (S2 + 0.5) + e
-    Y = e * 1.5
-    d = X.view(np.uint64) + ~Y.view(np.uint64)
-    m = (d >> np.uint64(52)).astype(np.int64)
-    s3 = (X.astype(np.longdouble) - 4 * e.astype(np.longdouble)).astype(np.float64)
-    t = (s3.view(np.uint64) >> np.uint64(63)).astype(np.int64)
+    _, _, m, t = _code_parts(S2, e)
     return np.minimum(m, top) - t
+
+
+def _code_rev_float(S2, e, top):
+    """top - code as the fused kernel forms it: the saturated difference
+    (top + 1) 2^25 - 1 + ay - ax, shifted right by 25, plus t."""
+    ax, ay, _, t = _code_parts(S2, e)
+    kr = np.uint64(((top + 1) << 25) - 1)
+    a = (ay + kr).astype(np.int64)
+    assert np.all(a < 2 ** 32)
+    s = np.maximum(a - ax.astype(np.int64), 0)
+    return (s >> 25) + t
 
 
 def test_code_float_form_at_thresholds(orc):
@@ -85,10 +118,12 @@ def test_code_float_form_at_thresholds(orc):
             cases.append((S2, e))
     S2 = np.array([c[0] for c in cases], dtype=np.float64)
     e = np.array([c[1] for c in cases], dtype=np.float64)
-    for top in (1, 3, 7, 15):
+    for top in (1, 3, 7, 15, 31, 255):
         got = _code_float(S2, e, top)
         ref = np.array([min(orc.ilog2((a + b) // (2 * b)), top) for a, b in cases])
         assert np.array_equal(got, ref)
+        if top <= 15:
+            assert np.array_equal(_code_rev_float(S2, e, top), top - ref)
 
 
 def test_code_float_form_on_rows(orc):
@@ -102,3 +137,5 @@ def test_code_float_form_on_rows(orc):
         codes = orc.unpack_codes(orc.lis_softmax_log4(row[None, None, :], 2.0 ** -10), Lk)[0, 0]
         got = _code_float(np.full(Lk, S2), e.astype(np.float64), 15)
         assert np.array_equal(got, codes.astype(np.int64))
+        got = _code_rev_float(np.full(Lk, S2), e.astype(np.float64), 15)
+        assert np.array_equal(got, 15 - codes.astype(np.int64))
