@@ -369,23 +369,22 @@ __device__ __forceinline__ int lis_code(uint32_t qL, uint32_t z, const RowSum& r
 // Float path
 // ---------------------------------------------------------------------------
 
-// I-Exp of one key in binary32: returns e = qL 2^(n - z) exactly.  u = -q is
-// clamped to n d (q <- max(q, n q_ln2)); z = floor(u / d) is the integer
-// nearest to u / d + 0.5 / d - 0.5, whose distance to the rounding boundaries
-// (at least 0.5 / d >= 2^-17) exceeds the error of the fma (below 2^-18 for
-// z <= 30); adding 1.5 * 2^23 rounds it to that integer, leaves z in the low
-// mantissa bits, and the exponent argument n - z is read from them.  Then
-// q_p + q_b = q_b - u + z d and qL = (q_p + q_b)^2 + q_c are integers below
-// 2^24, computed exactly by fma.
+// I-Exp of one key for the float path: e = qL 2^(n - z) as a binary32 value
+// (exact: qL < 2^24).  z, q_p + q_b and qL come from the 24-bit integer
+// steps of iexp_qL (magic division by a multiply-high, two 24-bit
+// multiply-adds), which cost less than binary32 arithmetic; the host accepts
+// only scales for which those steps are exact.  k.magic and the shifted u are
+// below 2^24, so the product maps to one v_mul_hi_u32_u24.
 __device__ __forceinline__ float iexp_f(int v, int mx, const LisConsts& k) {
     const uint32_t u = min((uint32_t)mx - (uint32_t)v, k.u_max);
-    const float uf = (float)u;
-    const float t = __builtin_fmaf(uf, k.f_inv_d, k.f_c0);
-    const float zb = t + 12582912.0f;            // 1.5 * 2^23 + z
-    const float zf = zb - 12582912.0f;
-    const float w = __builtin_fmaf(zf, k.f_d, k.f_qb - uf);
-    const float qL = __builtin_fmaf(w, w, k.f_qc);
-    return __builtin_ldexpf(qL, k.f_sK - __float_as_int(zb));
+    const uint32_t z =
+        (uint32_t)(((uint64_t)((u << k.pre) & 0xFFFFFFu) * (uint64_t)(k.magic & 0xFFFFFFu)) >> 32);
+    // q_p + q_b = z d + (q_b - u); written out because the compiler would
+    // otherwise select a 64-bit multiply-add
+    uint32_t w;
+    asm("v_mad_u32_u24 %0, %1, %2, %3" : "=v"(w) : "v"(z), "s"(k.d_ln2), "v"(k.qb - u));
+    const uint32_t qL = __umul24(w, w) + k.qc;
+    return __builtin_ldexpf((float)qL, k.n - (int)z);
 }
 
 // Code of one key on the float path, from e (its binary32 bit pattern) and the
@@ -822,6 +821,8 @@ __global__ __launch_bounds__(kBlock, 3) void lis_unit_kernel(LisArgs a, LisLaunc
 
     LisConsts k = a.k;
     k.u_max &= 0xFFFFFFu;
+    k.d_ln2 &= 0xFFFFFFu;
+    k.magic &= 0xFFFFFFu;
 
     StageRegs sr;
     if constexpr (FUSED)

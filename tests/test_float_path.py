@@ -1,42 +1,37 @@
-"""The float form of I-Exp and of the LIS code, as the fused head evaluates it
-(binary32 I-Exp, binary64 code), against the oracle's integer definitions.
+"""The float-path form of I-Exp and of the LIS code, as the fused kernels
+evaluate it (24-bit integer I-Exp steps ending in a binary32 value, the code
+from binary64 bit patterns and a binary32 comparison), against the oracle's
+integer definitions.
 
 The GPU parity tests compare the kernels with the oracle on sampled inputs;
-these tests establish, on the CPU, that the float formulation itself equals
-the definition on every input the I-Exp can see and at the exact code
-thresholds.  The binary32 fused multiply-add is emulated exactly: the product
-of two binary32 values is exact in the x87 extended format, the sum with the
-addend here stays within its 64-bit significand, and one rounding to binary32
-follows."""
+these tests establish, on the CPU, that the formulation itself equals the
+definition on every input the I-Exp can see and at the exact code
+thresholds."""
 import numpy as np
 import pytest
-
-F32_MAGIC = np.float32(12582912.0)   # 1.5 * 2^23
-
-
-def _fma32(a, b, c):
-    return (a.astype(np.longdouble) * b.astype(np.longdouble)
-            + np.asarray(c, dtype=np.longdouble)).astype(np.float32)
 
 
 def _float_consts(k):
     d = -k.q_ln2
-    return dict(inv_d=np.float32(1.0 / d), c0=np.float32(0.5 / d - 0.5), d=np.float32(d),
-                qb=np.float32(k.q_b), qc=np.float32(k.q_c), sK=np.int64(0x4B400000 + k.n),
-                umax=np.uint32(k.n * d))
+    pre = 0
+    while (d << pre) <= 256:
+        pre += 1
+    dp = d << pre
+    return dict(d=d, qb=int(k.q_b), qc=int(k.q_c), n=k.n, umax=np.uint64(k.n * d), pre=pre,
+                magic=(1 << 32) // dp + 1, ok=k.n * dp * dp < 2 ** 32 and k.n * dp < 2 ** 24)
 
 
 def _iexp_float(u_raw, f):
-    """e = qL 2^(n - z) from u = -q by the float steps of the kernel."""
-    u = np.minimum(u_raw.astype(np.uint32), f["umax"])
-    uf = u.astype(np.float32)
-    t = _fma32(uf, np.full_like(uf, f["inv_d"]), f["c0"])
-    zb = (t + F32_MAGIC).astype(np.float32)
-    zf = (zb - F32_MAGIC).astype(np.float32)
-    w = _fma32(zf, np.full_like(zf, f["d"]), (f["qb"] - uf).astype(np.float32))
-    qL = _fma32(w, w, f["qc"])
-    shift = f["sK"] - zb.view(np.int32).astype(np.int64)
-    return np.ldexp(qL.astype(np.float64), shift)
+    """e = qL 2^(n - z) from u = -q by the kernel's steps: z by the 24-bit
+    multiply-high with the magic constant, q_p + q_b and qL by 24-bit
+    multiply-adds, then a binary32 conversion and ldexp."""
+    u = np.minimum(u_raw.astype(np.uint64), f["umax"])
+    z = (((u << np.uint64(f["pre"])) & np.uint64(0xFFFFFF)) * np.uint64(f["magic"])) >> np.uint64(32)
+    w = (z * np.uint64(f["d"]) + np.uint64(f["qb"]) - u) & np.uint64(0xFFFFFFFF)
+    qL = (w * w + np.uint64(f["qc"])) & np.uint64(0xFFFFFFFF)
+    assert np.all(qL < 2 ** 24)
+    shift = np.int64(f["n"]) - z.astype(np.int64)
+    return np.ldexp(qL.astype(np.float32).astype(np.float64), shift)
 
 
 @pytest.mark.parametrize("s", [0.5, 0.05, 2.0 ** -10, 0.0005])
@@ -47,6 +42,8 @@ def test_iexp_float_form_exhaustive(orc, s, n):
     if k.q_b ** 2 + k.q_c >= 2 ** 24:
         pytest.skip("outside the float path's bound")
     f = _float_consts(k)
+    if not f["ok"]:
+        pytest.skip("outside the magic division's bound")
     u = np.arange(n * d + 4, dtype=np.int64)          # every clamped input, plus beyond the clamp
     got = _iexp_float(u, f)
     ref = np.array([orc.iexp(-int(x), k)[0] for x in u], dtype=np.float64)
