@@ -2,17 +2,17 @@
 // requantization of an int32 accumulator (the integer form of Supplement A.1)
 // for gfx950.
 //
-// Calibration runs four kernels:
+// Calibration runs five kernels:
 //   1. minmax_partial  per-workgroup minimum and maximum of x;
-//   2. alpha_partial   the layer-wise scale s = (max - min) / (2^b - 1) / 2^K
+//   2. calib_params    the layer-wise scale s = (max - min) / (2^b - 1) / 2^K
 //                      and zero point zp = clip(rint(-min / (2^K s)), 0, 2^b - 1)
-//                      in binary64 (eq. 9, 10), each operation rounded once,
-//                      then for every channel c and block of 64 consecutive
-//                      rows the squared errors of the K + 1 candidate grids
-//                      summed in row order (eq. 11 with its zero point and clip);
-//   3. alpha_sum       per channel and alpha, the block sums added in block order;
-//   4. alpha_argmin    per channel, the argmin over alpha (the smallest on ties).
-// Steps 2 and 3 reproduce the blocked summation order exactly, so the argmin
+//                      in binary64 (eq. 9, 10), each operation rounded once;
+//   3. alpha_partial   for every channel c and block of 64 consecutive rows
+//                      the squared errors of the K + 1 candidate grids summed
+//                      in row order (eq. 11 with its zero point and clip);
+//   4. alpha_sum       per channel and alpha, the block sums added in block order;
+//   5. alpha_argmin    per channel, the argmin over alpha (the smallest on ties).
+// Steps 3 and 4 reproduce the blocked summation order exactly, so the argmin
 // is a pure function of x.  x / (2^alpha s) is computed as ldexp(x / s,
 // -alpha): scaling by a power of two commutes with the rounding of the
 // quotient, which never leaves the normal range for binary32 inputs.
@@ -118,30 +118,40 @@ __device__ void calib_params(const float* part, int nparts, int bits, int K, dou
     zp_out = (int32_t)z - half;
 }
 
-// Workgroup (cx, k): channels cx*64 .. cx*64 + 63 (one per lane) and the
-// rows of block k; wavefront w computes the terms (x - deq_a(x))^2 of rows
-// 16 w .. 16 w + 15 of the block.  Each candidate's terms go through LDS and
-// one wavefront then adds that candidate's 64 terms in row order:
-// part[(a nb + k) C + c] = ((0 + term_0) + term_1) + ...  Every
-// workgroup derives s and zp from the min/max partials; workgroup (0, 0)
-// also stores them.
-constexpr int kRowsPerWave = kPtfErrBlock / (kBlock / 64);
-
-template <int K>
-__global__ __launch_bounds__(kBlock) void alpha_partial_kernel(const float* x, int64_t T, int C,
-                                                               int bits, const float* mm,
-                                                               int nparts, double* s_store,
-                                                               int32_t* zp_store, int64_t nb,
-                                                               double* part) {
-    __shared__ double term[kPtfErrBlock][64];      // 32 KB: one candidate at a time
+// One workgroup: s and zp from the min/max partials, stored for the kernels
+// that follow.
+__global__ __launch_bounds__(kBlock) void calib_params_kernel(const float* mm, int nparts, int bits,
+                                                              int K, double* s_store,
+                                                              int32_t* zp_store) {
     double s;
     int32_t zpc;
     calib_params(mm, nparts, bits, K, s, zpc);
-    if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) {
+    if (threadIdx.x == 0) {
         *s_store = s;
         *zp_store = zpc;
     }
-    if (!(s > 0.0)) return;                        // uniform over the grid
+}
+
+// Workgroup (cx, k): channels cx*64 .. cx*64 + 63 (one per lane) and the
+// rows of block k, taken in two halves of 32 rows.  For each half, every
+// wavefront loads 8 of its rows and forms x / s (one correctly rounded
+// division per element); x and the quotient go to LDS.  Wavefront w takes the
+// candidates alpha = w, w + 4, ...: it runs down the rows in order and adds
+// the terms (x - deq_a(x))^2 one at a time, carrying its sums from the first
+// half to the second, part[(a nb + k) C + c] = ((0 + term_0) + term_1) + ...
+// The row loads are issued before s and zp are read.
+constexpr int kHalfRows = kPtfErrBlock / 2;
+constexpr int kRowsPerWave = kHalfRows / (kBlock / 64);
+constexpr int kAlphaPerWave = 2;    // candidates per wavefront (K <= 7)
+
+template <int K>
+__global__ __launch_bounds__(kBlock) void alpha_partial_kernel(const float* x, int64_t T, int C,
+                                                               int bits, const double* s_ptr,
+                                                               const int32_t* zp_ptr, int64_t nb,
+                                                               double* part) {
+    static_assert(K + 1 <= kAlphaPerWave * (kBlock / 64), "candidates per wavefront");
+    __shared__ float xs[kHalfRows][64];            // 8 KB
+    __shared__ double qs[kHalfRows][64];           // 16 KB: x / s
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int c = blockIdx.x * 64 + lane;
@@ -149,35 +159,58 @@ __global__ __launch_bounds__(kBlock) void alpha_partial_kernel(const float* x, i
     const int64_t t0 = k * kPtfErrBlock;
     const int nt = (int)min<int64_t>(kPtfErrBlock, T - t0);   // rows in this block
     const int r0 = wave * kRowsPerWave;
-    const double zp = (double)(zpc + (1 << (bits - 1)));
-    const double levels = (double)((1 << bits) - 1);
 
-    double xv[kRowsPerWave], q0[kRowsPerWave];
+    float xv[2][kRowsPerWave];
 #pragma unroll
-    for (int i = 0; i < kRowsPerWave; ++i) {
-        const bool ok = c < C && r0 + i < nt;
-        xv[i] = ok ? (double)x[(t0 + r0 + i) * C + c] : 0.0;
-    }
-#pragma unroll
-    for (int i = 0; i < kRowsPerWave; ++i) q0[i] = xv[i] / s;
-
-#pragma unroll
-    for (int a = 0; a <= K; ++a) {
-        const double step = ldexp(s, a);
+    for (int h = 0; h < 2; ++h) {
 #pragma unroll
         for (int i = 0; i < kRowsPerWave; ++i) {
-            const double q = fmin(fmax(rint(ldexp(q0[i], -a)) + zp, 0.0), levels);
-            const double deq = (q - zp) * step;
-            const double e = xv[i] - deq;
-            term[r0 + i][lane] = e * e;
+            const int r = h * kHalfRows + r0 + i;
+            xv[h][i] = (c < C && r < nt) ? x[(t0 + r) * C + c] : 0.0f;
+        }
+    }
+    const double s = *s_ptr;
+    const int32_t zpc = *zp_ptr;
+    if (!(s > 0.0)) return;                        // uniform over the grid
+    const double zp = (double)(zpc + (1 << (bits - 1)));
+    const double lo = -zp, hi = (double)((1 << bits) - 1) - zp;
+
+    double acc[kAlphaPerWave];
+#pragma unroll
+    for (int j = 0; j < kAlphaPerWave; ++j) acc[j] = 0.0;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        if (h) __syncthreads();                    // the first half is consumed
+#pragma unroll
+        for (int i = 0; i < kRowsPerWave; ++i) {
+            xs[r0 + i][lane] = xv[h][i];
+            qs[r0 + i][lane] = (double)xv[h][i] / s;
         }
         __syncthreads();
-        if (wave == (a & 3)) {      // the summing wavefront rotates with a
-            double acc = 0.0;
-            for (int r = 0; r < nt; ++r) acc = acc + term[r][lane];
-            if (c < C) part[((int64_t)a * nb + k) * C + c] = acc;
+        const int nh = min(kHalfRows, nt - h * kHalfRows);
+#pragma unroll
+        for (int j = 0; j < kAlphaPerWave; ++j) {
+            const int a = wave + j * (kBlock / 64);
+            if (a > K) break;
+            const double step = ldexp(s, a);
+            double sum = acc[j];
+            // clamp(rint(.) + zp, 0, levels) - zp as one clamp of the integer
+            // rint(.) to [-zp, levels - zp]: the same value, all exact
+#pragma unroll 8
+            for (int r = 0; r < nh; ++r) {
+                const double qz = fmin(fmax(rint(ldexp(qs[r][lane], -a)), lo), hi);
+                const double deq = qz * step;
+                const double e = (double)xs[r][lane] - deq;
+                const double term = e * e;
+                sum = sum + term;
+            }
+            acc[j] = sum;
         }
-        __syncthreads();
+    }
+#pragma unroll
+    for (int j = 0; j < kAlphaPerWave; ++j) {
+        const int a = wave + j * (kBlock / 64);
+        if (a <= K && c < C) part[((int64_t)a * nb + k) * C + c] = acc[j];
     }
 }
 
@@ -337,10 +370,10 @@ size_t ptf_calibrate_workspace_bytes(int64_t T, int32_t C, int32_t K) {
 }
 
 template <int K>
-void launch_alpha_partial(const PtfCalibArgs& a, dim3 grid, const float* mm, int nparts,
-                          int64_t nb, double* part, hipStream_t stream) {
+void launch_alpha_partial(const PtfCalibArgs& a, dim3 grid, int64_t nb, double* part,
+                          hipStream_t stream) {
     launch_kernel(alpha_partial_kernel<K>, grid, dim3(kBlock), 0, stream, a.x, a.T, a.C, a.bits,
-                  mm, nparts, a.s, a.zp, nb, part);
+                  (const double*)a.s, (const int32_t*)a.zp, nb, part);
 }
 
 hipError_t launch_ptf_calibrate(const PtfCalibArgs& a, hipStream_t stream) {
@@ -355,17 +388,19 @@ hipError_t launch_ptf_calibrate(const PtfCalibArgs& a, hipStream_t stream) {
     set_launch_events(ev.start, nullptr);
     launch_kernel(minmax_partial_kernel, dim3(nb1), dim3(kBlock), 0, stream, a.x, n, vec4, mm);
     set_launch_events(nullptr, nullptr);
+    launch_kernel(calib_params_kernel, dim3(1), dim3(kBlock), 0, stream, (const float*)mm,
+                  (int)nb1, a.bits, a.K, a.s, a.zp);
     const int64_t nb = (a.T + kPtfErrBlock - 1) / kPtfErrBlock;
     const dim3 g3((unsigned)((a.C + 63) / 64), (unsigned)nb);
     switch (a.K) {
-        case 0: launch_alpha_partial<0>(a, g3, mm, (int)nb1, nb, part, stream); break;
-        case 1: launch_alpha_partial<1>(a, g3, mm, (int)nb1, nb, part, stream); break;
-        case 2: launch_alpha_partial<2>(a, g3, mm, (int)nb1, nb, part, stream); break;
-        case 3: launch_alpha_partial<3>(a, g3, mm, (int)nb1, nb, part, stream); break;
-        case 4: launch_alpha_partial<4>(a, g3, mm, (int)nb1, nb, part, stream); break;
-        case 5: launch_alpha_partial<5>(a, g3, mm, (int)nb1, nb, part, stream); break;
-        case 6: launch_alpha_partial<6>(a, g3, mm, (int)nb1, nb, part, stream); break;
-        default: launch_alpha_partial<7>(a, g3, mm, (int)nb1, nb, part, stream); break;
+        case 0: launch_alpha_partial<0>(a, g3, nb, part, stream); break;
+        case 1: launch_alpha_partial<1>(a, g3, nb, part, stream); break;
+        case 2: launch_alpha_partial<2>(a, g3, nb, part, stream); break;
+        case 3: launch_alpha_partial<3>(a, g3, nb, part, stream); break;
+        case 4: launch_alpha_partial<4>(a, g3, nb, part, stream); break;
+        case 5: launch_alpha_partial<5>(a, g3, nb, part, stream); break;
+        case 6: launch_alpha_partial<6>(a, g3, nb, part, stream); break;
+        default: launch_alpha_partial<7>(a, g3, nb, part, stream); break;
     }
     double* err = part + (int64_t)(a.K + 1) * nb * a.C;
     launch_kernel(alpha_sum_kernel, dim3((unsigned)((a.C + 63) / 64), (unsigned)(a.K + 1)),
