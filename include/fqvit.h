@@ -160,7 +160,9 @@ fq_status lis_attention_head(const int32_t* logits, const int32_t* bias, int32_t
  * Log-Int-Softmax and the BitShift Attn x V of Sec. 3.3 (the dataflow of its
  * Fig. 4), with the logits and codes kept on chip:
  *   logit[g,i,j] = sum_c (q[g,i,c] - zp_q)(k[g,j,c] - zp_k) (+ bias),
- * then exactly lis_attention_head on those logits.
+ * then exactly lis_attention_head on those logits.  Log-Int-Softmax depends
+ * only on the differences of a row's logits, so the result does not depend on
+ * zp_k (it is still validated); the kernel drops the per-query terms.
  *
  *   q       [G, Lq, dk] int8 container, 16-byte aligned; zp_q in [-128, 127].
  *   k       [G, Lk, dk] int8 container, 16-byte aligned; zp_k in [-128, 127].

@@ -17,9 +17,11 @@
 // With zero points (int8 containers; the 2^(b-1) offset cancels):
 //   sum_c (q - zq)(k - zk) = S - zk sum_c q - zq sum_c k + dk zq zk,
 // S = sum_c q k from the MFMA; the per-key term zq sum_c k is computed once per
-// unit (stored negated), the per-query term zk sum_c q - dk zq zk once per
-// tile, and each logit is one three-operand add.  All sums are
-// exact in int32 (|logit| <= dk 255^2 < 2^24 for dk <= 256).
+// unit (stored negated) and added to S.  The per-query term dk zq zk - zk
+// sum_c q is left out: it is the same for every key of a row, and the
+// Log-Int-Softmax of a row depends only on the differences of its logits
+// (I-Exp takes max - v).  All sums are exact in int32 (|S| <= dk 255^2 < 2^24
+// for dk <= 256).
 #pragma once
 
 #include "lis_device.h"
@@ -95,7 +97,6 @@ __global__ __launch_bounds__(kBlock, 3) void lis_qk_kernel(LisArgs a, QkArgs qa,
 
     const int8_t* q_base = qa.q + g * (int64_t)a.Lq * DK;
     const int32_t* bplane = a.bias ? a.bias + (g % a.Hb) * (int64_t)a.Lq * a.Lk : nullptr;
-    const int dkzz = DK * qa.zq * qa.zk;
 
     for (int tile = (wave + (int)(g & 3)) & 3; tile < p.ntiles; tile += 4) {
         const int i0 = 16 * tile;
@@ -104,23 +105,13 @@ __global__ __launch_bounds__(kBlock, 3) void lis_qk_kernel(LisArgs a, QkArgs qa,
         const int8_t* qrow = q_base + (int64_t)i * DK;
         i32x4v qb[DK >= 64 ? DK / 64 : 1];
         int64_t qb8 = 0;
-        int sq = 0;
         if constexpr (DK >= 64) {
 #pragma unroll
-            for (int m = 0; m < DK / 64; ++m) {
+            for (int m = 0; m < DK / 64; ++m)
                 qb[m] = *reinterpret_cast<const i32x4v*>(qrow + 64 * m + 16 * kg);
-                sq = __builtin_amdgcn_sdot4(qb[m].x, 0x01010101, sq, false);
-                sq = __builtin_amdgcn_sdot4(qb[m].y, 0x01010101, sq, false);
-                sq = __builtin_amdgcn_sdot4(qb[m].z, 0x01010101, sq, false);
-                sq = __builtin_amdgcn_sdot4(qb[m].w, 0x01010101, sq, false);
-            }
         } else {
             qb8 = *reinterpret_cast<const int64_t*>(qrow + 8 * kg);
-            sq = __builtin_amdgcn_sdot4((int)qb8, 0x01010101, sq, false);
-            sq = __builtin_amdgcn_sdot4((int)(qb8 >> 32), 0x01010101, sq, false);
         }
-        sq = row4_sum(sq);
-        const int ncq = dkzz - qa.zk * sq;   // minus the per-query term
 
         // logits of this tile in the Log-Int-Softmax lane layout
         int lg[NC][8];
@@ -151,7 +142,10 @@ __global__ __launch_bounds__(kBlock, 3) void lis_qk_kernel(LisArgs a, QkArgs qa,
                 const i32x4v cv = *reinterpret_cast<const i32x4v*>(ck + j0);
 #pragma unroll
                 for (int t = 0; t < 4; ++t) {
-                    const int v = s[t] + ncq + cv[t];
+                    // the per-query term zp_q zp_k dk - zp_k sum_c q[i][c] is
+                    // left out: the Log-Int-Softmax of a row depends only on
+                    // the differences of its logits (u = max - v)
+                    const int v = s[t] + cv[t];
                     // only the last chunk can hold keys past Lk
                     lg[c][4 * h + t] = (c < NC - 1 || j0 + t < a.Lk) ? v : INT_MIN;
                 }

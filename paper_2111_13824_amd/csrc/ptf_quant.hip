@@ -283,6 +283,13 @@ __device__ __forceinline__ int ptf_q(float x, double s, double zp, double levels
     return (int)q;
 }
 
+// Thread (quad, row slot): channels 4 quad .. 4 quad + 3 with quad =
+// 64 blockIdx.x + lane, and kQuantRows rows spaced 4 gridDim.y apart from
+// 4 blockIdx.y + wavefront, all loaded before any is converted; a wavefront's
+// 64 quads are 1 KB of contiguous input.  The channels' alphas are read once
+// per thread.
+constexpr int kQuantRows = 4;
+
 __global__ __launch_bounds__(kBlock) void quantize_kernel(const float* x, int64_t T, int C,
                                                           const double* s_ptr,
                                                           const int32_t* zp_ptr,
@@ -294,26 +301,44 @@ __global__ __launch_bounds__(kBlock) void quantize_kernel(const float* x, int64_
     const double zp = (double)(zpc + half);
     const double levels = (double)((1 << bits) - 1);
     const int cq = (C + 3) >> 2;
-    const int64_t total = T * (int64_t)cq;
-    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < total;
-         i += (int64_t)gridDim.x * kBlock) {
-        const int64_t t = i / cq;
-        const int c0 = (int)(i - t * cq) * 4;
-        const int64_t off = t * C + c0;
-        if (vec4) {
-            const vf4 v = __builtin_nontemporal_load(reinterpret_cast<const vf4*>(x + off));
-            int q[4];
-            const float xv[4] = {v.x, v.y, v.z, v.w};
+    const int quad = blockIdx.x * 64 + (threadIdx.x & 63);
+    if (quad >= cq) return;
+    const int c0 = quad * 4;
+    int al[4];
 #pragma unroll
-            for (int b = 0; b < 4; ++b)
-                q[b] = s > 0.0 ? ptf_q(xv[b], s, zp, levels, alpha[c0 + b]) - half : zpc;
-            const uint32_t pack = ((uint32_t)q[0] & 0xFFu) | (((uint32_t)q[1] & 0xFFu) << 8) |
-                                  (((uint32_t)q[2] & 0xFFu) << 16) | ((uint32_t)q[3] << 24);
-            __builtin_nontemporal_store(pack, reinterpret_cast<uint32_t*>(y + off));
+    for (int b = 0; b < 4; ++b) al[b] = c0 + b < C ? alpha[c0 + b] : 0;
+    const int64_t step = (int64_t)gridDim.y * 4;
+    for (int64_t t0 = (int64_t)blockIdx.y * 4 + (threadIdx.x >> 6); t0 < T;
+         t0 += step * kQuantRows) {
+        if (vec4) {
+            vf4 v[kQuantRows];
+#pragma unroll
+            for (int j = 0; j < kQuantRows; ++j) {
+                const int64_t t = t0 + j * step;
+                v[j] = t < T ? __builtin_nontemporal_load(reinterpret_cast<const vf4*>(x + t * C + c0))
+                             : vf4{0.f, 0.f, 0.f, 0.f};
+            }
+#pragma unroll
+            for (int j = 0; j < kQuantRows; ++j) {
+                const int64_t t = t0 + j * step;
+                int q[4];
+                const float xv[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
+#pragma unroll
+                for (int b = 0; b < 4; ++b)
+                    q[b] = s > 0.0 ? ptf_q(xv[b], s, zp, levels, al[b]) - half : zpc;
+                const uint32_t pack = ((uint32_t)q[0] & 0xFFu) | (((uint32_t)q[1] & 0xFFu) << 8) |
+                                      (((uint32_t)q[2] & 0xFFu) << 16) | ((uint32_t)q[3] << 24);
+                if (t < T) __builtin_nontemporal_store(pack, reinterpret_cast<uint32_t*>(y + t * C + c0));
+            }
         } else {
-            for (int b = 0; b < 4 && c0 + b < C; ++b)
-                y[off + b] = (int8_t)(s > 0.0 ? ptf_q(x[off + b], s, zp, levels, alpha[c0 + b]) - half
-                                               : zpc);
+            for (int j = 0; j < kQuantRows; ++j) {
+                const int64_t t = t0 + j * step;
+                if (t >= T) break;
+                const int64_t off = t * C + c0;
+                for (int b = 0; b < 4 && c0 + b < C; ++b)
+                    y[off + b] = (int8_t)(s > 0.0 ? ptf_q(x[off + b], s, zp, levels, al[b]) - half
+                                                   : zpc);
+            }
         }
     }
 }
@@ -338,15 +363,27 @@ __global__ __launch_bounds__(kBlock) void requant_kernel(const int32_t* q, int64
     const int64_t tid = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     const int64_t stride = (int64_t)gridDim.x * kBlock;
     if (vec4) {
+        // four 16-byte loads in flight per thread before any is converted
+        constexpr int kU = 4;
         const vi4* q4 = reinterpret_cast<const vi4*>(q);
         uint32_t* y4 = reinterpret_cast<uint32_t*>(y);
-        for (int64_t i = tid; i < n / 4; i += stride) {
-            const vi4 v = __builtin_nontemporal_load(q4 + i);
-            const uint32_t p = ((uint32_t)requant_one(v.x, N2, N1, zp, hi, half) & 0xFFu) |
-                               (((uint32_t)requant_one(v.y, N2, N1, zp, hi, half) & 0xFFu) << 8) |
-                               (((uint32_t)requant_one(v.z, N2, N1, zp, hi, half) & 0xFFu) << 16) |
-                               ((uint32_t)requant_one(v.w, N2, N1, zp, hi, half) << 24);
-            __builtin_nontemporal_store(p, y4 + i);
+        const int64_t n4 = n / 4;
+        for (int64_t i0 = tid; i0 < n4; i0 += stride * kU) {
+            vi4 v[kU];
+#pragma unroll
+            for (int u = 0; u < kU; ++u) {
+                const int64_t i = i0 + u * stride;
+                v[u] = i < n4 ? __builtin_nontemporal_load(q4 + i) : vi4{0, 0, 0, 0};
+            }
+#pragma unroll
+            for (int u = 0; u < kU; ++u) {
+                const int64_t i = i0 + u * stride;
+                const uint32_t p = ((uint32_t)requant_one(v[u].x, N2, N1, zp, hi, half) & 0xFFu) |
+                                   (((uint32_t)requant_one(v[u].y, N2, N1, zp, hi, half) & 0xFFu) << 8) |
+                                   (((uint32_t)requant_one(v[u].z, N2, N1, zp, hi, half) & 0xFFu) << 16) |
+                                   ((uint32_t)requant_one(v[u].w, N2, N1, zp, hi, half) << 24);
+                if (i < n4) __builtin_nontemporal_store(p, y4 + i);
+            }
         }
         for (int64_t i = (n / 4) * 4 + tid; i < n; i += stride)
             y[i] = (int8_t)requant_one(q[i], N2, N1, zp, hi, half);
@@ -418,9 +455,11 @@ hipError_t launch_ptf_quantize(const PtfQuantArgs& a, hipStream_t stream) {
                       (reinterpret_cast<uintptr_t>(a.y) & 3) == 0)
                          ? 1
                          : 0;
-    const int64_t work = a.T * (int64_t)((a.C + 3) / 4);
-    launch_kernel(quantize_kernel, dim3(grid_for(work, kBlock * 4, 8192)), dim3(kBlock), 0, stream,
-                  a.x, a.T, a.C, a.s, a.zp, a.alpha, a.bits, vec4, a.y);
+    const unsigned gx = (unsigned)(((a.C + 3) / 4 + 63) / 64);
+    const int64_t gy =
+        std::min<int64_t>((a.T + 4 * kQuantRows - 1) / (4 * kQuantRows), std::max<int64_t>(1, 4096 / gx));
+    launch_kernel(quantize_kernel, dim3(gx, (unsigned)gy), dim3(kBlock), 0, stream, a.x, a.T, a.C,
+                  a.s, a.zp, a.alpha, a.bits, vec4, a.y);
     return hipGetLastError();
 }
 
