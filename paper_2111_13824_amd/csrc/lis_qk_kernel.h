@@ -32,7 +32,8 @@ namespace lis {
 struct QkArgs {
     const int8_t* q;    // [G, Lq, DK] int8 container
     const int8_t* k;    // [G, Lk, DK] int8 container
-    int32_t zq, zk;     // zero points, container form
+    int32_t zq;         // zero point of q, container form
+    int32_t zk;         // zero point of k: carried, not used (it cancels, see above)
 };
 
 typedef int32_t i32x4v __attribute__((ext_vector_type(4)));
