@@ -277,8 +277,9 @@ def main():
         pmc_summary(*args.pmc_summary)
         return
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
-              "the hot path shards without communication, see the design notes.", file=sys.stderr)
+        print(f"bench.py: the benchmark measures one GPU only (asked for --gpus {args.gpus}); "
+              "the hot path shards over attention units and tokens without communication, so "
+              "N GPUs run N independent copies of this workload.", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
