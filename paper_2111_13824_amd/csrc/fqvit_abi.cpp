@@ -58,18 +58,12 @@ fq_status lis_constants(float s_logit, int32_t bits, int32_t n, int32_t Lk,
     k->pre = pre;
     k->n = n;
     k->top = (1 << bits) - 1;
-    // The float form: every I-Exp intermediate is an integer below 2^24 (exact
-    // in binary32) and 2S + e + 1/2 lies below 2^52 (exact in binary64).
+    // The float path: every e = qL 2^(n - z) is exact in binary32 (qL < 2^24)
+    // and 2S + e stays below 2^52 (exact in binary64).
     const uint64_t qlmax = qb * qb + qc;
     k->fp_ok = qlmax < (1ull << 24) &&
                (unsigned __int128)(2 * (uint64_t)Lk + 1) * ((unsigned __int128)qlmax << n) <
                    ((unsigned __int128)1 << 52);
-    k->f_inv_d = (float)(1.0 / (double)d);
-    k->f_c0 = (float)(0.5 / (double)d - 0.5);
-    k->f_d = (float)d;
-    k->f_qb = (float)qb;
-    k->f_qc = (float)qc;
-    k->f_sK = 0x4B400000 + n;
     return FQ_OK;
 }
 

@@ -67,15 +67,10 @@ struct LisConsts {
     int32_t pre;        // pre-shift making (d_ln2 << pre) > 256
     int32_t n;          // clamp depth
     int32_t top;        // 2^bits - 1
-    // Exact single/double precision form of the same arithmetic, valid when
-    // q_b^2 + q_c < 2^24 and (2 Lk + 1)(q_b^2 + q_c) 2^n < 2^52 (fp_ok).
+    // The float path (e held exactly in binary32, the row sum and the code's
+    // values exactly in binary64) is valid when q_b^2 + q_c < 2^24 and
+    // (2 Lk + 1)(q_b^2 + q_c) 2^n < 2^52.
     int32_t fp_ok;
-    float f_inv_d;      // 1 / d_ln2 rounded to float
-    float f_c0;         // 0.5 / d_ln2 - 0.5 rounded to float
-    float f_d;          // d_ln2
-    float f_qb;         // q_b
-    float f_qc;         // q_c
-    int32_t f_sK;       // bit pattern of 1.5 * 2^23 plus n
 };
 
 struct LisArgs {

@@ -451,12 +451,17 @@ __device__ __forceinline__ uint32_t code_rev_f(int ebits, const RowState& st, ui
     return r + (e > st.tau ? 1u : 0u);
 }
 
-// Largest binary32 value <= floor(S2 / 3), S2 an integer below 2^53: the
-// binary64 quotient is S2 / 3 rounded to a grid of at most 1/2, so its floor
-// is floor(S2 / 3); the conversion rounds to nearest and is stepped down when
-// it lands above.
+// Largest binary32 value <= floor(S2 / 3), S2 an integer below 2^53, with no
+// division: q0 = floor(S2 RN(1/3)) is floor(S2 / 3) or one less (RN(1/3)
+// is below 1/3 by at most 2^-55, so the product falls short of S2 / 3 by at
+// most 1/4 before its rounding, itself at most 1/4 either way below 2^52),
+// and the exact remainder S2 - 3 q0 (one fma; all values integers below
+// 2^53) tells which.  The conversion to binary32 rounds to nearest and is
+// stepped down when it lands above.
 __device__ __forceinline__ float third_floor_f32(double S2) {
-    const double q = floor(S2 / 3.0);
+    double q = floor(S2 * (1.0 / 3.0));
+    const double r = fma(-3.0, q, S2);
+    q = r >= 3.0 ? q + 1.0 : q;
     const float f = (float)q;
     return (double)f > q ? __int_as_float(__float_as_int(f) - 1) : f;
 }

@@ -59,10 +59,14 @@ def _shr27(v):
 
 
 def _third_floor_f32(S2):
-    """Largest binary32 value <= floor(S2 / 3), as the kernel forms it: the
-    binary64 quotient floored, converted to nearest and stepped down when
-    above."""
-    q = np.floor(S2 / 3.0)
+    """Largest binary32 value <= floor(S2 / 3), as the kernel forms it:
+    q0 = floor(S2 RN(1/3)), plus one when the exact remainder S2 - 3 q0 is 3
+    or more; then converted to nearest and stepped down when above."""
+    q0 = np.floor(S2 * (1.0 / 3.0))
+    r = np.array([int(a) - 3 * int(b) for a, b in zip(S2, q0)], dtype=object)
+    q = np.where(r >= 3, q0 + 1.0, q0)
+    exact = np.array([int(a) // 3 for a in S2], dtype=object)
+    assert np.all(np.array([int(v) for v in q], dtype=object) == exact)
     f = q.astype(np.float32)
     down = (f.astype(np.float64) > q)
     f = np.where(down, (f.view(np.int32) - 1).view(np.float32), f)
