@@ -101,7 +101,10 @@ fq_status ptf_layernorm_int8(const int8_t* x_q, int64_t T, int32_t C, int32_t zp
  *   logits  [G, Lq, Lk] int32 attention logits with scale s_logit
  *           (G = attention units, e.g. batch x windows x heads).
  *   bias    NULL or [Hb, Lq, Lk] int32 added to the logits of unit g from
- *           head g % Hb before the row maximum (Swin relative-position bias).
+ *           plane g % Hb before the row maximum (Swin relative-position bias:
+ *           Hb = heads; with units ordered (image, window, head), a shifted-
+ *           window mask is folded in by passing the sum of mask and bias as
+ *           [windows, heads, Lq, Lk] with Hb = windows x heads).
  *   s_logit in [1e-4, 0.5].
  *   bits    code width b in [1, 8]; codes are Attn_Q in [0, 2^b - 1] and the
  *           LIS output of the paper is N - Attn_Q with N = 2^b - 1, scale 2^-N.
