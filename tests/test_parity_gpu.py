@@ -338,6 +338,22 @@ def test_prepared_calls_match_direct(fq, orc):
     assert np.array_equal(host(y), _ln_ref(orc, d))
 
 
+def test_swin_shifted_window_mask_in_bias(fq, orc):
+    """A shifted-window mask folds into the bias planes: with units ordered
+    (image, window, head), the bias is mask[window] + relative-position
+    bias[head], passed as [windows x heads, Lq, Lk]."""
+    say("swin shifted-window mask as bias")
+    H, nW, B = 3, 4, 2
+    a = W.attn_inputs(B * nW * H, 49, 49, 32, seed=21, heads=H, bias=True)
+    mask = W.shifted_window_mask(14, 7, 3, -int(100 / S))
+    comb = (mask[:, None, :, :] + a["bias"][None, :, :, :]).reshape(nW * H, 49, 49)
+    comb = np.ascontiguousarray(comb.astype(np.int32))
+    out = fq.lis_attention_head(dev(a["logits"]), dev(a["v"]), S, bias=dev(comb))
+    assert np.array_equal(host(out), orc.lis_attention_head(a["logits"], a["v"], S, bias=comb))
+    codes = fq.lis_softmax_log4(dev(a["logits"]), S, bias=dev(comb))
+    assert np.array_equal(host(codes), orc.lis_softmax_log4(a["logits"], S, bias=comb))
+
+
 def test_head_codes_out_and_unfused_equal(fq, orc):
     """The fused head writes the same codes as lis_softmax_log4, and its output
     equals lis_attn_v_shift of those codes (MFMA product vs VALU shifts)."""

@@ -176,6 +176,22 @@ def attn_inputs(G: int, Lq: int, Lk: int, d: int, seed: int, heads: int = 1,
                 s_logit=s_logit, bits=LIS_BITS, exp_n=EXP_N)
 
 
+def shifted_window_mask(hw: int, window: int, shift: int, masked: int) -> np.ndarray:
+    """Additive mask [nW, window^2, window^2] int32 of shifted-window attention
+    on an hw x hw token grid: after a cyclic shift by `shift`, the grid is cut
+    into nW = (hw / window)^2 windows; tokens that came from different regions
+    of the unshifted grid (three bands per axis: [0, hw - window),
+    [hw - window, hw - shift), [hw - shift, hw)) get `masked`, others 0."""
+    assert hw % window == 0 and 0 < shift < window
+    bands = np.zeros(hw, dtype=np.int64)
+    bands[hw - window:hw - shift] = 1
+    bands[hw - shift:] = 2
+    region = bands[:, None] * 3 + bands[None, :]          # [hw, hw]
+    n = hw // window
+    wins = region.reshape(n, window, n, window).transpose(0, 2, 1, 3).reshape(n * n, window * window)
+    return np.where(wins[:, :, None] != wins[:, None, :], masked, 0).astype(np.int32)
+
+
 def qk_inputs(G: int, Lq: int, Lk: int, dk: int, d: int, seed: int, sigma: float = 30.0,
               zp_q: int = 0, zp_k: int = 0, heads: int = 1, bias: bool = False) -> dict:
     """int8 query and key activations [G, Lq|Lk, dk] (rounded Gaussians of
