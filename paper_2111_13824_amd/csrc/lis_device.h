@@ -29,8 +29,9 @@
 //     code = min(m, N) - [2S < 3e],   m = floor(log2((2S + e) / (1.5 e))),
 // (m >= 1 always, since 2S >= 2e, and 2S < 3e forces m = 1).  Two exact
 // evaluations of this formula are implemented:
-//   * float path: I-Exp in binary32 (every intermediate is an integer below
-//     2^24) and the code from binary64 values (2S + e below 2^52), m being the
+//   * float path: I-Exp by the 24-bit integer steps, e = qL 2^(n - z) held as
+//     a binary32 value (qL < 2^24), the row sum in binary64, and the code
+//     from binary64 values (2S + e below 2^52), m being the
 //     difference of the IEEE bit patterns of 2S + e and 1.5 e shifted right
 //     by 52 (both positive, so the pattern difference is the exponent
 //     difference minus a borrow exactly when the significand of the quotient
@@ -759,9 +760,9 @@ __device__ __forceinline__ void tile_load(int (&lg)[NC][8], const RowPtrs& rp, i
 // the I-Exp pass of the current tile, and chunk PF + c right after chunk c of
 // the current tile has gone through its MFMA (its registers are free by then),
 // so the next tile is in flight without holding two tiles in registers.
-// Measured on the ViT-B/16 shapes, PF = 0, 4 and 7 run equally fast and
-// requesting the next tile before the I-Exp pass is slower; PF = 0 needs the
-// fewest registers.
+// Measured on the ViT-B/16 shapes with the current arithmetic: PF = 0 is the
+// fastest; PF = 7 (168 VGPRs and a few spilled) and requesting the whole next
+// tile before the I-Exp pass are about 15 % slower.
 constexpr int unit_prefetch(int NC) { return NC < 0 ? NC : 0; }
 
 template <int NC, bool HALF>
