@@ -42,12 +42,39 @@ LIS_SOURCES = ["lis_device.h", "lis_attention.hip", "lis_inst_lo.hip", "lis_inst
                "fqvit_internal.h"]
 
 
+def _code_only(text):
+    """C/C++ source without comments and with whitespace runs collapsed, so
+    that editing a comment does not change the hash of the code."""
+    out, i, n = [], 0, len(text)
+    while i < n:
+        c = text[i]
+        if c in "\"'":                                   # string or char literal
+            j = i + 1
+            while j < n and text[j] != c:
+                j += 2 if text[j] == "\\" else 1
+            out.append(text[i:j + 1])
+            i = j + 1
+        elif text.startswith("//", i):
+            j = text.find("\n", i)
+            i = n if j < 0 else j
+        elif text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        else:
+            out.append(c)
+            i += 1
+    return " ".join("".join(out).split())
+
+
 def lis_sources_sha256():
+    """Hash of the code (comments excluded) of the fused head's sources: the
+    recorded HBM traffic is used only while it still describes this code."""
     import hashlib
     h = hashlib.sha256()
     for name in LIS_SOURCES:
-        with open(os.path.join(ROOT, "paper_2111_13824_amd", "csrc", name), "rb") as f:
-            h.update(name.encode() + b"\0" + f.read())
+        with open(os.path.join(ROOT, "paper_2111_13824_amd", "csrc", name), encoding="utf-8") as f:
+            h.update(name.encode() + b"\0" + _code_only(f.read()).encode())
     return h.hexdigest()
 
 
