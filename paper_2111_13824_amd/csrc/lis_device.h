@@ -761,8 +761,9 @@ __device__ __forceinline__ void tile_load(int (&lg)[NC][8], const RowPtrs& rp, i
 // the current tile has gone through its MFMA (its registers are free by then),
 // so the next tile is in flight without holding two tiles in registers.
 // Measured on the ViT-B/16 shapes with the current arithmetic: PF = 0 is the
-// fastest; PF = 7 (168 VGPRs and a few spilled) and requesting the whole next
-// tile before the I-Exp pass are about 15 % slower.
+// fastest; PF = 1 to 3 (150 to 164 VGPRs) are 1 to 2 % slower, and PF = 7 (168
+// VGPRs and a few spilled) and requesting the whole next tile before the I-Exp
+// pass about 15 % slower.
 constexpr int unit_prefetch(int NC) { return NC < 0 ? NC : 0; }
 
 template <int NC, bool HALF>
