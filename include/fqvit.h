@@ -55,7 +55,7 @@ int32_t fq_version(void);
  * then records that kernel's start and `stop` its end (hipExtLaunchKernel
  * semantics), so hipEventElapsedTime gives the kernel's own duration with no
  * extra packets on the stream.  Every other entry point launches one kernel.
- * ptf_calibrate, which launches five kernels, records `start` on the first and
+ * ptf_calibrate, which launches four kernels, records `start` on the first and
  * `stop` on the last, so the interval covers the whole calibration.
  * The events are consumed by that next call whatever it returns; a call that
  * enqueues nothing (empty tensors, failed validation) leaves them unrecorded.

@@ -2,7 +2,7 @@
 // requantization of an int32 accumulator (the integer form of Supplement A.1)
 // for gfx950.
 //
-// Calibration runs five kernels:
+// Calibration runs four kernels:
 //   1. minmax_partial  per-workgroup minimum and maximum of x;
 //   2. calib_params    the layer-wise scale s = (max - min) / (2^b - 1) / 2^K
 //                      and zero point zp = clip(rint(-min / (2^K s)), 0, 2^b - 1)
@@ -10,8 +10,9 @@
 //   3. alpha_partial   for every channel c and block of 64 consecutive rows
 //                      the squared errors of the K + 1 candidate grids summed
 //                      in row order (eq. 11 with its zero point and clip);
-//   4. alpha_sum       per channel and alpha, the block sums added in block order;
-//   5. alpha_argmin    per channel, the argmin over alpha (the smallest on ties).
+//   4. alpha_select    per channel and alpha, the block sums added in block
+//                      order, then per channel the argmin over alpha (the
+//                      smallest on ties).
 // Steps 3 and 4 reproduce the blocked summation order exactly, so the argmin
 // is a pure function of x.  x / (2^alpha s) is computed as ldexp(x / s,
 // -alpha): scaling by a power of two commutes with the rounding of the
@@ -214,65 +215,63 @@ __global__ __launch_bounds__(kBlock) void alpha_partial_kernel(const float* x, i
     }
 }
 
-// Workgroup (cx, a): channels cx*64 .. cx*64 + 63, candidate alpha = a.  The
-// block sums are staged in LDS, up to kSumChunk blocks at a time (loaded by
-// the whole workgroup), and each channel's lane of wavefront 0 adds them in
-// block order: err[a C + c] = ((0 + part_0) + part_1) + ...
-constexpr int kSumChunk = 128;   // 64 KB of LDS per pass
+// Error sums and the argmin of eq. 11 in one launch.  Workgroup g owns the
+// channels g*cb .. g*cb + cb - 1 with cb = kSelChains / (K + 1), i.e. cb (K + 1)
+// chains (channel, alpha).  The block sums of each chain are staged in LDS, up
+// to kSelRows blocks per pass (loaded by the whole workgroup), and the chain's
+// lane of wavefront 0 adds them in block order:
+//     err(c, a) = ((0 + part_0) + part_1) + ...
+// Then one lane per channel takes the argmin over alpha, ties to the smallest.
+constexpr int kSelChains = 16;
+constexpr int kSelRows = 256;    // 32 KB of LDS per pass
+constexpr int kSelPerThread = kSelRows * kSelChains / kBlock;
 
-__global__ __launch_bounds__(kBlock) void alpha_sum_kernel(const double* part, int C, int64_t nb,
-                                                           const double* s_ptr, double* err) {
-    extern __shared__ double tile[];   // [kSumChunk][64]
-    const int c0 = blockIdx.x * 64;
-    const int a = blockIdx.y;
-    const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
-    if (!(*s_ptr > 0.0)) return;
-    const double* p = part + (int64_t)a * nb * C + c0;
-    double acc = 0.0;
-    constexpr int kPerThread = kSumChunk / (kBlock / 64);
-    for (int64_t k0 = 0; k0 < nb; k0 += kSumChunk) {
-        const int nk = (int)min<int64_t>(kSumChunk, nb - k0);
-        // all of this thread's loads first, then the LDS stores
-        double v[kPerThread];
-#pragma unroll
-        for (int i = 0; i < kPerThread; ++i) {
-            const int r = wave + i * (kBlock / 64);
-            v[i] = (r < nk && c0 + lane < C) ? p[(k0 + r) * C + lane] : 0.0;
-        }
-#pragma unroll
-        for (int i = 0; i < kPerThread; ++i) {
-            const int r = wave + i * (kBlock / 64);
-            if (r < nk) tile[r * 64 + lane] = v[i];
-        }
-        __syncthreads();
-        if (wave == 0)
-            for (int r = 0; r < nk; ++r) acc = acc + tile[r * 64 + lane];
-        __syncthreads();
-    }
-    if (wave == 0 && c0 + lane < C) err[(int64_t)a * C + c0 + lane] = acc;
-}
-
-// One thread per channel: argmin over alpha with ties to the smallest.
-__global__ __launch_bounds__(kBlock) void alpha_argmin_kernel(const double* err, int C, int K,
-                                                              const double* s_ptr,
+__global__ __launch_bounds__(kBlock) void alpha_select_kernel(const double* part, int C, int K,
+                                                              int64_t nb, const double* s_ptr,
                                                               uint8_t* alpha) {
-    const int c = blockIdx.x * kBlock + threadIdx.x;
-    if (c >= C) return;
+    __shared__ double tile[kSelRows * kSelChains];
+    __shared__ double err[kSelChains];
+    const int cb = kSelChains / (K + 1);
+    const int nch = cb * (K + 1);
+    const int c0 = blockIdx.x * cb;
+    const int t = threadIdx.x;
     if (!(*s_ptr > 0.0)) {
-        alpha[c] = 0;
+        if (t < cb && c0 + t < C) alpha[c0 + t] = 0;
         return;
     }
-    int best = 0;
-    double best_err = INFINITY;
-    for (int a = 0; a <= K; ++a) {
-        const double e = err[(int64_t)a * C + c];
-        if (e < best_err) {
-            best_err = e;
-            best = a;
+    double acc = 0.0;
+    for (int64_t k0 = 0; k0 < nb; k0 += kSelRows) {
+        const int nk = (int)min<int64_t>(kSelRows, nb - k0);
+        // all of this thread's loads first, then the LDS stores
+        double v[kSelPerThread];
+#pragma unroll
+        for (int i = 0; i < kSelPerThread; ++i) {
+            const int idx = t + i * kBlock;
+            const int row = idx / kSelChains, ch = idx - row * kSelChains;
+            const int a = ch / cb, c = c0 + ch - a * cb;
+            v[i] = (row < nk && ch < nch && c < C) ? part[((int64_t)a * nb + k0 + row) * C + c] : 0.0;
         }
+        __syncthreads();   // the previous pass's sums have read the tile
+#pragma unroll
+        for (int i = 0; i < kSelPerThread; ++i) tile[t + i * kBlock] = v[i];
+        __syncthreads();
+        if (t < nch)
+            for (int r = 0; r < nk; ++r) acc = acc + tile[r * kSelChains + t];
     }
-    alpha[c] = (uint8_t)best;
+    if (t < nch) err[t] = acc;
+    __syncthreads();
+    if (t < cb && c0 + t < C) {
+        int best = 0;
+        double best_err = INFINITY;
+        for (int a = 0; a <= K; ++a) {
+            const double e = err[a * cb + t];
+            if (e < best_err) {
+                best_err = e;
+                best = a;
+            }
+        }
+        alpha[c0 + t] = (uint8_t)best;
+    }
 }
 
 // X_Q = clip(rint(x / (2^alpha_c s)) + zp, 0, 2^b - 1) (eq. 8), stored in the
@@ -439,13 +438,10 @@ hipError_t launch_ptf_calibrate(const PtfCalibArgs& a, hipStream_t stream) {
         case 6: launch_alpha_partial<6>(a, g3, nb, part, stream); break;
         default: launch_alpha_partial<7>(a, g3, nb, part, stream); break;
     }
-    double* err = part + (int64_t)(a.K + 1) * nb * a.C;
-    launch_kernel(alpha_sum_kernel, dim3((unsigned)((a.C + 63) / 64), (unsigned)(a.K + 1)),
-                  dim3(kBlock), (size_t)kSumChunk * 64 * sizeof(double), stream,
-                  (const double*)part, a.C, nb, (const double*)a.s, err);
+    const int cb = kSelChains / (a.K + 1);
     set_launch_events(nullptr, ev.stop);
-    launch_kernel(alpha_argmin_kernel, dim3((unsigned)((a.C + kBlock - 1) / kBlock)), dim3(kBlock), 0,
-                  stream, (const double*)err, a.C, a.K, (const double*)a.s, a.alpha);
+    launch_kernel(alpha_select_kernel, dim3((unsigned)((a.C + cb - 1) / cb)), dim3(kBlock), 0, stream,
+                  (const double*)part, a.C, a.K, nb, (const double*)a.s, a.alpha);
     set_launch_events(nullptr, nullptr);
     return hipGetLastError();
 }

@@ -49,8 +49,9 @@ def _calib_check(fq, orc, x, bits, K):
     return s, zp, alpha, s_ref, zp_ref, alpha_ref
 
 
+# (20000, 40): 313 row blocks, more than one LDS pass of the per-channel sums
 CAL_SHAPES = [(1, 5, 0), (65, 13, 0), (197, 192, 0), (150, 96, 4), (1576, 384, 0),
-              (4099, 768, 8), (130, 1000, 2)]
+              (4099, 768, 8), (130, 1000, 2), (20000, 40, 1)]
 
 
 @pytest.mark.parametrize("T,C,outliers", CAL_SHAPES)
