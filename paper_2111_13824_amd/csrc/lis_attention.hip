@@ -231,9 +231,9 @@ hipError_t launch_lis(const LisArgs& a, hipStream_t stream) {
         const bool half = a.Lk - 32 * (nc - 1) <= 16;
         return launch_lis_unit(nc, fused, dt, half, a, u, (size_t)u.vt_bytes + out_lds, stream);
     }
-    // Tile kernels for rows of up to 640 keys: codes only, or the fused product
-    // without a codes output and with d <= 64.
-    const bool regs = nc <= 20 && (!fused || (a.codes == nullptr && dt <= 4));
+    // Tile kernels: codes only for rows of up to 640 keys, the fused product
+    // (without a codes output, d <= 64) for rows of up to 384 keys.
+    const bool regs = fused ? (nc <= kRegsFusedMaxNC && a.codes == nullptr && dt <= 4) : nc <= 20;
     if (regs) {
         const size_t lds = (size_t)p.vt_bytes + out_lds;
         return nc <= 10 ? launch_lis_regs_lo(nc, fused, dt, fp, a, p, grid, lds, stream)

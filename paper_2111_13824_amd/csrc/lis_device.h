@@ -954,6 +954,13 @@ __global__ __launch_bounds__(kBlock, lis_waves_per_simd(NC)) void lis_kernel(Lis
 
 // Launch of the tile kernel for exactly NC chunks; the host has checked that
 // dtm is 2 or 4 for fused calls (d <= 64).  MULTI follows from NC and dtm.
+// Longest rows (in 32-key chunks) of the fused tile kernels.  Beyond 12 chunks
+// a wavefront holds its rows in registers at one wavefront per SIMD, and the
+// stream kernel is faster (d = 64, G = 64 square units, on one MI355X: 400
+// keys 63 against 68 us, 577 keys 114 against 158 us, 640 keys 256 against
+// 322 us for 128 units; at 300 and 330 keys the tile kernels stay faster).
+constexpr int kRegsFusedMaxNC = 12;
+
 template <int NC>
 hipError_t launch_lis_nc(bool fused, int dtm, bool fp, const LisArgs& a, const LisLaunch& p,
                          dim3 grid, size_t lds, hipStream_t s) {
@@ -964,6 +971,8 @@ hipError_t launch_lis_nc(bool fused, int dtm, bool fp, const LisArgs& a, const L
     if (!fused) {
         if (fp) FQ_LIS(false, false, 1, true);
         else FQ_LIS(false, false, 1, false);
+    } else if constexpr (NC > kRegsFusedMaxNC) {
+        return hipErrorInvalidValue;    // longer fused rows take the stream kernel
     } else if (dtm == 2) {
         if (fp) FQ_LIS(true, kMulti2, 2, true);
         else FQ_LIS(true, kMulti2, 2, false);
