@@ -6,10 +6,11 @@
 namespace fqvit {
 namespace lis {
 
-// Rows longer than 640 keys, head dimensions above 64 and fused calls that also
-// write the codes: the same arithmetic with the logits re-read in each pass
-// instead of held in registers.
-template <bool FUSED>
+// Long rows, head dimensions above 64 and fused calls that also write the
+// codes: the same arithmetic with the logits re-read in each pass instead of
+// held in registers.  DTMAX = dpad / 16 output column tiles (1 without the
+// product), a template constant so that the accumulators stay in registers.
+template <bool FUSED, int DTMAX>
 __global__ __launch_bounds__(kBlock) void lis_kernel_stream(LisArgs a, LisLaunch p) {
     extern __shared__ uint16_t vt[];
     const int64_t total = a.G * (int64_t)p.ntiles;
@@ -61,8 +62,6 @@ __global__ __launch_bounds__(kBlock) void lis_kernel_stream(LisArgs a, LisLaunch
 
     const bool row_ok = (i0 + r) < a.Lq;
     uint8_t* crow = a.codes ? a.codes + (g * a.Lq + i) * (int64_t)a.ld_codes : nullptr;
-    constexpr int DTMAX = 16;
-    const int DT = p.dpad >> 4;
     f32x4 acc[DTMAX];
 #pragma unroll
     for (int dt = 0; dt < DTMAX; ++dt) acc[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -98,7 +97,8 @@ __global__ __launch_bounds__(kBlock) void lis_kernel_stream(LisArgs a, LisLaunch
             av.w = pbits[6] | (pbits[7] << 16);
             const bf16x8 A = __builtin_bit_cast(bf16x8, av);
             const int cs = c - stage * cps;
-            for (int dt = 0; dt < DT; ++dt) {
+#pragma unroll
+            for (int dt = 0; dt < DTMAX; ++dt) {
                 const u32x4 bv = *reinterpret_cast<const u32x4*>(
                     vt + (16 * dt + r) * p.ld + 32 * cs + 8 * kg);
                 acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, __builtin_bit_cast(bf16x8, bv),
@@ -108,7 +108,8 @@ __global__ __launch_bounds__(kBlock) void lis_kernel_stream(LisArgs a, LisLaunch
     }
 
     if (FUSED && active) {
-        for (int dt = 0; dt < DT; ++dt) {
+#pragma unroll
+        for (int dt = 0; dt < DTMAX; ++dt) {
             const int col = 16 * dt + r;
             if (col >= a.d) continue;
 #pragma unroll
@@ -232,7 +233,7 @@ hipError_t launch_lis(const LisArgs& a, hipStream_t stream) {
         return launch_lis_unit(nc, fused, dt, half, a, u, (size_t)u.vt_bytes + out_lds, stream);
     }
     // Tile kernels: codes only for rows of up to 640 keys, the fused product
-    // (without a codes output, d <= 64) for rows of up to 384 keys.
+    // (without a codes output, d <= 64) for rows of up to 288 keys.
     const bool regs = fused ? (nc <= kRegsFusedMaxNC && a.codes == nullptr && dt <= 4) : nc <= 20;
     if (regs) {
         const size_t lds = (size_t)p.vt_bytes + out_lds;
@@ -240,10 +241,16 @@ hipError_t launch_lis(const LisArgs& a, hipStream_t stream) {
                         : launch_lis_regs_hi(nc, fused, dt, fp, a, p, grid, lds, stream);
     }
     const size_t lds = fused ? (size_t)p.vt_bytes : 0;
-    if (fused)
-        launch_kernel(lis_kernel_stream<true>, grid, dim3(kBlock), lds, stream, a, p);
+    if (!fused)
+        launch_kernel(lis_kernel_stream<false, 1>, grid, dim3(kBlock), 0, stream, a, p);
+    else if (dt == 2)
+        launch_kernel(lis_kernel_stream<true, 2>, grid, dim3(kBlock), lds, stream, a, p);
+    else if (dt == 4)
+        launch_kernel(lis_kernel_stream<true, 4>, grid, dim3(kBlock), lds, stream, a, p);
+    else if (dt == 8)
+        launch_kernel(lis_kernel_stream<true, 8>, grid, dim3(kBlock), lds, stream, a, p);
     else
-        launch_kernel(lis_kernel_stream<false>, grid, dim3(kBlock), 0, stream, a, p);
+        launch_kernel(lis_kernel_stream<true, 16>, grid, dim3(kBlock), lds, stream, a, p);
     return hipGetLastError();
 }
 

@@ -954,12 +954,12 @@ __global__ __launch_bounds__(kBlock, lis_waves_per_simd(NC)) void lis_kernel(Lis
 
 // Launch of the tile kernel for exactly NC chunks; the host has checked that
 // dtm is 2 or 4 for fused calls (d <= 64).  MULTI follows from NC and dtm.
-// Longest rows (in 32-key chunks) of the fused tile kernels.  Beyond 12 chunks
-// a wavefront holds its rows in registers at one wavefront per SIMD, and the
-// stream kernel is faster (d = 64, G = 64 square units, on one MI355X: 400
-// keys 63 against 68 us, 577 keys 114 against 158 us, 640 keys 256 against
-// 322 us for 128 units; at 300 and 330 keys the tile kernels stay faster).
-constexpr int kRegsFusedMaxNC = 12;
+// Longest rows (in 32-key chunks) of the fused tile kernels.  Beyond 9 chunks
+// the stream kernel, which re-reads the logits instead of holding them, is
+// faster (d = 64, 64 square units, on one MI355X: 300 keys 30 against 36 us,
+// 384 keys 41 against 61 us); up to 9 chunks the tile kernels are (288 keys
+// 15 against 29 us, 240 keys 10 against 19 us).
+constexpr int kRegsFusedMaxNC = 9;
 
 template <int NC>
 hipError_t launch_lis_nc(bool fused, int dtm, bool fp, const LisArgs& a, const LisLaunch& p,

@@ -268,13 +268,13 @@ def test_attn_v_shift_any_codes(fq, orc):
         assert np.array_equal(got, orc.lis_attn_v_shift(codes, v, zp_v=-3, bits=bits, Lk=65))
 
 
-# (2, 40, 350, 64) and (2, 33, 384, 32): the longest rows of the fused tile
-# kernels (11 and 12 chunks of 32 keys); (2, 40, 400, 64): the first that
-# takes the stream kernel
+# (2, 40, 288, 64) and (2, 33, 270, 32): the longest rows of the fused tile
+# kernels (9 chunks of 32 keys); (2, 40, 290, 64): the shortest that takes the
+# stream kernel, with (2, 40, 350, 64), (2, 33, 384, 32) and (2, 40, 400, 64)
 HEAD_SHAPES = [(3, 5, 1, 64), (2, 17, 33, 16), (3, 64, 197, 64), (2, 70, 197, 64), (1, 65, 577, 64),
                (12, 49, 49, 32), (2, 3, 640, 64), (1, 3, 700, 64), (1, 2, 4096, 32), (2, 20, 96, 100),
-               (2, 33, 65, 256), (2, 19, 129, 1), (2, 40, 350, 64), (2, 33, 384, 32),
-               (2, 40, 400, 64)]
+               (2, 33, 65, 256), (2, 19, 129, 1), (2, 40, 288, 64), (2, 33, 270, 32),
+               (2, 40, 290, 64), (2, 40, 350, 64), (2, 33, 384, 32), (2, 40, 400, 64)]
 
 
 @pytest.mark.parametrize("G,Lq,Lk,d", HEAD_SHAPES)
