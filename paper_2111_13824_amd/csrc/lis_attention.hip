@@ -10,7 +10,9 @@ namespace lis {
 // codes: the same arithmetic with the logits re-read in each pass instead of
 // held in registers.  DTMAX = dpad / 16 output column tiles (1 without the
 // product), a template constant so that the accumulators stay in registers.
-template <bool FUSED, int DTMAX>
+// FP: the float path of the unit kernel (binary32 e, binary64 row sum and the
+// funnel-shift code), for scales where it is exact; else the integer path.
+template <bool FUSED, int DTMAX, bool FP>
 __global__ __launch_bounds__(kBlock) void lis_kernel_stream(LisArgs a, LisLaunch p) {
     extern __shared__ uint16_t vt[];
     const int64_t total = a.G * (int64_t)p.ntiles;
@@ -47,18 +49,39 @@ __global__ __launch_bounds__(kBlock) void lis_kernel_stream(LisArgs a, LisLaunch
     }
     mx = row4_max(mx);
 
-    uint64_t sum = 0;
-    for (int c = 0; c < nc; ++c) {
-        int lg[8];
-        load_chunk<false>(lg, row, brow, c, kg, Lk, tail_vec);
+    RowState st;
+    if constexpr (FP) {
+        // two partial sums of integers below 2^53: exact in any order
+        double part[2] = {0.0, 0.0};
+        for (int c = 0; c < nc; ++c) {
+            int lg[8];
+            load_chunk<false>(lg, row, brow, c, kg, Lk, tail_vec);
 #pragma unroll
-        for (int t = 0; t < 8; ++t) {
-            uint32_t z;
-            const uint32_t qL = iexp_qL(lg[t], mx, k, z);
-            sum += lg[t] != INT_MIN ? ((uint64_t)qL << (k.n - (int)z)) : 0ull;
+            for (int t = 0; t < 8; ++t) {
+                const float e = iexp_f(lg[t], mx, k);
+                part[t & 1] += lg[t] != INT_MIN ? (double)e : 0.0;
+            }
         }
+        const double S2 = 2.0 * row4_sum(part[0] + part[1]);
+        st.S2s = S2 * kCodeScale;
+        st.sc = kCodeScale;
+        asm volatile("" : "+s"(st.sc));
+        st.tau = third_floor_f32(S2);
+    } else {
+        uint64_t sum = 0;
+        for (int c = 0; c < nc; ++c) {
+            int lg[8];
+            load_chunk<false>(lg, row, brow, c, kg, Lk, tail_vec);
+#pragma unroll
+            for (int t = 0; t < 8; ++t) {
+                uint32_t z;
+                const uint32_t qL = iexp_qL(lg[t], mx, k, z);
+                sum += lg[t] != INT_MIN ? ((uint64_t)qL << (k.n - (int)z)) : 0ull;
+            }
+        }
+        st.rs = row_sum(sum, k);
     }
-    const RowSum rs = row_sum(sum, k);
+    const uint32_t kr = ((uint32_t)(k.top + 1) << 25) - 1u;
 
     const bool row_ok = (i0 + r) < a.Lq;
     uint8_t* crow = a.codes ? a.codes + (g * a.Lq + i) * (int64_t)a.ld_codes : nullptr;
@@ -82,11 +105,18 @@ __global__ __launch_bounds__(kBlock) void lis_kernel_stream(LisArgs a, LisLaunch
 #pragma unroll
         for (int t = 0; t < 8; ++t) {
             const bool valid = lg[t] != INT_MIN;
-            uint32_t z;
-            const uint32_t qL = iexp_qL(valid ? lg[t] : mx, mx, k, z);
-            const int cd = lis_code(qL, z, rs, k);
-            code[t] = valid ? cd : 0;
-            pbits[t] = valid ? (uint32_t)(ptop - (cd << 7)) : 0u;
+            if constexpr (FP) {
+                const int eb = __float_as_int(iexp_f(valid ? lg[t] : mx, mx, k));
+                code[t] = 0;
+                if (!FUSED || crow) code[t] = valid ? code_f(eb, st, k.top) : 0;
+                pbits[t] = (FUSED && valid) ? (127u + code_rev_f(eb, st, kr)) << 7 : 0u;
+            } else {
+                uint32_t z;
+                const uint32_t qL = iexp_qL(valid ? lg[t] : mx, mx, k, z);
+                const int cd = lis_code(qL, z, st.rs, k);
+                code[t] = valid ? cd : 0;
+                pbits[t] = valid ? (uint32_t)(ptop - (cd << 7)) : 0u;
+            }
         }
         if (crow && row_ok) store_codes_row(crow, Lk, k.top, c, kg, code);
         if (FUSED) {
@@ -194,6 +224,26 @@ __global__ __launch_bounds__(kBlock) void attn_v_shift_kernel(AvArgs a, int tpr,
 
 }  // namespace lis
 
+namespace {
+
+template <bool FP>
+void launch_stream(bool fused, int dt, dim3 grid, size_t lds, hipStream_t stream,
+                   const LisArgs& a, const lis::LisLaunch& p) {
+    using namespace lis;
+    if (!fused)
+        launch_kernel(lis_kernel_stream<false, 1, FP>, grid, dim3(kBlock), 0, stream, a, p);
+    else if (dt == 2)
+        launch_kernel(lis_kernel_stream<true, 2, FP>, grid, dim3(kBlock), lds, stream, a, p);
+    else if (dt == 4)
+        launch_kernel(lis_kernel_stream<true, 4, FP>, grid, dim3(kBlock), lds, stream, a, p);
+    else if (dt == 8)
+        launch_kernel(lis_kernel_stream<true, 8, FP>, grid, dim3(kBlock), lds, stream, a, p);
+    else
+        launch_kernel(lis_kernel_stream<true, 16, FP>, grid, dim3(kBlock), lds, stream, a, p);
+}
+
+}  // namespace
+
 hipError_t launch_lis(const LisArgs& a, hipStream_t stream) {
     using namespace lis;
     const bool fused = a.out != nullptr;
@@ -241,16 +291,10 @@ hipError_t launch_lis(const LisArgs& a, hipStream_t stream) {
                         : launch_lis_regs_hi(nc, fused, dt, fp, a, p, grid, lds, stream);
     }
     const size_t lds = fused ? (size_t)p.vt_bytes : 0;
-    if (!fused)
-        launch_kernel(lis_kernel_stream<false, 1>, grid, dim3(kBlock), 0, stream, a, p);
-    else if (dt == 2)
-        launch_kernel(lis_kernel_stream<true, 2>, grid, dim3(kBlock), lds, stream, a, p);
-    else if (dt == 4)
-        launch_kernel(lis_kernel_stream<true, 4>, grid, dim3(kBlock), lds, stream, a, p);
-    else if (dt == 8)
-        launch_kernel(lis_kernel_stream<true, 8>, grid, dim3(kBlock), lds, stream, a, p);
+    if (fp)
+        launch_stream<true>(fused, dt, grid, lds, stream, a, p);
     else
-        launch_kernel(lis_kernel_stream<true, 16>, grid, dim3(kBlock), lds, stream, a, p);
+        launch_stream<false>(fused, dt, grid, lds, stream, a, p);
     return hipGetLastError();
 }
 
