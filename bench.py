@@ -9,16 +9,17 @@ Inputs are synthetic (seeded generators of ``workloads``) and resident in HBM
 before timing.  Four independent copies of every tensor (4 x 187 MB) rotate
 from step to step so that the 256 MB Infinity Cache cannot hold the working
 set.  Warm-up steps are untimed; the K timed steps are bracketed by device
-synchronisation and two events on the launch stream.  Inside the timed
-region the kernels of every EVENT_EVERY-th step carry a pair of HIP events
-attached to their own launch (fq_time_next_call), which record the kernel's
-start and end, so the per-kernel averages are kernel durations.  Sampling keeps
-the events' own cost (a few microseconds per attached launch) out of the step
-time.
+synchronisation and two events on the launch stream, with nothing else on the
+stream.  After the timed region, max(EVENT_SAMPLES, K) further steps run with
+a pair of HIP events attached to each kernel's own launch (fq_time_next_call),
+which record that kernel's start and end: the per-kernel averages are kernel
+durations, measured outside the timed region so that the events' own cost (a
+few microseconds per attached launch) stays out of the step time.
 
 Prints one JSON line with the throughput in tokens/s, the roofline of the
 dominant kernel (lis_attention_head) against the 8 TB/s HBM peak, and the
-CPU oracle timed on two complete steps of the same workload on the host.
+CPU oracle timed on complete steps of the same workload on the host (one
+thread and all usable CPUs).
 """
 import argparse
 import json
@@ -33,15 +34,14 @@ HBM_PEAK_GBS = 8000.0
 METRIC = "tokens/s and achieved HBM GB/s for PTF-LayerNorm + LIS attention, ViT-B bs64"
 TRAFFIC_WORKLOAD = "vit_base16_224_b64"
 N_SETS = 4
-EVENT_EVERY = 8
+EVENT_SAMPLES = 64
 COPY_BYTES = 512 * 2 ** 20
 COPY_REPS = 3
 # Summary of the counter runs of the fused head; its traffic figure is used only
 # while the hash of the LIS sources matches the one recorded with it.
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "lis_attention_head_vit_base16_224_b64_traffic.txt")
 LIS_SOURCES = ["lis_device.h", "lis_attention.hip", "lis_inst_lo.hip", "lis_inst_hi.hip",
-               "lis_inst_unit.hip",
-               "fqvit_internal.h"]
+               "lis_inst_unit.hip", "fqvit_internal.h", "fqvit_launch.h"]
 
 
 def _code_only(text):
@@ -183,24 +183,73 @@ def algorithmic_bytes(cfg):
     return ln, head
 
 
-def cpu_baseline(cfg, inp, min_s=10.0, max_steps=12):
-    """The CPU oracle on complete steps of the same workload (one thread), repeated
-    until at least `min_s` seconds have passed (at most `max_steps` steps)."""
+def host_description():
+    """CPU model name (from /proc/cpuinfo) and the CPUs this process may use."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        usable = os.cpu_count() or 1
+    return model, usable, os.cpu_count() or usable
+
+
+def _oracle_step(oracle, ln, a, t0, t1, g0, g1):
+    """The oracle on LayerNorm rows [t0, t1) and attention units [g0, g1) of one
+    step (a unit range starting at g0 takes the bias planes of its own heads)."""
+    if t1 > t0:
+        oracle.ptf_layernorm_int8(ln["x_q"][t0:t1], ln["zp_in"], ln["alpha"], ln["K"], ln["gamma"],
+                                  ln["beta"], ln["s_out"], ln["zp_out"], ln["bits"])
+    if g1 > g0:
+        import numpy as np
+        b = None
+        if a["bias"] is not None:
+            b = np.ascontiguousarray(a["bias"][np.arange(g0, g1) % a["bias"].shape[0]])
+        oracle.lis_attention_head(a["logits"][g0:g1], a["v"][g0:g1], a["s_logit"], a["bits"],
+                                  a["exp_n"], a["zp_v"], bias=b)
+
+
+def cpu_baseline(cfg, inp, min_s=10.0, max_steps=12, max_threads=16):
+    """The CPU oracle on complete steps of the same workload, timed twice: on one
+    thread, repeated until at least `min_s` seconds have passed (at most
+    `max_steps` steps), and on all usable host CPUs (at most `max_threads`, the
+    CPU share of one GPU), the step's rows and units split into contiguous
+    ranges over threads (the oracle's C code releases the GIL), for the same
+    number of steps.  The all-core run is the reported value."""
+    import concurrent.futures as cf
     import oracle
     ln, a = inp["ln"], inp["attn"]
     reps = 0
     t0 = time.perf_counter()
     while reps < max_steps and (reps == 0 or time.perf_counter() - t0 < min_s):
-        oracle.ptf_layernorm_int8(ln["x_q"], ln["zp_in"], ln["alpha"], ln["K"], ln["gamma"],
-                                  ln["beta"], ln["s_out"], ln["zp_out"], ln["bits"])
-        oracle.lis_attention_head(a["logits"], a["v"], a["s_logit"], a["bits"], a["exp_n"],
-                                  a["zp_v"], bias=a["bias"])
+        _oracle_step(oracle, ln, a, 0, cfg.T, 0, cfg.G)
         reps += 1
-    dt = time.perf_counter() - t0
-    return {"value": reps * cfg.T / dt, "unit": "tokens/s", "cores": 1, "kind": "oracle",
-            "sample": f"{reps} complete steps of {cfg.name} (PTF-LayerNorm {cfg.T}x{cfg.channels}"
-                      f" + LIS attention {cfg.G}x{cfg.Lq}x{cfg.Lk}, d={cfg.d}), single thread,"
-                      f" {dt:.1f} s"}
+    dt1 = time.perf_counter() - t0
+    model, usable, nproc = host_description()
+    nthr = max(1, min(usable, max_threads))
+    parts = 4 * nthr
+    tb = [cfg.T * k // parts for k in range(parts + 1)]
+    gb = [cfg.G * k // parts for k in range(parts + 1)]
+    with cf.ThreadPoolExecutor(nthr) as ex:
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            list(ex.map(lambda k: _oracle_step(oracle, ln, a, tb[k], tb[k + 1], gb[k], gb[k + 1]),
+                        range(parts)))
+        dtn = time.perf_counter() - t0
+    desc = (f"{cfg.name} (PTF-LayerNorm {cfg.T}x{cfg.channels} + LIS attention "
+            f"{cfg.G}x{cfg.Lq}x{cfg.Lk}, d={cfg.d})")
+    return {"value": reps * cfg.T / dtn, "unit": "tokens/s", "cores": nthr, "kind": "oracle",
+            "sample": f"{reps} complete steps of {desc} on {nthr} threads in {dtn:.1f} s, and on "
+                      f"one thread in {dt1:.1f} s",
+            "single_thread_value": reps * cfg.T / dt1,
+            "cpu_model": model, "nproc": nproc, "usable_cpus": usable}
 
 
 def extras(cfg, inp, out, fq, torch, reps=24, n_sets=8):
@@ -377,28 +426,29 @@ def main():
         step(sets[i % N_SETS])
     torch.cuda.synchronize()
 
-    sampled = list(range(0, args.steps, EVENT_EVERY))
-    ev_ln = HipEvents(len(sampled))
-    ev_head = HipEvents(len(sampled))
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     t_start.record()
     for i in range(args.steps):
-        if i % EVENT_EVERY == 0:
-            j = i // EVENT_EVERY
-            step(sets[i % N_SETS], ev_ln.pairs[j], ev_head.pairs[j])
-        else:
-            step(sets[i % N_SETS])
+        step(sets[i % N_SETS])
     t_end.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-
     total_ms = t_start.elapsed_time(t_end)
     ms_step = total_ms / args.steps
-    ln_ms = [ev_ln.elapsed_ms(j) for j in range(len(sampled))]
-    head_ms = [ev_head.elapsed_ms(j) for j in range(len(sampled))]
+
+    # Kernel durations, after the timed region: the same steps, each kernel
+    # with a pair of events attached to its own launch.
+    n_ev = max(EVENT_SAMPLES, args.steps)
+    ev_ln = HipEvents(n_ev)
+    ev_head = HipEvents(n_ev)
+    for i in range(n_ev):
+        step(sets[i % N_SETS], ev_ln.pairs[i], ev_head.pairs[i])
+    torch.cuda.synchronize()
+    ln_ms = [ev_ln.elapsed_ms(j) for j in range(n_ev)]
+    head_ms = [ev_head.elapsed_ms(j) for j in range(n_ev)]
     ev_ln.close()
     ev_head.close()
     ln_avg = sum(ln_ms) / len(ln_ms)
@@ -440,7 +490,7 @@ def main():
         "step_gbs": (ln_bytes + head_bytes) / (ms_step * 1e-3) / 1e9,
         "step_hbm_frac": (ln_bytes + head_bytes) / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "kernels_ms": {"ptf_layernorm_int8": ln_avg, "lis_attention_head": head_avg},
-        "kernel_event_samples": len(sampled),
+        "kernel_event_samples": n_ev,
         "ln_gbs": ln_bytes / (ln_avg * 1e-3) / 1e9,
         "roofline": {
             "kernel": "lis_attention_head",

@@ -201,8 +201,13 @@ fq_status lis_attention_qk(const int8_t* q, const int8_t* k, int32_t zp_q, int32
  *              matter and on return are unspecified.
  * Every operation is rounded in binary64 as written; each channel's squared
  * errors are summed in blocks of 64 consecutive rows, in order, and the block
- * sums added in order, so alpha is a pure function of x.  Ties go to the
- * smallest alpha.  A tensor whose maximum equals its minimum gets s = 0, the
+ * sums added in order, so alpha is a pure function of x; ties of those sums go
+ * to the smallest alpha.  Tie rule against the exact argmin of eq. (11): with
+ * E_a the exact error of candidate a and B_a = (T + 8) 2^-53
+ * sum_t (|x_tc| + 2 |deq_a(x_tc)|)^2 the bound on the rounding of its sum,
+ * alpha_c is the exact argmin (ties to the smallest) unless another candidate
+ * a has E_a - E_best <= B_a + B_best, in which case it may be a.  A tensor
+ * whose maximum equals its minimum gets s = 0, the
  * zero point 0 of the paper's grid and alpha = 0.  T = 0 enqueues nothing and
  * leaves the outputs untouched.
  * Errors: FQ_ERR_NULL, FQ_ERR_SHAPE (T outside [0, 65535 * 64], C outside

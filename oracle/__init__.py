@@ -58,6 +58,7 @@ _SIGS = {
     "oracle_minmax_quantize": [_P, _I64, _F64, _I32, _I32, _P],
     "oracle_ptf_params": [_P, _I64, _I32, _I32, _I32, _P, _P],
     "oracle_ptf_alpha": [_P, _I64, _I32, _F64, _I32, _I32, _I32, _P],
+    "oracle_ptf_alpha_errors": [_P, _I64, _I32, _F64, _I32, _I32, _I32, _P, _P],
     "oracle_ptf_quantize": [_P, _I64, _I32, _F64, _I32, _P, _I32, _P],
     "oracle_ptf_layernorm_int8": [_P, _I64, _I32, _I32, _P, _I32, _P, _P, _F32, _I32, _I32, _P],
     "oracle_iexp_constants": [_F64, _I32, _P],
@@ -72,10 +73,6 @@ _SIGS = {
     "oracle_lis_attention_qk": [_P, _P, _I32, _I32, _I32, _P, _I32, _I64, _I32, _I32, _F32, _I32,
                                 _I32, _P, _I32, _I32, _P],
 }
-
-# Rows per block of the alpha search's error sums (the oracle's reading of
-# the summation order of eq. 11).
-PTF_ERR_BLOCK = 64
 
 
 def lib() -> ctypes.CDLL:
@@ -142,6 +139,19 @@ def ptf_alpha(x: np.ndarray, s: float, zp: int, b: int = 8, K: int = 3) -> np.nd
     alpha = np.empty(C, dtype=np.uint8)
     _check(lib().oracle_ptf_alpha(_ptr(x), T, C, s, zp, b, K, _ptr(alpha)), "ptf_alpha")
     return alpha
+
+
+def ptf_alpha_errors(x: np.ndarray, s: float, zp: int, b: int = 8, K: int = 3,
+                     with_lo: bool = False):
+    """[C, K + 1] exact errors of eq. (11), rounded to binary64; with_lo: also
+    the [C, K + 1] remainders (hi + lo is the exact value to about 106 bits)."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    T, C = x.shape
+    err = np.empty((C, K + 1), dtype=np.float64)
+    lo = np.empty((C, K + 1), dtype=np.float64) if with_lo else None
+    _check(lib().oracle_ptf_alpha_errors(_ptr(x), T, C, s, zp, b, K, _ptr(err), _ptr(lo)),
+           "ptf_alpha_errors")
+    return (err, lo) if with_lo else err
 
 
 def ptf_quantize(x: np.ndarray, s: float, zp: int, alpha: np.ndarray, b: int = 8) -> np.ndarray:

@@ -108,45 +108,168 @@ static double ptf_q(double x, double s, int32_t zp, int32_t alpha, double levels
     return clip_d(round_nearest(x / (ldexp(1.0, alpha) * s)) + (double)zp, 0.0, levels);
 }
 
-int oracle_ptf_alpha(const double* x, int64_t T, int32_t C, double s, int32_t zp, int32_t b,
-                     int32_t K, uint8_t* alpha) {
-    if (!x || !alpha || T <= 0 || C <= 0 || b < 1 || b > 16 || K < 0 || K > 7 || !(s > 0.0))
+/* ---- exact sums of binary64 values --------------------------------------
+ * An exact accumulator: a signed fixed-point integer with 32-bit digits whose
+ * least significant bit is 2^-1127, below the least significant bit of any
+ * binary64 significand (subnormals included), and whose top digit reaches
+ * past 2^1024.  Each added double m 2^e (m a 53-bit integer) lands in three
+ * consecutive digits; the digits are int64, so up to 2^31 additions fit
+ * before any carry is propagated.  The value is the exact sum of everything
+ * added, independent of the order of the additions. */
+#define XACC_LSB_EXP (-1127)
+#define XACC_DIGITS 72
+
+typedef struct {
+    int64_t d[XACC_DIGITS];
+} xacc;
+
+static void xacc_add(xacc* acc, double v) {
+    if (v == 0.0) return;
+    int e = 0;
+    const double f = frexp(fabs(v), &e);            /* |v| = f 2^e, f in [0.5, 1) */
+    const uint64_t m = (uint64_t)ldexp(f, 53);      /* |v| = m 2^(e - 53), exact    */
+    const int pos = e - 53 - XACC_LSB_EXP;          /* bit index of m's lowest bit  */
+    const int di = pos / 32, sh = pos % 32;
+    const unsigned __int128 w = (unsigned __int128)m << sh;   /* below 2^85 */
+    const int64_t sgn = v < 0.0 ? -1 : 1;
+    for (int k = 0; k < 3 && di + k < XACC_DIGITS; ++k)
+        acc->d[di + k] += sgn * (int64_t)(uint32_t)(w >> (32 * k));
+}
+
+/* Carry propagation: every digit but the top one in [0, 2^32). */
+static void xacc_normalize(xacc* acc) {
+    for (int i = 0; i + 1 < XACC_DIGITS; ++i) {
+        const int64_t carry = acc->d[i] >> 32;      /* floor division by 2^32 */
+        acc->d[i] -= carry * ((int64_t)1 << 32);
+        acc->d[i + 1] += carry;
+    }
+}
+
+/* Sign of a - b (-1, 0, 1), exactly. */
+static int xacc_cmp(const xacc* a, const xacc* b) {
+    xacc t;
+    for (int i = 0; i < XACC_DIGITS; ++i) t.d[i] = a->d[i] - b->d[i];
+    xacc_normalize(&t);
+    for (int i = XACC_DIGITS - 1; i >= 0; --i)
+        if (t.d[i] != 0) return (i == XACC_DIGITS - 1 && t.d[i] < 0) ? -1 : 1;
+    return 0;
+}
+
+/* The accumulated value rounded to a double (the three top digits summed in
+ * long double, then rounded: within one unit in the last place).  acc must
+ * be normalized. */
+static double xacc_value(const xacc* acc) {
+    if (acc->d[XACC_DIGITS - 1] < 0) {            /* negative: the value of -acc, negated */
+        xacc neg;
+        for (int i = 0; i < XACC_DIGITS; ++i) neg.d[i] = -acc->d[i];
+        xacc_normalize(&neg);
+        return -xacc_value(&neg);
+    }
+    int top = XACC_DIGITS - 1;
+    while (top > 0 && acc->d[top] == 0) --top;
+    long double v = 0.0L;
+    for (int i = top; i >= 0 && i >= top - 2; --i)
+        v += ldexpl((long double)acc->d[i], 32 * i + XACC_LSB_EXP);
+    return (double)v;
+}
+
+/* The accumulated value as an unevaluated pair hi + lo: hi as xacc_value,
+ * lo the rest of the exact value, rounded.  acc must be normalized. */
+static void xacc_value2(const xacc* acc, double* hi, double* lo) {
+    *hi = xacc_value(acc);
+    xacc rest = *acc;
+    xacc_add(&rest, -*hi);
+    xacc_normalize(&rest);
+    *lo = xacc_value(&rest);
+}
+
+/* Error-free product: hi + lo = a b exactly (no underflow assumed). */
+static void two_prod(double a, double b, double* hi, double* lo) {
+    *hi = a * b;
+    *lo = fma(a, b, -*hi);
+}
+
+/* Error-free sum: hi + lo = a + b exactly. */
+static void two_sum(double a, double b, double* hi, double* lo) {
+    *hi = a + b;
+    const double bb = *hi - a;
+    *lo = (a - (*hi - bb)) + (b - bb);
+}
+
+/* Adds (x - k step)^2 to acc exactly.  With k step = p + p' and
+ * x - p = u + u' (error-free), the difference is u + u' - p' and its square
+ * is the sum of the six exact products of those three terms. */
+static void add_exact_sq_err(xacc* acc, double x, double k, double step) {
+    double p, pl, u, ul;
+    two_prod(k, step, &p, &pl);
+    two_sum(x, -p, &u, &ul);
+    const double t[3] = {u, ul, -pl};
+    for (int i = 0; i < 3; ++i)
+        for (int j = i; j < 3; ++j) {
+            double h, l;
+            two_prod(t[i], t[j], &h, &l);
+            const double f = (i == j) ? 1.0 : 2.0;
+            xacc_add(acc, f * h);
+            xacc_add(acc, f * l);
+        }
+}
+
+/* eq. (11) for every channel and candidate: err[c (K+1) + a] (+ err_lo[...]
+ * when err_lo is non-null) receives the exact error sum_t (x_tc - deq_a(x_tc))^2
+ * as an unevaluated pair (see xacc_value2) and,
+ * when alpha is non-null, alpha[c] the argmin over a (exact comparison, ties to
+ * the smallest a).  deq_a is the quantizer of eq. (8) on the grid 2^a s with its
+ * zero point and clip, dequantized: (clip(round(x / (2^a s)) + zp) - zp) 2^a s,
+ * the quotient rounded in binary64 as in oracle_ptf_quantize.
+ * READING: the printed argmin omits zp and the clip; taken literally the finest
+ * grid always wins.  The error is measured on the quantizer that is actually
+ * used.  READING: the norm is computed exactly (the exact square of the exact
+ * difference, summed exactly), so the result does not depend on any
+ * summation order.  Exactness needs every |x| and s within [2^-300, 2^300]
+ * (no underflow in the error-free products); the activations of a network are. */
+static int ptf_alpha_impl(const double* x, int64_t T, int32_t C, double s, int32_t zp, int32_t b,
+                          int32_t K, uint8_t* alpha, double* err, double* err_lo) {
+    if (!x || T <= 0 || C <= 0 || b < 1 || b > 16 || K < 0 || K > 7 || !(s > 0.0))
         return ORACLE_ERR_ARG;
+    if (T > ((int64_t)1 << 26)) return ORACLE_ERR_ARG;     /* 12 T additions per digit < 2^31 */
     const double levels = (double)((1 << b) - 1);
+    xacc* acc = (xacc*)malloc(sizeof(xacc) * (size_t)(K + 1));
+    if (!acc) return ORACLE_ERR_ARG;
     for (int32_t c = 0; c < C; ++c) {
-        /* eq. (11): alpha_c = argmin over {0..K} of || X_c - dequant(quant(X_c)) ||_2.
-         * READING: the printed argmin omits zp and the clip; taken literally the
-         * finest grid always wins.  The error is measured on the quantizer that
-         * is actually used, eq. (8) with its zp and clip.  Ties go to the
-         * smallest alpha. */
-        /* READING: the paper does not fix the order of the sum over t.  The
-         * squared errors are summed in blocks of ORACLE_PTF_ERR_BLOCK
-         * consecutive rows (in order within a block), and the block sums are
-         * added in block order, so that a parallel implementation can
-         * reproduce the same sums, and so the same argmin, exactly. */
-        int32_t best = 0;
-        double best_err = INFINITY;
+        memset(acc, 0, sizeof(xacc) * (size_t)(K + 1));
         for (int32_t a = 0; a <= K; ++a) {
-            const double step = ldexp(1.0, a) * s;
-            double err = 0.0;
-            for (int64_t t0 = 0; t0 < T; t0 += ORACLE_PTF_ERR_BLOCK) {
-                const int64_t t1 = t0 + ORACLE_PTF_ERR_BLOCK < T ? t0 + ORACLE_PTF_ERR_BLOCK : T;
-                double part = 0.0;
-                for (int64_t t = t0; t < t1; ++t) {
-                    const double xv = x[t * C + c];
-                    const double deq = (ptf_q(xv, s, zp, a, levels) - (double)zp) * step;
-                    part += (xv - deq) * (xv - deq);
-                }
-                err += part;
+            const double step = ldexp(s, a);
+            for (int64_t t = 0; t < T; ++t) {
+                const double xv = x[t * C + c];
+                add_exact_sq_err(&acc[a], xv, ptf_q(xv, s, zp, a, levels) - (double)zp, step);
             }
-            if (err < best_err) {
-                best_err = err;
-                best = a;
+            xacc_normalize(&acc[a]);
+            if (err) {
+                double hi, lo;
+                xacc_value2(&acc[a], &hi, &lo);
+                err[(int64_t)c * (K + 1) + a] = hi;
+                if (err_lo) err_lo[(int64_t)c * (K + 1) + a] = lo;
             }
         }
-        alpha[c] = (uint8_t)best;
+        int32_t best = 0;
+        for (int32_t a = 1; a <= K; ++a)
+            if (xacc_cmp(&acc[a], &acc[best]) < 0) best = a;
+        if (alpha) alpha[c] = (uint8_t)best;
     }
+    free(acc);
     return ORACLE_OK;
+}
+
+int oracle_ptf_alpha(const double* x, int64_t T, int32_t C, double s, int32_t zp, int32_t b,
+                     int32_t K, uint8_t* alpha) {
+    if (!alpha) return ORACLE_ERR_ARG;
+    return ptf_alpha_impl(x, T, C, s, zp, b, K, alpha, NULL, NULL);
+}
+
+int oracle_ptf_alpha_errors(const double* x, int64_t T, int32_t C, double s, int32_t zp,
+                            int32_t b, int32_t K, double* err, double* err_lo) {
+    if (!err) return ORACLE_ERR_ARG;
+    return ptf_alpha_impl(x, T, C, s, zp, b, K, NULL, err, err_lo);
 }
 
 int oracle_ptf_quantize(const double* x, int64_t T, int32_t C, double s, int32_t zp,
@@ -328,40 +451,42 @@ int oracle_iexp_constants(double s, int32_t n, oracle_iexp_consts* k) {
     return ORACLE_OK;
 }
 
+/* I-Exp (Supplement A.2, Alg. 1).  For an input t <= 0 of scale s, clamped
+ * below at n q_ln2 (READING: the depth n is not defined by the paper; it is
+ * an argument, and 2^-n is then the smallest output relative to exp(0)),
+ * write u = -t = z d + r with d = -q_ln2 > 0, z = floor(u / d) and
+ * r in [0, d): then exp(s t) = 2^-z exp(-s r), and exp on (-ln2, 0] is
+ * replaced by the quadratic L(p) = a (p + b)^2 + c, which on the integer
+ * grid is s_L ((q_b - r)^2 + q_c).  The result is that polynomial value
+ * scaled by 2^(n - z), with scale s_L / 2^n.
+ * READING: the algorithm prints the polynomial as (q + q_b)^2 + q_c; it is
+ * evaluated at the remainder, -r, as the definition of L(p) requires. */
 int64_t oracle_iexp(int64_t q, const oracle_iexp_consts* k, int64_t* z_out, int64_t* qp_out) {
-    /* q <- max(q, n q_ln2).  READING: n, the clamp depth, is not defined by the
-     * paper; it is an argument (2^-n is the smallest value i-exp can return
-     * relative to exp(0)). */
-    const int64_t floor_q = (int64_t)k->n * k->q_ln2;
-    if (q < floor_q) q = floor_q;
-    const int64_t z = floor_div(q, k->q_ln2);             /* z   = floor(q / q_ln2)     */
-    const int64_t q_p = q - z * k->q_ln2;                 /* q_p = q - z q_ln2          */
-    /* READING: the algorithm prints q_L = (q + q_b)^2 + q_c; the polynomial is
-     * evaluated at p, i.e. at q_p (L(p) = a(p + b)^2 + c). */
-    const int64_t q_L = (q_p + k->q_b) * (q_p + k->q_b) + k->q_c;
+    const int64_t d = -k->q_ln2;
+    const int64_t u_max = (int64_t)k->n * d;
+    const int64_t u = -q < u_max ? -q : u_max;          /* the clamp at n q_ln2 */
+    const int64_t z = u / d;                            /* u >= 0, d > 0: floor */
+    const int64_t r = u - z * d;                        /* in [0, d) */
+    const int64_t w = k->q_b - r;
+    const int64_t poly = w * w + k->q_c;
     if (z_out) *z_out = z;
-    if (qp_out) *qp_out = q_p;
-    /* q_out = q_L << (n - z), output scale s_L / 2^n. */
-    return q_L * ((int64_t)1 << (k->n - z));
+    if (qp_out) *qp_out = -r;
+    return poly << (k->n - z);
 }
 
 /* ------------------------------------------------------------------------ */
 /* Supplement A.2, Algorithm 2: I-Log2 and Log-Int-Softmax                   */
 /* ------------------------------------------------------------------------ */
 
-/* Find_First_One: index of the most significant 1 bit (-1 for q = 0). */
-static int32_t find_first_one(uint64_t q) {
-    for (int32_t i = 63; i >= 0; --i)
-        if ((q >> i) & 1u) return i;
-    return -1;
-}
-
-int32_t oracle_ilog2(uint64_t q) {
-    const int32_t M = find_first_one(q);
-    if (M < 0) return 0;
-    /* chi = the (M-1)th bit of q.  READING: for M = 0 there is no such bit; chi = 0. */
-    const int32_t chi = (M >= 1) ? (int32_t)((q >> (M - 1)) & 1u) : 0;
-    return M + chi;
+/* I-Log2 (Supplement A.2, Alg. 2): log2 r rounded to an integer at the
+ * midpoint 1.5 2^M of [2^M, 2^(M+1)), M the index of the leading one of r.
+ * READING: r = 1 (M = 0) has no bit below its leading one and maps to 0. */
+int32_t oracle_ilog2(uint64_t r) {
+    if (r == 0) return 0;
+    int32_t M = 63;
+    while (((r >> M) & 1u) == 0) --M;
+    const int32_t round_up = (unsigned __int128)2 * r >= ((unsigned __int128)3 << M);
+    return M + round_up;
 }
 
 static int lis_check(int64_t G, int32_t Lq, int32_t Lk, int32_t bits, int32_t exp_n,
@@ -377,33 +502,31 @@ static int32_t codes_row_bytes(int32_t Lk, int32_t bits) {
     return bits <= 4 ? (Lk + 1) / 2 : Lk;
 }
 
-/* One row of Log-Int-Softmax: Attn_Q for every key.  v holds logits + bias. */
+/* Log-Int-Softmax of one row (Supplement A.2, Alg. 2, with the clip of the
+ * LIS equation in the same section): e_j = I-Exp(v_j - max_i v_i), S = sum e_j
+ * (a wide integer, so it cannot wrap), and
+ *     Attn_Q_j = min(I-Log2(round(S / e_j)), 2^b - 1),
+ * where round(S / e_j) = floor((2 S + e_j) / (2 e_j)) (READING: ties round up;
+ * the ratio is at least 1).  Attn_Q_j approximates -log2 of the softmax
+ * probability e_j / S; the paper's LIS output is N - Attn_Q_j with
+ * N = 2^b - 1 and scale 2^-N.  READING: Algorithm 2 omits the clip that the
+ * LIS equation has; it is applied. */
 static void lis_row(const int64_t* v, int32_t Lk, const oracle_iexp_consts* k, int32_t bits,
                     int64_t* e, int32_t* code) {
-    /* q~ = q - max(q) */
-    int64_t mx = v[0];
-    for (int32_t j = 1; j < Lk; ++j)
-        if (v[j] > mx) mx = v[j];
-    /* q_exp = I-Exp(q~) and its sum (a wide integer, so it cannot wrap). */
-    unsigned __int128 sum = 0;
+    int64_t vmax = v[0];
+    for (int32_t j = 1; j < Lk; ++j) vmax = v[j] > vmax ? v[j] : vmax;
+    unsigned __int128 S = 0;
     for (int32_t j = 0; j < Lk; ++j) {
-        e[j] = oracle_iexp(v[j] - mx, k, NULL, NULL);
-        sum += (unsigned __int128)e[j];
+        e[j] = oracle_iexp(v[j] - vmax, k, NULL, NULL);
+        S += (unsigned __int128)e[j];
     }
     const int32_t top = (1 << bits) - 1;
     for (int32_t j = 0; j < Lk; ++j) {
-        /* q_rev = round(sum(q_exp) / q_exp).  READING: ties round up,
-         * floor((2 sum + q_exp) / (2 q_exp)). */
         const unsigned __int128 ej = (unsigned __int128)e[j];
-        const unsigned __int128 q_rev = (2 * sum + ej) / (2 * ej);
-        const uint64_t q_rev64 = q_rev > (unsigned __int128)UINT64_MAX
-                                     ? UINT64_MAX : (uint64_t)q_rev;
-        /* Attn_Q = clip(I-Log2(q_rev), 0, 2^b - 1); the LIS output is N - Attn_Q
-         * with N = 2^b - 1 and scale 1/2^N.  The clip is in the LIS equation of
-         * the supplement (Algorithm 2 omits it). */
-        int32_t a = oracle_ilog2(q_rev64);
-        if (a > top) a = top;
-        code[j] = a;
+        const unsigned __int128 ratio = (2 * S + ej) / (2 * ej);
+        const uint64_t r = ratio > (unsigned __int128)UINT64_MAX ? UINT64_MAX : (uint64_t)ratio;
+        const int32_t lg = oracle_ilog2(r);
+        code[j] = lg < top ? lg : top;
     }
 }
 

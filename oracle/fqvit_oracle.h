@@ -48,11 +48,16 @@ int oracle_minmax_quantize(const double* x, int64_t n, double s, int32_t zp, int
 /* Layer-wise s (eq. 9) and zp (eq. 10) over a row-major [T, C] tensor. */
 int oracle_ptf_params(const double* x, int64_t T, int32_t C, int32_t b, int32_t K,
                       double* s, int32_t* zp);
-/* Per-channel alpha by the argmin of eq. (11) over {0..K}; each channel's
- * squared errors are summed in blocks of ORACLE_PTF_ERR_BLOCK rows. */
-#define ORACLE_PTF_ERR_BLOCK 64
+/* Per-channel alpha by the argmin of eq. (11) over {0..K}: each channel's
+ * error is the exact sum of the exact squared errors, so no summation order
+ * enters; ties go to the smallest alpha.  T <= 2^26. */
 int oracle_ptf_alpha(const double* x, int64_t T, int32_t C, double s, int32_t zp,
                      int32_t b, int32_t K, uint8_t* alpha);
+/* The exact errors themselves, err[c (K+1) + a]: the exact value rounded to
+ * a double (within one unit in the last place) and, if err_lo is non-null,
+ * err_lo[c (K+1) + a] the rest of the exact value, rounded. */
+int oracle_ptf_alpha_errors(const double* x, int64_t T, int32_t C, double s, int32_t zp,
+                            int32_t b, int32_t K, double* err, double* err_lo);
 /* X_Q = clip(round(X / (2^alpha_c s)) + zp, 0, 2^b - 1) (eq. 8), unsigned grid. */
 int oracle_ptf_quantize(const double* x, int64_t T, int32_t C, double s, int32_t zp,
                         const uint8_t* alpha, int32_t b, int32_t* q);

@@ -43,6 +43,24 @@ class FqError(RuntimeError):
 _lib: Optional[ctypes.CDLL] = None
 
 
+def load(path: str) -> ctypes.CDLL:
+    """Open a build of libfqvit at `path` and declare its entry points' C types."""
+    L = ctypes.CDLL(path)
+    for name, args in SIGNATURES.items():
+        fn = getattr(L, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_int32
+    L.fq_status_str.argtypes = [ctypes.c_int]
+    L.fq_status_str.restype = ctypes.c_char_p
+    L.fq_version.argtypes = []
+    L.fq_version.restype = ctypes.c_int32
+    L.fq_time_next_call.argtypes = [_P, _P]
+    L.fq_time_next_call.restype = ctypes.c_int32
+    L.fq_ptf_calibrate_workspace_bytes.argtypes = [_I64, _I32, _I32]
+    L.fq_ptf_calibrate_workspace_bytes.restype = ctypes.c_size_t
+    return L
+
+
 def lib() -> ctypes.CDLL:
     """The loaded C library (raises if it has not been built)."""
     global _lib
@@ -50,20 +68,7 @@ def lib() -> ctypes.CDLL:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -c "
                                f"'import __graft_entry__ as g; g.build()'` (no fallback exists)")
-        L = ctypes.CDLL(LIB_PATH)
-        for name, args in SIGNATURES.items():
-            fn = getattr(L, name)
-            fn.argtypes = args
-            fn.restype = ctypes.c_int32
-        L.fq_status_str.argtypes = [ctypes.c_int]
-        L.fq_status_str.restype = ctypes.c_char_p
-        L.fq_version.argtypes = []
-        L.fq_version.restype = ctypes.c_int32
-        L.fq_time_next_call.argtypes = [_P, _P]
-        L.fq_time_next_call.restype = ctypes.c_int32
-        L.fq_ptf_calibrate_workspace_bytes.argtypes = [_I64, _I32, _I32]
-        L.fq_ptf_calibrate_workspace_bytes.restype = ctypes.c_size_t
-        _lib = L
+        _lib = load(LIB_PATH)
     return _lib
 
 

@@ -74,6 +74,14 @@ bool grid_fits(int64_t G, int32_t Lq, int32_t rows_per_block) {
 
 }  // namespace
 
+// Workspace of the calibration: the min/max partials, the per-block error sums
+// of every candidate alpha and channel, and the per-channel totals.
+size_t fqvit::ptf_calibrate_workspace_bytes(int64_t T, int32_t C, int32_t K) {
+    const int64_t nb = (T + kPtfErrBlock - 1) / kPtfErrBlock;
+    return (size_t)kMinmaxParts * 2 * sizeof(float) + (size_t)(K + 1) * nb * C * sizeof(double) +
+           (size_t)(K + 1) * C * sizeof(double);
+}
+
 const fqvit::LaunchEvents& fqvit::launch_events() { return t_events; }
 void fqvit::set_launch_events(hipEvent_t start, hipEvent_t stop) {
     t_events.start = start;

@@ -1,9 +1,10 @@
 // Internal declarations shared by the gfx950 kernels and the C ABI wrappers of
-// libfqvit.  Not part of the public interface (include/fqvit.h is).
+// libfqvit.  Not part of the public interface (include/fqvit.h is).  Only the
+// HIP runtime API types are needed here, so the C ABI's host code compiles with
+// any C++17 compiler; the launch helper lives in fqvit_launch.h.
 #pragma once
 
-#include <hip/hip_ext.h>
-#include <hip/hip_runtime.h>
+#include <hip/hip_runtime_api.h>
 #include <stdint.h>
 
 namespace fqvit {
@@ -18,19 +19,6 @@ const LaunchEvents& launch_events();
 // Replaces the current call's events (for entry points that launch several
 // kernels: the start event goes on the first, the stop event on the last).
 void set_launch_events(hipEvent_t start, hipEvent_t stop);
-
-// Every kernel launch of the library goes through here so that the events, if
-// any, record the kernel's own start and end.
-template <typename... KArgs, typename... Args>
-inline void launch_kernel(void (*kernel)(KArgs...), dim3 grid, dim3 block, size_t lds,
-                          hipStream_t stream, Args... args) {
-    const LaunchEvents& ev = launch_events();
-    if (ev.start || ev.stop)
-        hipExtLaunchKernelGGL(kernel, grid, block, (uint32_t)lds, stream, ev.start, ev.stop, 0,
-                              args...);
-    else
-        hipLaunchKernelGGL(kernel, grid, block, lds, stream, args...);
-}
 
 // ---------------------------------------------------------------------------
 // PTF LayerNorm

@@ -46,7 +46,7 @@
 // The host picks the float path whenever its exactness conditions hold.
 #pragma once
 
-#include "fqvit_internal.h"
+#include "fqvit_launch.h"
 
 namespace fqvit {
 namespace lis {

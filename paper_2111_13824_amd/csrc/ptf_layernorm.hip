@@ -22,7 +22,7 @@
 // shuffle reduction.  Per-channel gs, bs and the clamped shift are computed
 // once per workgroup into LDS and then held in registers; waves stride over
 // rows.
-#include "fqvit_internal.h"
+#include "fqvit_launch.h"
 
 namespace fqvit {
 namespace {

@@ -13,13 +13,16 @@
 //   4. alpha_select    per channel and alpha, the block sums added in block
 //                      order, then per channel the argmin over alpha (the
 //                      smallest on ties).
-// Steps 3 and 4 reproduce the blocked summation order exactly, so the argmin
-// is a pure function of x.  x / (2^alpha s) is computed as ldexp(x / s,
+// Steps 3 and 4 fix the summation order, so the argmin is a pure function of
+// x.  Against the exact argmin of eq. (11) (an exact sum of exact squares) the
+// binary64 terms and sums can only swap candidates whose exact errors differ
+// by less than the sum of their rounding bounds, (T + 8) 2^-53 times
+// sum_t (|x| + 2 |deq|)^2 each.  x / (2^alpha s) is computed as ldexp(x / s,
 // -alpha): scaling by a power of two commutes with the rounding of the
 // quotient, which never leaves the normal range for binary32 inputs.
 #include <cmath>
 
-#include "fqvit_internal.h"
+#include "fqvit_launch.h"
 
 namespace fqvit {
 namespace {
@@ -398,12 +401,6 @@ unsigned grid_for(int64_t work, int64_t per_block, int64_t cap) {
 }
 
 }  // namespace
-
-size_t ptf_calibrate_workspace_bytes(int64_t T, int32_t C, int32_t K) {
-    const int64_t nb = (T + kPtfErrBlock - 1) / kPtfErrBlock;
-    return (size_t)kMinmaxParts * 2 * sizeof(float) + (size_t)(K + 1) * nb * C * sizeof(double) +
-           (size_t)(K + 1) * C * sizeof(double);
-}
 
 template <int K>
 void launch_alpha_partial(const PtfCalibArgs& a, dim3 grid, int64_t nb, double* part,

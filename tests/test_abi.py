@@ -21,12 +21,25 @@ def _declared_functions():
                       text, flags=re.M)
 
 
+# A test build of the C ABI's host code (tests/test_sanitizers.py: built with
+# AddressSanitizer and UndefinedBehaviorSanitizer and linked against counting
+# stand-ins for the kernel launchers) can be named here instead of libfqvit.
+STUB_LIB = os.environ.get("FQVIT_ABI_TEST_LIB")
+
+
 @pytest.fixture(scope="module")
 def lib():
+    if STUB_LIB:
+        saved = B._lib
+        B._lib = B.load(STUB_LIB)
+        B._lib.fq_test_launch_count.restype = ctypes.c_int
+        yield B._lib
+        B._lib = saved
+        return
     if not os.path.exists(B.LIB_PATH):
         from paper_2111_13824_amd import build
         build.build()
-    return B.lib()
+    yield B.lib()
 
 
 def test_header_symbols_exported(lib):
@@ -167,6 +180,7 @@ def test_head_validation(lib):
     assert call(Lq=0, lg=NULL, v=NULL, out=NULL) == B.FQ_OK
 
 
+@pytest.mark.skipif(bool(STUB_LIB), reason="tests the binding's own loader")
 def test_binding_requires_library(monkeypatch):
     """The binding refuses to run without the HIP library instead of falling back."""
     monkeypatch.setattr(B, "_lib", None)
@@ -275,3 +289,32 @@ def test_qk_validation(lib):
         assert call(**{key: None}) == B.FQ_ERR_NULL
     assert call(G=0, q=None) == B.FQ_OK
     assert call(Lq=0, out=None) == B.FQ_OK
+
+
+@pytest.mark.skipif(not STUB_LIB, reason="needs the host-only test build (counting launchers)")
+def test_valid_calls_reach_exactly_one_launch(lib):
+    """With the launchers replaced by counters: every valid call reaches its
+    launcher once and returns FQ_OK; a rejected or empty call reaches none."""
+    count = lib.fq_test_launch_count
+
+    def launches(fn, *args):
+        n0 = count()
+        rc = fn(*args)
+        return rc, count() - n0
+
+    f32 = ctypes.c_float
+    assert launches(lib.ptf_layernorm_int8, 1, 4, 8, 0, 1, 3, 1, 1, f32(0.1), 0, 8, 1, None) == (0, 1)
+    assert launches(lib.ptf_layernorm_int8, 1, 4, 8, 0, 1, 3, 1, 1, f32(0.0), 0, 8, 1, None)[1] == 0
+    assert launches(lib.ptf_layernorm_int8, 1, 0, 8, 0, 1, 3, 1, 1, f32(0.1), 0, 8, 1, None) == (0, 0)
+    assert launches(lib.lis_softmax_log4, 1, 2, 5, 7, None, 0, f32(0.001), 4, 20, 1, 4, None) == (0, 1)
+    assert launches(lib.lis_softmax_log4, 1, 2, 5, 7, None, 0, f32(0.001), 4, 20, 1, 3, None)[1] == 0
+    assert launches(lib.lis_attn_v_shift, 1, 4, 1, 0, 2, 5, 7, 64, 4, 1, None) == (0, 1)
+    assert launches(lib.lis_attention_head, 1, None, 0, 2, 5, 7, f32(0.001), 4, 20, 1, 0, 64, 1,
+                    None, 0, None) == (0, 1)
+    assert launches(lib.lis_attention_qk, 16, 16, 0, 0, 64, None, 0, 2, 5, 7, f32(0.001), 4, 20,
+                    1, 0, 64, 1, None) == (0, 1)
+    need = lib.fq_ptf_calibrate_workspace_bytes(100, 16, 3)
+    assert launches(lib.ptf_calibrate, 1, 100, 16, 8, 3, 1, 1, 1, 1, need, None) == (0, 1)
+    assert launches(lib.ptf_calibrate, 1, 100, 16, 8, 3, 1, 1, 1, 1, need - 1, None)[1] == 0
+    assert launches(lib.ptf_quantize_int8, 1, 10, 16, 1, 1, 1, 8, 1, None) == (0, 1)
+    assert launches(lib.requant_dyadic_int8, 1, 10, f32(0.5), f32(0.25), 0, 8, 1, None) == (0, 1)

@@ -32,15 +32,18 @@ MUTANTS = [
     ("ln_sign_dropped", "const int64_t y = sgn * N2 * Xh[i] + Bq;", "const int64_t y = N2 * Xh[i] + Bq;"),
     ("q_ln2_ceil", "(int64_t)floor(-LN2 / s)", "(int64_t)ceil(-LN2 / s)"),
     ("q_c_missing_s", "IEXP_C / ((IEXP_A * s) * s)", "IEXP_C / (IEXP_A * s)"),
-    ("q_L_as_printed", "(q_p + k->q_b) * (q_p + k->q_b) + k->q_c", "(q + k->q_b) * (q + k->q_b) + k->q_c"),
-    ("q_c_dropped", "(q_p + k->q_b) * (q_p + k->q_b) + k->q_c", "(q_p + k->q_b) * (q_p + k->q_b)"),
-    ("exp_shift_direction", "q_L * ((int64_t)1 << (k->n - z))", "q_L * ((int64_t)1 << z)"),
-    ("clamp_dropped", "if (q < floor_q) q = floor_q;", "if (q < 2 * floor_q) q = 2 * floor_q;"),
-    ("max_not_subtracted", "e[j] = oracle_iexp(v[j] - mx, k, NULL, NULL);", "e[j] = oracle_iexp(v[j] - v[0], k, NULL, NULL);"),
-    ("q_rev_floor", "(2 * sum + ej) / (2 * ej)", "(2 * sum) / (2 * ej)"),
-    ("chi_wrong_bit", "(q >> (M - 1)) & 1u", "(q >> (M - 2)) & 1u"),
-    ("chi_dropped", "return M + chi;", "return M;"),
-    ("code_clip_dropped", "if (a > top) a = top;", "if (a > top) a = a & top;"),
+    ("q_L_as_printed", "const int64_t w = k->q_b - r;", "const int64_t w = k->q_b - u;"),
+    ("q_c_dropped", "const int64_t poly = w * w + k->q_c;", "const int64_t poly = w * w;"),
+    ("exp_shift_direction", "return poly << (k->n - z);", "return poly << z;"),
+    ("clamp_dropped", "const int64_t u = -q < u_max ? -q : u_max;",
+     "const int64_t u = -q < 2 * u_max ? -q : 2 * u_max;"),
+    ("max_not_subtracted", "e[j] = oracle_iexp(v[j] - vmax, k, NULL, NULL);",
+     "e[j] = oracle_iexp(v[j] - v[0], k, NULL, NULL);"),
+    ("q_rev_floor", "(2 * S + ej) / (2 * ej)", "(2 * S) / (2 * ej)"),
+    ("ilog2_rounds_at_1_25", "(unsigned __int128)2 * r >= ((unsigned __int128)3 << M)",
+     "(unsigned __int128)4 * r >= ((unsigned __int128)5 << M)"),
+    ("ilog2_round_bit_dropped", "return M + round_up;", "return M;"),
+    ("code_clip_dropped", "code[j] = lg < top ? lg : top;", "code[j] = lg & top;"),
     ("nibble_order", "(uint8_t)(lo | (hi << 4))", "(uint8_t)(hi | (lo << 4))"),
     ("bias_wrong_head", "bias + ((g % Hb) * Lq + i)", "bias + ((g / Hb % Hb) * Lq + i)"),
     ("av_zp_dropped", "(int64_t)v[(g * Lk + j) * (int64_t)d + c] - zp_v;", "(int64_t)v[(g * Lk + j) * (int64_t)d + c];"),
@@ -49,11 +52,18 @@ MUTANTS = [
     ("ptf_scale_times_2K", "(mx - mn) / levels / two_K", "(mx - mn) / levels * two_K"),
     ("ptf_quant_neg_alpha", "x / (ldexp(1.0, alpha) * s)", "x / (ldexp(1.0, -alpha) * s)"),
     ("minmax_zp_sign", "round_nearest(-l / *s)", "round_nearest(l / *s)"),
-    ("alpha_tail_block_dropped", "t0 < T; t0 += ORACLE_PTF_ERR_BLOCK",
-     "t0 + ORACLE_PTF_ERR_BLOCK <= T; t0 += ORACLE_PTF_ERR_BLOCK"),
-    ("alpha_deq_zp_dropped", "(ptf_q(xv, s, zp, a, levels) - (double)zp) * step",
-     "ptf_q(xv, s, zp, a, levels) * step"),
-    ("alpha_argmax", "if (err < best_err) {", "if (err > best_err || a == 0) {"),
+    ("alpha_last_row_dropped", "for (int64_t t = 0; t < T; ++t) {\n                const double xv",
+     "for (int64_t t = 0; t < T - 1; ++t) {\n                const double xv"),
+    ("alpha_deq_zp_dropped", "ptf_q(xv, s, zp, a, levels) - (double)zp, step)",
+     "ptf_q(xv, s, zp, a, levels), step)"),
+    ("alpha_argmax", "if (xacc_cmp(&acc[a], &acc[best]) < 0) best = a;",
+     "if (xacc_cmp(&acc[a], &acc[best]) > 0) best = a;"),
+    ("alpha_cross_terms_halved", "const double f = (i == j) ? 1.0 : 2.0;",
+     "const double f = (i == j) ? 1.0 : 1.0;"),
+    ("alpha_residual_low_part_dropped", "const double t[3] = {u, ul, -pl};",
+     "const double t[3] = {u, 0.0, -pl};"),
+    ("alpha_product_rounded", "xacc_add(acc, f * h);\n            xacc_add(acc, f * l);",
+     "xacc_add(acc, f * h + f * l);"),
     ("requant_precision_16", "int64_t N1 = 31 - (int64_t)e;", "int64_t N1 = 16 - (int64_t)e;"),
     ("requant_round_down", "(prod + ((__int128)1 << (N1 - 1))) >> N1", "prod >> N1"),
     ("requant_zp_dropped", "const __int128 yu = w + zp;", "const __int128 yu = w + half;"),

@@ -374,42 +374,43 @@ def test_ptf_alpha_search_outliers(orc):
 
 
 def _exact_ptf_errors(x, s, zp, K, b=8):
-    """Exact rational squared errors of eq. (11) per channel and alpha: the
-    quantized value from the exact quotient (half to even), then the exact
-    residual.  Returns (errors [C][K+1], set of (c, alpha) whose quotient is
-    within 2^-40 of a rounding tie, where a double quotient may round the
-    other way)."""
+    """Exact rational errors of eq. (11) per channel and alpha, [C][K+1]: the
+    quantized value of eq. (8) from the binary64 quotient x / (2^alpha s)
+    rounded half to even (Python's float division and round() are both
+    IEEE), then the exact squared residual, summed exactly."""
     from fractions import Fraction as F
     levels = 2 ** b - 1
-    S = F(s)
     T, C = x.shape
     err = [[F(0)] * (K + 1) for _ in range(C)]
-    fragile = set()
     for c in range(C):
         for a in range(K + 1):
-            step = S * 2 ** a
+            step = F(s) * 2 ** a
+            step_d = s * 2.0 ** a
             tot = F(0)
             for t in range(T):
-                xv = F(float(x[t, c]))
-                r = xv / step
-                fl = r.numerator // r.denominator
-                frac = r - fl
-                if abs(frac - F(1, 2)) < F(1, 2 ** 40):
-                    fragile.add((c, a))
-                q = fl + (1 if frac > F(1, 2) or (frac == F(1, 2) and fl % 2 == 1) else 0)
-                q = min(max(q + zp, 0), levels)
-                tot += (xv - (q - zp) * step) ** 2
+                xd = float(x[t, c])
+                q = min(max(round(xd / step_d) + zp, 0), levels)
+                tot += (F(xd) - (q - zp) * step) ** 2
             err[c][a] = tot
-    return err, fragile
+    return err
+
+
+def _exact_argmin(errs):
+    """argmin with ties to the smallest index."""
+    best = 0
+    for a in range(1, len(errs)):
+        if errs[a] < errs[best]:
+            best = a
+    return best
 
 
 def test_ptf_alpha_matches_exact_argmin(orc):
-    """The alpha search against exact rational arithmetic: wherever the exact
-    errors of the best and the runner-up differ by more than 1e-9 relative, the
-    oracle's double sums in 64-row blocks cannot reorder them and its argmin
-    must be the exact one.  T = 150 leaves a partial last block; channel 0 has
-    all its information in that block, channel 1 is all zeros (every alpha
-    exact: the tie goes to alpha = 0)."""
+    """The alpha search against exact rational arithmetic on every channel:
+    the oracle's argmin is the exact argmin (ties to the smallest alpha) and
+    its reported errors are the exact ones rounded to binary64 (one unit in
+    the last place).  Channel 0 holds all its information in its last rows,
+    channel 1 is all zeros (every alpha exact: the tie goes to alpha = 0),
+    channel 4 is an outlier channel."""
     rng = np.random.default_rng(41)
     T, C, K = 150, 12, 3
     x = (rng.standard_normal((T, C)) * np.exp(rng.uniform(np.log(0.05), np.log(2.5), C))).astype(np.float32)
@@ -420,20 +421,68 @@ def test_ptf_alpha_matches_exact_argmin(orc):
     xd = x.astype(np.float64)
     s, zp = orc.ptf_params(xd, b=8, K=K)
     alpha = orc.ptf_alpha(xd, s, zp, b=8, K=K)
-    err, fragile = _exact_ptf_errors(x, s, zp, K)
-    assert alpha[1] == 0
-    checked = 0
+    got_err, got_lo = orc.ptf_alpha_errors(xd, s, zp, b=8, K=K, with_lo=True)
+    err = _exact_ptf_errors(xd, s, zp, K)
+    from fractions import Fraction as F
     for c in range(C):
-        order = sorted(range(K + 1), key=lambda a: (err[c][a], a))
-        best, second = order[0], order[1]
-        if any((c, a) in fragile for a in range(K + 1)):
-            continue
-        gap = err[c][second] - err[c][best]
-        if gap == 0 or gap > 1e-9 * max(err[c][second], 1e-300):
-            assert alpha[c] == best, (c, [float(e) for e in err[c]])
-            checked += 1
-    assert checked >= C - 1
-    assert alpha[0] != 0          # decided by the partial last block alone
+        assert alpha[c] == _exact_argmin(err[c]), (c, [float(e) for e in err[c]])
+        for a in range(K + 1):
+            want = float(err[c][a])
+            assert abs(got_err[c, a] - want) <= np.spacing(want), (c, a, got_err[c, a], want)
+            # hi + lo carries the exact value to about 106 bits
+            assert abs(F(got_err[c, a]) + F(got_lo[c, a]) - err[c][a]) <= err[c][a] * F(1, 2 ** 100)
+    assert alpha[1] == 0 and alpha[4] >= 2
+    assert alpha[0] != 0          # decided by the last rows alone
+
+
+def _near_tie_channel(rng, eps_units, s, n_common=600):
+    """One channel (values in units of s, all exact binary64 with s a power of
+    two) on which alpha = 0 and alpha = 1 of eq. (11) (b = 8, zp = 250, so the
+    grid of alpha = 0 ends at 5 s) have errors that differ by exactly
+    2 eps_units s^2:
+      * common rows (2m + f) s, |f| < 1/2: the same nearest point on both
+        grids, the same residual;
+      * two rows (2m + 1.25) s: residual 0.25 s on the grid s, 0.75 s on 2 s;
+      * one row (6 + eps_units) s above the grid of alpha = 0: clipped to 5 s
+        there (residual (1 + eps) s), residual eps s on the grid 2 s.
+    The two rows cost alpha = 1 exactly s^2 more, the last row costs alpha = 0
+    (1 + eps)^2 s^2 - eps^2 s^2 = (1 + 2 eps) s^2 more: the errors tie for
+    eps = 0 and differ by 2 eps s^2 otherwise."""
+    m = rng.integers(-100, 3, size=n_common)
+    f = rng.choice([-0.375, -0.25, -0.125, 0.125, 0.25, 0.375], size=n_common)
+    vals = list((2 * m + f) * s)
+    vals += [(2 * -7 + 1.25) * s, (2 * 1 + 1.25) * s]
+    vals.append((6.0 + eps_units) * s)
+    return np.array(vals, dtype=np.float64)
+
+
+def test_ptf_alpha_exact_ties_and_near_ties(orc):
+    """eq. (11) evaluated exactly: an exact tie between alpha = 0 and alpha = 1
+    (both errors non-zero) goes to alpha = 0, and errors that differ by a
+    less than one unit in the last place of their binary64 value (a plain
+    binary64 sum of the terms, in row order, reversed or in 64-row blocks,
+    orders them wrongly or ties them) are ordered by their exact values.  The expected alphas come
+    from the construction and are re-derived in Fractions."""
+    s, zp, K = 2.0 ** -7, 250, 1
+    rng = np.random.default_rng(7)
+    # 6 + eps is exact in binary64 for these eps (its unit in the last place is 2^-50)
+    eps = [0.0, 2.0 ** -50, -2.0 ** -50, 2.0 ** -49, -2.0 ** -48]
+    cols = [_near_tie_channel(rng, e, s) for e in eps]
+    x = np.stack(cols, axis=1)
+    alpha = orc.ptf_alpha(x, s, zp, b=8, K=K)
+    want = [0, 1, 0, 1, 0]
+    err = _exact_ptf_errors(x, s, zp, K)
+    for c, e in enumerate(eps):
+        gap = err[c][0] - err[c][1]
+        from fractions import Fraction as F
+        assert gap == 2 * F(e) * F(s) ** 2, (c, gap)
+        assert err[c][0] > 0 and err[c][1] > 0
+        assert _exact_argmin(err[c]) == want[c]
+        if e != 0.0:
+            # below one unit in the last place of the binary64 total: any
+            # rounded sum of the squared residuals sees a tie or the wrong order
+            assert abs(gap) <= np.spacing(float(err[c][0]))
+    assert list(alpha) == want
 
 
 # ---------------------------------------------------------------------------

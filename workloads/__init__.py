@@ -205,6 +205,23 @@ def qk_inputs(G: int, Lq: int, Lk: int, dk: int, d: int, seed: int, sigma: float
     return dict(q=q, k=k, v=v, zp_q=zp_q, zp_k=zp_k, bias=b)
 
 
+def lis_lattice(chunk: int, step: int, jitter: int = 0, seed: int = 0, rows_per_chunk_log8: int = 7):
+    """Rows of 8 keys whose entries run over {0, -1, ..., -7} * step, every
+    combination once (8^8 rows in 8^(8 - rows_per_chunk_log8) chunks; row r of
+    the whole lattice has entry k equal to -digit_k(r) step, digit_k the k-th
+    base-8 digit), optionally plus an integer jitter uniform on
+    [-jitter, jitter] (seeded by seed and chunk).  Returned as int32
+    [rows / 4, 4, 8]: attention units of 4 query rows and 8 keys."""
+    n = 8 ** rows_per_chunk_log8
+    idx = np.arange(chunk * n, (chunk + 1) * n, dtype=np.int64)
+    digits = np.stack([(idx >> (3 * k)) & 7 for k in range(8)], axis=1)
+    rows = -digits * step
+    if jitter:
+        rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, chunk])))
+        rows = rows + rng.integers(-jitter, jitter + 1, size=rows.shape)
+    return rows.astype(np.int32).reshape(n // 4, 4, 8)
+
+
 def config_inputs(cfg: Config, part: str = "all", G: Optional[int] = None,
                   T: Optional[int] = None) -> dict:
     """Inputs of a named config.  ``G`` truncates the attention unit count (the
