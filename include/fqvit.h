@@ -146,6 +146,34 @@ fq_status lis_attn_v_shift(const uint8_t* codes, int32_t ld_codes, const int8_t*
                            int32_t bits, int32_t* out, void* stream);
 
 /*
+ * BitShift Attn x V for codes of any width b in [1, 8], including the 8-bit
+ * attention maps of the paper's 8/8/8 setting (Sec. 3.3; its Table 1).  The
+ * paper does not say how codes wider than 4 bits multiply V: with
+ * N = 2^b - 1 the integer form (V - zp) << (N - code) would need shifts of up
+ * to 255.  This product keeps the fixed output scale s_V / 2^W with
+ * W = min(2^b - 1, 44):
+ *   out[g, i, c] = sum_j floor((v[g, j, c] - zp_v) 2^(W - code[g, i, j])),
+ * which is exact (no floor acts) for every code <= W.  Log-Int-Softmax never
+ * produces a code above 44 for Lk <= 4096 and n <= 30 (round(S / e) stays
+ * below 2^43 + 1), so its products are exact, and below 255 (1.5) 2^44 in
+ * magnitude; for b <= 4 the result is lis_attn_v_shift's widened to int64.
+ * A code above W (not one made by Log-Int-Softmax) contributes the floor of
+ * its shifted value, and a sum that leaves int64 (again only for such codes)
+ * wraps modulo 2^64.
+ *
+ *   codes   [G, Lq, ld_codes] as written by lis_softmax_log4 with the same
+ *           bits: nibbles for b <= 4 (ld_codes >= ceil(Lk/2)), one byte per
+ *           code for b >= 5 (ld_codes >= Lk).
+ *   v       [G, Lk, d] int8, zero point zp_v in [-128, 127].
+ *   out     [G, Lq, d] int64, scale s_V / 2^W.
+ * Errors: FQ_ERR_NULL, FQ_ERR_SHAPE (G or Lq < 0, Lk outside [1, 4096], d
+ * outside [1, 256], ld_codes below the row's bytes), FQ_ERR_PARAM (bits, zp_v).
+ */
+fq_status lis_attn_v_shift_wide(const uint8_t* codes, int32_t ld_codes, const int8_t* v,
+                                int32_t zp_v, int64_t G, int32_t Lq, int32_t Lk, int32_t d,
+                                int32_t bits, int64_t* out, void* stream);
+
+/*
  * Fused Log-Int-Softmax and BitShift Attn x V, the integer-only attention of
  * Sec. 3.3 (the MSA dataflow of its Fig. 4): the same results as
  * lis_softmax_log4 followed by lis_attn_v_shift, with the codes kept on chip.

@@ -66,6 +66,7 @@ _SIGS = {
     "oracle_lis_softmax_log4": [_P, _I64, _I32, _I32, _P, _I32, _F32, _I32, _I32, _P, _I32],
     "oracle_lis_row_exp": [_P, _P, _I32, _F32, _I32, _P, _P],
     "oracle_lis_attn_v_shift": [_P, _I32, _P, _I32, _I64, _I32, _I32, _I32, _I32, _P],
+    "oracle_lis_attn_v_shift_wide": [_P, _I32, _P, _I32, _I64, _I32, _I32, _I32, _I32, _P],
     "oracle_lis_attention_head": [_P, _P, _I32, _I64, _I32, _I32, _F32, _I32, _I32, _P, _I32,
                                   _I32, _P, _P, _I32],
     "oracle_requant_dyadic_int8": [_P, _I64, _F32, _F32, _I32, _I32, _P],
@@ -261,6 +262,20 @@ def lis_attn_v_shift(codes, v, zp_v=0, bits=4, Lk=None) -> np.ndarray:
     out = np.empty((G, Lq, d), dtype=np.int32)
     _check(lib().oracle_lis_attn_v_shift(_ptr(codes), ld, _ptr(v), zp_v, G, Lq, Lk, d, bits,
                                          _ptr(out)), "lis_attn_v_shift")
+    return out
+
+
+def lis_attn_v_shift_wide(codes, v, zp_v=0, bits=8, Lk=None) -> np.ndarray:
+    """int64 [G, Lq, d] product at scale s_V / 2^min(2^bits - 1, 44)."""
+    codes = np.ascontiguousarray(codes, dtype=np.uint8)
+    v = np.ascontiguousarray(v, dtype=np.int8)
+    G, Lk_v, d = v.shape
+    Lk = Lk_v if Lk is None else Lk
+    Gc, Lq, ld = codes.shape
+    assert Gc == G
+    out = np.empty((G, Lq, d), dtype=np.int64)
+    _check(lib().oracle_lis_attn_v_shift_wide(_ptr(codes), ld, _ptr(v), zp_v, G, Lq, Lk, d, bits,
+                                              _ptr(out)), "lis_attn_v_shift_wide")
     return out
 
 

@@ -633,6 +633,54 @@ int oracle_lis_attn_v_shift(const uint8_t* codes, int32_t ld_codes, const int8_t
     return rc;
 }
 
+/* BitShift Attn x V for codes of any width b in [1, 8] (READING: the paper
+ * does not say how codes wider than 4 bits multiply V; with N = 2^b - 1 the
+ * integer form (V - zp) << (N - code) would need shifts of up to 255).  The
+ * product is kept at the fixed output scale s_V / 2^W, W = min(2^b - 1, 44):
+ *     out[g,i,c] = sum_j floor((v[g,j,c] - zp_v) 2^(W - code[g,i,j])),
+ * exact (no floor acts) for every code <= W.  W = 44 covers every code
+ * Log-Int-Softmax can produce for Lk <= 4096 and n <= 30: the row sum is at
+ * most Lk (q_b^2 + q_c) 2^n, every I-Exp value is at least
+ * min(q_b^2 + q_c, 2 ((q_b + q_ln2 + 1)^2 + q_c)) > (q_b^2 + q_c) / 2, so
+ * round(S / e) < 2^43 + 1 and I-Log2 of it is at most 44.  Those products are
+ * below 255 (1.5) 2^44 < 2^53 in magnitude (sum_j 2^-code_j < 1.5 without a
+ * clip).  A code above W (only from codes not made by Log-Int-Softmax)
+ * contributes the floor of its right shift; a sum that leaves int64 (again
+ * only for such codes) wraps modulo 2^64.  For b <= 4 this is
+ * oracle_lis_attn_v_shift widened to int64.  Codes are stored as
+ * oracle_lis_softmax_log4 writes them (nibbles for b <= 4, bytes above). */
+int oracle_lis_attn_v_shift_wide(const uint8_t* codes, int32_t ld_codes, const int8_t* v,
+                                 int32_t zp_v, int64_t G, int32_t Lq, int32_t Lk, int32_t d,
+                                 int32_t bits, int64_t* out) {
+    if (G < 0 || Lq < 0 || Lk < 1 || d < 1 || bits < 1 || bits > 8 ||
+        ld_codes < codes_row_bytes(Lk, bits) || zp_v < -128 || zp_v > 127)
+        return ORACLE_ERR_ARG;
+    if (G == 0 || Lq == 0) return ORACLE_OK;
+    if (!codes || !v || !out) return ORACLE_ERR_ARG;
+    const int32_t N = (1 << bits) - 1;
+    const int32_t W = N < 44 ? N : 44;
+    for (int64_t g = 0; g < G; ++g) {
+        for (int32_t i = 0; i < Lq; ++i) {
+            const uint8_t* crow = codes + (g * Lq + i) * (int64_t)ld_codes;
+            for (int32_t c = 0; c < d; ++c) {
+                uint64_t acc = 0;      /* two's complement sum, modulo 2^64 */
+                for (int32_t j = 0; j < Lk; ++j) {
+                    int32_t attn_q;
+                    if (bits <= 4) attn_q = (j % 2 == 0) ? (crow[j / 2] & 15) : (crow[j / 2] >> 4);
+                    else attn_q = crow[j];
+                    const int64_t vq = (int64_t)v[(g * Lk + j) * (int64_t)d + c] - zp_v;
+                    int64_t term;
+                    if (attn_q <= W) term = vq * ((int64_t)1 << (W - attn_q));
+                    else term = floor_div(vq, (int64_t)1 << (attn_q - W < 62 ? attn_q - W : 62));
+                    acc += (uint64_t)term;
+                }
+                out[(g * Lq + i) * (int64_t)d + c] = (int64_t)acc;
+            }
+        }
+    }
+    return ORACLE_OK;
+}
+
 int oracle_lis_attention_head(const int32_t* logits, const int32_t* bias, int32_t Hb,
                               int64_t G, int32_t Lq, int32_t Lk, float s_logit, int32_t bits,
                               int32_t exp_n, const int8_t* v, int32_t zp_v, int32_t d,

@@ -123,6 +123,15 @@ int oracle_lis_attn_v_shift(const uint8_t* codes, int32_t ld_codes, const int8_t
                             int32_t zp_v, int64_t G, int32_t Lq, int32_t Lk, int32_t d,
                             int32_t bits, int32_t* out);
 
+/* The same product for codes of any width b in [1, 8], as int64 at the output
+ * scale s_V / 2^W, W = min(2^b - 1, 44): out = sum_j floor((v - zp_v)
+ * 2^(W - code)), exact for codes <= W (every code Log-Int-Softmax produces);
+ * modulo 2^64 if a sum leaves int64 (never for those codes).
+ * codes: nibbles for b <= 4, one byte per code above. */
+int oracle_lis_attn_v_shift_wide(const uint8_t* codes, int32_t ld_codes, const int8_t* v,
+                                 int32_t zp_v, int64_t G, int32_t Lq, int32_t Lk, int32_t d,
+                                 int32_t bits, int64_t* out);
+
 /* Log-Int-Softmax followed by BitShift Attn x V. codes_out is nullable. */
 int oracle_lis_attention_head(const int32_t* logits, const int32_t* bias, int32_t Hb,
                               int64_t G, int32_t Lq, int32_t Lk, float s_logit, int32_t bits,

@@ -24,6 +24,7 @@ SIGNATURES = {
     "ptf_layernorm_int8": [_P, _I64, _I32, _I32, _P, _I32, _P, _P, _F32, _I32, _I32, _P, _P],
     "lis_softmax_log4": [_P, _I64, _I32, _I32, _P, _I32, _F32, _I32, _I32, _P, _I32, _P],
     "lis_attn_v_shift": [_P, _I32, _P, _I32, _I64, _I32, _I32, _I32, _I32, _P, _P],
+    "lis_attn_v_shift_wide": [_P, _I32, _P, _I32, _I64, _I32, _I32, _I32, _I32, _P, _P],
     "lis_attention_head": [_P, _P, _I32, _I64, _I32, _I32, _F32, _I32, _I32, _P, _I32, _I32, _P,
                            _P, _I32, _P],
     "lis_attention_qk": [_P, _P, _I32, _I32, _I32, _P, _I32, _I64, _I32, _I32, _F32, _I32, _I32,
@@ -207,6 +208,24 @@ def lis_attn_v_shift(codes, v, Lk: int, zp_v: int = 0, bits: int = 4, out=None, 
     args = (_dev_ptr(codes, torch.uint8, "codes", 3), ld, _dev_ptr(v, torch.int8, "v", 3), zp_v,
             G, Lq, Lk, d, bits, _dev_ptr(out, torch.int32, "out", 3), _stream(stream, v))
     return _invoke("lis_attn_v_shift", args, (codes, v, out), prepare, out)
+
+
+def lis_attn_v_shift_wide(codes, v, Lk: int, zp_v: int = 0, bits: int = 8, out=None, stream=None,
+                          prepare: bool = False):
+    """BitShift Attn x V for codes of any width b in [1, 8] (nibbles for b <= 4,
+    bytes above): int64 [G, Lq, d] at scale s_V / 2^min(2^b - 1, 44)."""
+    import torch
+    G, Lq, ld = codes.shape
+    d = v.shape[2]
+    if v.dim() != 3 or v.shape[:2] != (G, Lk):
+        raise ValueError("v must be [G, Lk, d]")
+    if out is None:
+        out = torch.empty((G, Lq, d), dtype=torch.int64, device=v.device)
+    if out.shape != (G, Lq, d):
+        raise ValueError("out must be [G, Lq, d]")
+    args = (_dev_ptr(codes, torch.uint8, "codes", 3), ld, _dev_ptr(v, torch.int8, "v", 3), zp_v,
+            G, Lq, Lk, d, bits, _dev_ptr(out, torch.int64, "out", 3), _stream(stream, v))
+    return _invoke("lis_attn_v_shift_wide", args, (codes, v, out), prepare, out)
 
 
 def lis_attention_head(logits, v, s_logit: float, bits: int = 4, exp_n: int = 20, zp_v: int = 0,

@@ -167,6 +167,22 @@ fq_status lis_attn_v_shift(const uint8_t* codes, int32_t ld_codes, const int8_t*
     return from_hip(fqvit::launch_attn_v_shift(a, (hipStream_t)stream));
 }
 
+fq_status lis_attn_v_shift_wide(const uint8_t* codes, int32_t ld_codes, const int8_t* v,
+                                int32_t zp_v, int64_t G, int32_t Lq, int32_t Lk, int32_t d,
+                                int32_t bits, int64_t* out, void* stream) {
+    ConsumeEvents consume;
+    const int32_t row_bytes = (bits >= 5 && bits <= 8) ? Lk : (Lk + 1) / 2;
+    if (G < 0 || Lq < 0 || Lk < 1 || Lk > kMaxLk || d < 1 || d > kMaxD || ld_codes < row_bytes ||
+        !grid_fits(G, Lq, 16))
+        return FQ_ERR_SHAPE;
+    if (bits < 1 || bits > 8 || zp_v < -128 || zp_v > 127) return FQ_ERR_PARAM;
+    if (G == 0 || Lq == 0) return FQ_OK;
+    if (!codes || !v || !out) return FQ_ERR_NULL;
+    const int32_t N = (1 << bits) - 1;
+    fqvit::AvWideArgs a{codes, ld_codes, v, zp_v, G, Lq, Lk, d, bits, N < 44 ? N : 44, out};
+    return from_hip(fqvit::launch_attn_v_shift_wide(a, (hipStream_t)stream));
+}
+
 fq_status lis_attention_head(const int32_t* logits, const int32_t* bias, int32_t Hb,
                              int64_t G, int32_t Lq, int32_t Lk, float s_logit, int32_t bits,
                              int32_t exp_n, const int8_t* v, int32_t zp_v, int32_t d,

@@ -105,6 +105,21 @@ struct AvArgs {
 
 hipError_t launch_attn_v_shift(const AvArgs& a, hipStream_t stream);
 
+// BitShift product for codes of any width: int64 output at scale s_V / 2^W.
+struct AvWideArgs {
+    const uint8_t* codes;
+    int32_t ld_codes;
+    const int8_t* v;
+    int32_t zp_v;
+    int64_t G;
+    int32_t Lq, Lk, d;
+    int32_t bits;           // code width: nibbles for <= 4, bytes above
+    int32_t W;              // output exponent min(2^bits - 1, 44)
+    int64_t* out;
+};
+
+hipError_t launch_attn_v_shift_wide(const AvWideArgs& a, hipStream_t stream);
+
 // ---------------------------------------------------------------------------
 // PTF calibration / quantization and dyadic requantization
 // ---------------------------------------------------------------------------

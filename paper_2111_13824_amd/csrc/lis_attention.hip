@@ -222,6 +222,87 @@ __global__ __launch_bounds__(kBlock) void attn_v_shift_kernel(AvArgs a, int tpr,
     }
 }
 
+// The same product for codes of any width b (bytes for b >= 5) at the output
+// scale s_V / 2^W, W = min(2^b - 1, 44): each term is (V - zp_V) 2^(W - code),
+// exact in int64, or for a code above W (never one from Log-Int-Softmax) the
+// arithmetic right shift of V - zp_V by code - W, i.e. its floor.  Sums are
+// accumulated modulo 2^64.  Layout and staging as attn_v_shift_kernel, with
+// the codes themselves staged as bytes.
+__global__ __launch_bounds__(kBlock) void attn_v_shift_wide_kernel(AvWideArgs a, int tpr, int rows,
+                                                                   int ntiles, int kb) {
+    extern __shared__ int16_t lds16[];
+    const int dpad = 16 * tpr;
+    int16_t* sv = lds16;                                            // [kb][dpad]
+    uint8_t* scode = reinterpret_cast<uint8_t*>(lds16 + kb * dpad); // [rows][kb]
+    const int64_t total = a.G * (int64_t)ntiles;
+    const int64_t lb = xcd_remap(blockIdx.x, total);
+    const int64_t g = lb / ntiles;
+    const int tile = (int)(lb - g * ntiles);
+    const int row_local = threadIdx.x / tpr;
+    const int cgrp = threadIdx.x - row_local * tpr;
+    const int irow = tile * rows + row_local;
+    const int Lk = a.Lk;
+
+    uint64_t acc[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) acc[q] = 0;
+
+    for (int k0 = 0; k0 < Lk; k0 += kb) {
+        const int kc = min(kb, Lk - k0);
+        __syncthreads();
+        for (int idx = threadIdx.x; idx < kb * dpad; idx += blockDim.x) {
+            const int jj = idx / dpad;
+            const int dd = idx - jj * dpad;
+            const int j = k0 + jj;
+            sv[idx] = (jj < kc && dd < a.d) ? (int16_t)((int)a.v[(g * Lk + j) * (int64_t)a.d + dd] - a.zp_v)
+                                            : (int16_t)0;
+        }
+        for (int idx = threadIdx.x; idx < rows * kb; idx += blockDim.x) {
+            const int rl = idx / kb;
+            const int jj = idx - rl * kb;
+            const int ir = tile * rows + rl;
+            const int j = k0 + jj;
+            int code = a.W;     // padding keys: any code (their V is 0)
+            if (ir < a.Lq && jj < kc) {
+                const uint8_t* crow = a.codes + (g * a.Lq + ir) * (int64_t)a.ld_codes;
+                if (a.bits <= 4) {
+                    const uint8_t byte = crow[j >> 1];
+                    code = (j & 1) ? (byte >> 4) : (byte & 15);
+                } else {
+                    code = crow[j];
+                }
+            }
+            scode[idx] = (uint8_t)code;
+        }
+        __syncthreads();
+        if (irow < a.Lq) {
+            const int16_t* vbase = sv + 16 * cgrp;
+            const uint8_t* srow = scode + row_local * kb;
+            for (int jj = 0; jj < kc; ++jj) {
+                const int code = srow[jj];
+                const int16_t* vr = vbase + jj * dpad;
+                if (code <= a.W) {
+                    const int sh = a.W - code;
+#pragma unroll
+                    for (int q = 0; q < 16; ++q) acc[q] += (uint64_t)(int64_t)vr[q] << sh;
+                } else {
+                    const int sh = min(code - a.W, 63);
+#pragma unroll
+                    for (int q = 0; q < 16; ++q) acc[q] += (uint64_t)((int64_t)vr[q] >> sh);
+                }
+            }
+        }
+    }
+    if (irow < a.Lq) {
+        int64_t* orow = a.out + (g * a.Lq + irow) * (int64_t)a.d;
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+            const int col = 16 * cgrp + q;
+            if (col < a.d) orow[col] = (int64_t)acc[q];
+        }
+    }
+}
+
 }  // namespace lis
 
 namespace {
@@ -312,6 +393,23 @@ hipError_t launch_attn_v_shift(const AvArgs& a, hipStream_t stream) {
     const int64_t blocks = a.G * (int64_t)ntiles;
     launch_kernel(lis::attn_v_shift_kernel, dim3((unsigned)blocks), dim3(kBlock), lds, stream, a,
                        tpr, rows, ntiles, kb);
+    return hipGetLastError();
+}
+
+hipError_t launch_attn_v_shift_wide(const AvWideArgs& a, hipStream_t stream) {
+    using lis::kBlock;
+    int tpr = 1;
+    while (16 * tpr < a.d) tpr <<= 1;          // threads per row, 16 columns each
+    const int rows = kBlock / tpr;
+    const int ntiles = (a.Lq + rows - 1) / rows;
+    const int dpad = 16 * tpr;
+    // LDS: kb * dpad int16 + rows * kb bytes <= 32 KB
+    int kb = 32768 / (2 * dpad + rows);
+    kb = std::max(16, std::min(kb, 256));
+    const size_t lds = (size_t)kb * dpad * sizeof(int16_t) + (size_t)rows * kb;
+    const int64_t blocks = a.G * (int64_t)ntiles;
+    launch_kernel(lis::attn_v_shift_wide_kernel, dim3((unsigned)blocks), dim3(kBlock), lds, stream,
+                  a, tpr, rows, ntiles, kb);
     return hipGetLastError();
 }
 

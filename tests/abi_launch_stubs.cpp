@@ -16,6 +16,7 @@ hipError_t launch_lis_qk(const LisArgs&, const QkInput&, hipStream_t) {
     return hipSuccess;
 }
 hipError_t launch_attn_v_shift(const AvArgs&, hipStream_t) { ++g_launches; return hipSuccess; }
+hipError_t launch_attn_v_shift_wide(const AvWideArgs&, hipStream_t) { ++g_launches; return hipSuccess; }
 hipError_t launch_ptf_calibrate(const PtfCalibArgs&, hipStream_t) { ++g_launches; return hipSuccess; }
 hipError_t launch_ptf_quantize(const PtfQuantArgs&, hipStream_t) { ++g_launches; return hipSuccess; }
 hipError_t launch_requant(const RequantArgs&, hipStream_t) { ++g_launches; return hipSuccess; }

@@ -47,7 +47,8 @@ def test_header_symbols_exported(lib):
     assert set(names) >= {"ptf_layernorm_int8", "lis_softmax_log4", "lis_attn_v_shift",
                           "lis_attention_head", "fq_status_str", "fq_version",
                           "fq_time_next_call", "ptf_calibrate", "fq_ptf_calibrate_workspace_bytes",
-                          "ptf_quantize_int8", "requant_dyadic_int8", "lis_attention_qk"}
+                          "ptf_quantize_int8", "requant_dyadic_int8", "lis_attention_qk",
+                          "lis_attn_v_shift_wide"}
     for n in names:
         assert hasattr(lib, n), f"{n} declared in fqvit.h but not exported"
     # the binding exposes the compute entry points under the same names
@@ -157,6 +158,30 @@ def test_attn_v_validation(lib):
     assert call(out=NULL) == B.FQ_ERR_NULL
     assert call(v=NULL) == B.FQ_ERR_NULL
     assert call(G=0, codes=NULL, v=NULL, out=NULL) == B.FQ_OK
+
+
+def test_attn_v_wide_validation(lib):
+    f = lib.lis_attn_v_shift_wide
+    args = dict(c=1, ld=7, v=1, zp=0, G=2, Lq=5, Lk=7, d=64, bits=8, out=1)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return f(a["c"], a["ld"], a["v"], a["zp"], a["G"], a["Lq"], a["Lk"], a["d"], a["bits"],
+                 a["out"], NULL)
+
+    assert call(G=-1) == B.FQ_ERR_SHAPE
+    assert call(Lk=0) == B.FQ_ERR_SHAPE
+    assert call(Lk=4097, ld=4097) == B.FQ_ERR_SHAPE
+    assert call(d=0) == B.FQ_ERR_SHAPE
+    assert call(d=257) == B.FQ_ERR_SHAPE
+    assert call(ld=6) == B.FQ_ERR_SHAPE              # one byte per code at 8 bits
+    assert call(bits=4, ld=3) == B.FQ_ERR_SHAPE      # nibbles: ceil(7 / 2) = 4 bytes
+    assert call(bits=0) == B.FQ_ERR_PARAM
+    assert call(bits=9) == B.FQ_ERR_PARAM
+    assert call(zp=128) == B.FQ_ERR_PARAM
+    for k in ("c", "v", "out"):
+        assert call(**{k: None}) == B.FQ_ERR_NULL
+    assert call(G=0, c=None, v=None, out=None) == B.FQ_OK
 
 
 def test_head_validation(lib):
@@ -309,6 +334,8 @@ def test_valid_calls_reach_exactly_one_launch(lib):
     assert launches(lib.lis_softmax_log4, 1, 2, 5, 7, None, 0, f32(0.001), 4, 20, 1, 4, None) == (0, 1)
     assert launches(lib.lis_softmax_log4, 1, 2, 5, 7, None, 0, f32(0.001), 4, 20, 1, 3, None)[1] == 0
     assert launches(lib.lis_attn_v_shift, 1, 4, 1, 0, 2, 5, 7, 64, 4, 1, None) == (0, 1)
+    assert launches(lib.lis_attn_v_shift_wide, 1, 7, 1, 0, 2, 5, 7, 64, 8, 1, None) == (0, 1)
+    assert launches(lib.lis_attn_v_shift_wide, 1, 4, 1, 0, 2, 5, 7, 64, 4, 1, None) == (0, 1)
     assert launches(lib.lis_attention_head, 1, None, 0, 2, 5, 7, f32(0.001), 4, 20, 1, 0, 64, 1,
                     None, 0, None) == (0, 1)
     assert launches(lib.lis_attention_qk, 16, 16, 0, 0, 64, None, 0, 2, 5, 7, f32(0.001), 4, 20,

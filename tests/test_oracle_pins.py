@@ -332,6 +332,88 @@ def test_head_is_lis_then_attn_v(orc):
 
 
 # ---------------------------------------------------------------------------
+# BitShift Attn x V for wide codes (b in [5, 8])
+# ---------------------------------------------------------------------------
+
+def _pack(codes, bits):
+    """[..., Lk] codes -> stored form: nibbles (even key low) for bits <= 4, bytes above."""
+    if bits > 4:
+        return np.ascontiguousarray(codes.astype(np.uint8))
+    Lk = codes.shape[-1]
+    ld = (Lk + 1) // 2
+    packed = np.zeros(codes.shape[:-1] + (ld,), dtype=np.uint8)
+    for j in range(Lk):
+        packed[..., j // 2] |= (codes[..., j] << (4 * (j % 2))).astype(np.uint8)
+    return packed
+
+
+def _wide_w(bits):
+    return min(2 ** bits - 1, 44)
+
+
+def test_attn_v_wide_equals_narrow_for_4_bits_or_less(orc):
+    rng = np.random.default_rng(61)
+    for bits in (1, 2, 3, 4):
+        codes = rng.integers(0, 2 ** bits, size=(3, 7, 33))
+        v = rng.integers(-128, 128, size=(3, 33, 20)).astype(np.int8)
+        pk = _pack(codes, bits)
+        narrow = orc.lis_attn_v_shift(pk, v, zp_v=5, bits=bits, Lk=33).astype(np.int64)
+        assert np.array_equal(orc.lis_attn_v_shift_wide(pk, v, zp_v=5, bits=bits, Lk=33), narrow)
+
+
+@pytest.mark.parametrize("bits", [5, 6, 8])
+def test_attn_v_wide_single_element_exhaustive(orc, bits):
+    """One key, one column: every code the storage holds (0 .. 2^b - 1) times
+    every byte value and three zero points, against the floor of the exact
+    product (v - zp) 2^(W - code) in Python integers (>> floors)."""
+    W = _wide_w(bits)
+    codes = np.arange(2 ** bits)
+    vals = np.arange(-128, 128)
+    for zp in (0, -7, 127):
+        cc = np.repeat(codes, vals.size).reshape(1, -1, 1)          # rows = (code, v) pairs
+        vv = np.tile(vals, codes.size)
+        # unit g = pair: 1 query row, 1 key, 1 column
+        G = cc.shape[1]
+        got = orc.lis_attn_v_shift_wide(_pack(cc.reshape(G, 1, 1), bits),
+                                        vv.astype(np.int8).reshape(G, 1, 1), zp_v=zp, bits=bits, Lk=1)
+        want = [((int(v) - zp) << (W - int(c))) if c <= W else ((int(v) - zp) >> (int(c) - W))
+                for c, v in zip(cc.ravel(), vv)]
+        assert np.array_equal(got.ravel(), np.array(want, dtype=np.int64)), (bits, zp)
+
+
+def test_attn_v_wide_on_lis_codes_is_exact(orc):
+    """8-bit Log-Int-Softmax codes of spread rows never exceed W = 44, and the
+    product is then the integer matrix product P (V - zp) with
+    P = 2^(44 - code) (numpy int64, a textbook routine); the row sums of
+    2^-code stay below 1.5 (no clip acts at 8 bits)."""
+    for s, n, sigma in ((2.0 ** -10, 20, 9.0), (2e-4, 30, 9.0), (0.05, 30, 60.0)):
+        a = W.attn_inputs(3, 20, 577, 48, seed=17, sigma=(sigma,), s_logit=s, v_lo=-128, v_hi=127)
+        pk = orc.lis_softmax_log4(a["logits"], s, bits=8, exp_n=n)
+        codes = pk[..., :577].astype(np.int64)
+        assert codes.max() <= 44 and codes.max() > 15
+        assert np.sum(np.ldexp(1.0, -codes), axis=-1).max() < 1.5
+        got = orc.lis_attn_v_shift_wide(pk, a["v"], zp_v=-3, bits=8, Lk=577)
+        P = np.left_shift(np.int64(1), 44 - codes)
+        ref = np.matmul(P, a["v"].astype(np.int64) + 3)
+        assert np.array_equal(got, ref), (s, n)
+
+
+def test_lis_code_bound_44_at_extreme_parameters(orc):
+    """The largest codes Log-Int-Softmax produces within the accepted
+    parameters: Lk = 4096 keys, all at the maximum but one far below it.  That
+    key is clamped (z = n, p = 0), so its I-Exp value equals q_b^2 + q_c while
+    every other key has (q_b^2 + q_c) 2^n: round(S / e) = 4095 2^n exactly,
+    whose leading one is bit n + 11 with the bit below it set, so its code is
+    n + 12 (42 at n = 30, the deepest clamp, with s = 0.5, the coarsest scale;
+    32 at n = 20).  Both stay within the wide product's exponent W = 44."""
+    for s, n in ((0.5, 30), (2.0 ** -10, 20), (1e-3, 25)):
+        lg = np.zeros((1, 1, 4096), dtype=np.int32)
+        lg[0, 0, 0] = -(2 ** 29)
+        pk = orc.lis_softmax_log4(lg, s, bits=8, exp_n=n)
+        assert int(pk[0, 0, 0]) == n + 12 <= 44, (s, n, int(pk[0, 0, 0]))
+
+
+# ---------------------------------------------------------------------------
 # PTF quantizer (Sec. 3.2)
 # ---------------------------------------------------------------------------
 

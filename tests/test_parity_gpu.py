@@ -268,6 +268,63 @@ def test_attn_v_shift_any_codes(fq, orc):
         assert np.array_equal(got, orc.lis_attn_v_shift(codes, v, zp_v=-3, bits=bits, Lk=65))
 
 
+def _stored_codes(codes, bits):
+    """[..., Lk] codes -> stored form (nibbles for bits <= 4, bytes above)."""
+    if bits > 4:
+        return np.ascontiguousarray(codes.astype(np.uint8))
+    Lk = codes.shape[-1]
+    packed = np.zeros(codes.shape[:-1] + ((Lk + 1) // 2,), dtype=np.uint8)
+    for j in range(Lk):
+        packed[..., j // 2] |= (codes[..., j] << (4 * (j % 2))).astype(np.uint8)
+    return packed
+
+
+@pytest.mark.parametrize("G,Lq,Lk,d,bits", [(2, 5, 1, 64, 8), (3, 17, 33, 16, 8), (2, 64, 197, 64, 8),
+                                            (2, 70, 197, 17, 6), (1, 9, 577, 64, 8), (4, 49, 49, 32, 5),
+                                            (1, 3, 700, 256, 8), (2, 20, 96, 100, 7),
+                                            (2, 33, 65, 48, 4), (2, 30, 40, 8, 2)])
+def test_attn_v_shift_wide(fq, orc, G, Lq, Lk, d, bits):
+    """The wide BitShift product on Log-Int-Softmax codes of b bits (spread rows,
+    so that 8-bit codes pass 15) and on arbitrary codes of every stored value,
+    above the output exponent W = min(2^b - 1, 44) too (the floor path)."""
+    say("av wide", G, Lq, Lk, d, bits)
+    rng = np.random.default_rng(G * Lk + d + bits)
+    a = W.attn_inputs(G, Lq, Lk, d, seed=13, sigma=(9.0,), s_logit=2e-4, v_lo=-128, v_hi=127)
+    lis = orc.lis_softmax_log4(a["logits"], 2e-4, bits=bits, exp_n=30) if Lk > 1 else None
+    anyc = _stored_codes(rng.integers(0, 2 ** bits, size=(G, Lq, Lk)), bits)
+    for codes in ([lis] if lis is not None else []) + [anyc]:
+        got = host(fq.lis_attn_v_shift_wide(dev(codes), dev(a["v"]), Lk, zp_v=-5, bits=bits))
+        assert got.dtype == np.int64
+        assert np.array_equal(got, orc.lis_attn_v_shift_wide(codes, a["v"], zp_v=-5, bits=bits, Lk=Lk))
+
+
+def test_attention_888_full_vit_base(fq, orc):
+    """The 8/8/8 attention of the ViT-B/16 batch-64 workload: 8-bit
+    Log-Int-Softmax codes on the GPU, then the wide BitShift product, against
+    the same chain in the oracle (every unit; oracle split over host threads)."""
+    import concurrent.futures as cf
+    import os
+    say("attention 8/8/8 full vit_b")
+    cfg = W.BY_NAME["vit_base16_224_b64"]
+    a = W.config_inputs(cfg, "attn")["attn"]
+    codes = fq.lis_softmax_log4(dev(a["logits"]), a["s_logit"], bits=8, exp_n=a["exp_n"])
+    out = host(fq.lis_attn_v_shift_wide(codes, dev(a["v"]), cfg.Lk, zp_v=a["zp_v"], bits=8))
+    got_codes = host(codes)
+    G = cfg.G
+    bounds = np.linspace(0, G, 65).astype(int)
+
+    def run(k):
+        g0, g1 = bounds[k], bounds[k + 1]
+        c = orc.lis_softmax_log4(a["logits"][g0:g1], a["s_logit"], bits=8, exp_n=a["exp_n"])
+        return c, orc.lis_attn_v_shift_wide(c, a["v"][g0:g1], zp_v=a["zp_v"], bits=8)
+
+    with cf.ThreadPoolExecutor(max(1, min(16, os.cpu_count() or 1))) as ex:
+        parts = list(ex.map(run, range(64)))
+    assert np.array_equal(got_codes, np.concatenate([p[0] for p in parts]))
+    assert got_codes.max() > 15
+    assert np.array_equal(out, np.concatenate([p[1] for p in parts]))
+
+
 # (2, 40, 288, 64) and (2, 33, 270, 32): the longest rows of the fused tile
 # kernels (9 chunks of 32 keys); (2, 40, 290, 64): the shortest that takes the
 # stream kernel, with (2, 40, 350, 64), (2, 33, 384, 32) and (2, 40, 400, 64)
