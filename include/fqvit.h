@@ -39,7 +39,8 @@ typedef enum fq_status {
     FQ_ERR_SHAPE = 2,     /* a size is out of the supported range                    */
     FQ_ERR_PARAM = 3,     /* a scalar parameter is out of range                      */
     FQ_ERR_HEADROOM = 4,  /* the exact integer sums could overflow 64 bits           */
-    FQ_ERR_HIP = 5        /* the HIP runtime rejected a launch                       */
+    FQ_ERR_HIP = 5,       /* the HIP runtime rejected a launch                       */
+    FQ_ERR_SCRATCH = 6    /* the call needs more than the fixed device scratch holds */
 } fq_status;
 
 /* Static, human-readable name of a status code (never NULL). */
@@ -245,6 +246,27 @@ size_t fq_ptf_calibrate_workspace_bytes(int64_t T, int32_t C, int32_t K);
 fq_status ptf_calibrate(const float* x, int64_t T, int32_t C, int32_t bits, int32_t K, double* s,
                         int32_t* zp, uint8_t* alpha, void* workspace, size_t workspace_bytes,
                         void* stream);
+
+/*
+ * ptf_calibrate for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation): the
+ * same kernels and results, with the workspace taken from a fixed device
+ * array of FQ_NOALLOC_SCRATCH_BYTES that the library holds on each GPU it runs
+ * on until the process ends.  This call allocates nothing (no hipMalloc, no
+ * hipFree, no allocating library routine); on its first call on a device it
+ * looks up that device's copy of the array (hipGetSymbolAddress).
+ *   x, T, C, bits, K, s, zp, alpha: as ptf_calibrate.
+ * Every call on one GPU shares that GPU's array, so calls that overlap on one
+ * GPU (different streams, or host threads, without ordering between them)
+ * race and give undefined results; calls ordered on one stream are safe.  The
+ * array's contents on entry do not matter.
+ * Errors: as ptf_calibrate, and FQ_ERR_SCRATCH when
+ * fq_ptf_calibrate_workspace_bytes(T, C, K) exceeds FQ_NOALLOC_SCRATCH_BYTES
+ * (nothing enqueued); FQ_ERR_HIP if the array cannot be looked up.
+ */
+#define FQ_NOALLOC_SCRATCH_BYTES ((size_t)8 << 20)
+fq_status ptf_calibrate_noalloc(const float* x, int64_t T, int32_t C, int32_t bits, int32_t K,
+                                double* s, int32_t* zp, uint8_t* alpha, void* stream);
 
 /*
  * PTF quantizer (Sec. 3.2, eq. 8): X_Q = clip(rint(x / (2^alpha_c s)) + zp,

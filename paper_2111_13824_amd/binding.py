@@ -15,7 +15,10 @@ from typing import Optional
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libfqvit.so")
 
-FQ_OK, FQ_ERR_NULL, FQ_ERR_SHAPE, FQ_ERR_PARAM, FQ_ERR_HEADROOM, FQ_ERR_HIP = range(6)
+(FQ_OK, FQ_ERR_NULL, FQ_ERR_SHAPE, FQ_ERR_PARAM, FQ_ERR_HEADROOM, FQ_ERR_HIP,
+ FQ_ERR_SCRATCH) = range(7)
+# Bytes of the library's fixed device scratch (FQ_NOALLOC_SCRATCH_BYTES).
+NOALLOC_SCRATCH_BYTES = 8 << 20
 
 # Entry points declared in include/fqvit.h and their C argument types.
 _P = ctypes.c_void_p
@@ -30,6 +33,7 @@ SIGNATURES = {
     "lis_attention_qk": [_P, _P, _I32, _I32, _I32, _P, _I32, _I64, _I32, _I32, _F32, _I32, _I32,
                          _P, _I32, _I32, _P, _P],
     "ptf_calibrate": [_P, _I64, _I32, _I32, _I32, _P, _P, _P, _P, ctypes.c_size_t, _P],
+    "ptf_calibrate_noalloc": [_P, _I64, _I32, _I32, _I32, _P, _P, _P, _P],
     "ptf_quantize_int8": [_P, _I64, _I32, _P, _P, _P, _I32, _P, _P],
     "requant_dyadic_int8": [_P, _I64, _F32, _F32, _I32, _I32, _P, _P],
 }
@@ -281,6 +285,23 @@ def ptf_calibrate(x, bits: int = 8, K: int = 3, s=None, zp=None, alpha=None, wor
             _dev_ptr(alpha, torch.uint8, "alpha", 1), _dev_ptr(workspace, torch.uint8, "workspace", 1),
             workspace.numel(), _stream(stream, x))
     return _invoke("ptf_calibrate", args, (x, s, zp, alpha, workspace), prepare, (s, zp, alpha))
+
+
+def ptf_calibrate_noalloc(x, bits: int = 8, K: int = 3, s=None, zp=None, alpha=None,
+                          stream=None, prepare: bool = False):
+    """ptf_calibrate with the workspace in the library's fixed device scratch:
+    the entry point allocates nothing (outputs not given are allocated here,
+    by torch, before the call)."""
+    import torch
+    T, C = x.shape
+    dev = x.device
+    s = torch.empty(1, dtype=torch.float64, device=dev) if s is None else s
+    zp = torch.empty(1, dtype=torch.int32, device=dev) if zp is None else zp
+    alpha = torch.empty(C, dtype=torch.uint8, device=dev) if alpha is None else alpha
+    args = (_dev_ptr(x, torch.float32, "x", 2), T, C, bits, K,
+            _dev_ptr(s, torch.float64, "s", 1), _dev_ptr(zp, torch.int32, "zp", 1),
+            _dev_ptr(alpha, torch.uint8, "alpha", 1), _stream(stream, x))
+    return _invoke("ptf_calibrate_noalloc", args, (x, s, zp, alpha), prepare, (s, zp, alpha))
 
 
 def ptf_quantize_int8(x, s, zp, alpha, bits: int = 8, x_q=None, stream=None,

@@ -98,6 +98,8 @@ const char* fq_status_str(int status) {
         case FQ_ERR_PARAM: return "FQ_ERR_PARAM: a scalar parameter is out of range";
         case FQ_ERR_HEADROOM: return "FQ_ERR_HEADROOM: the i-exp row sum could overflow 64 bits";
         case FQ_ERR_HIP: return "FQ_ERR_HIP: the HIP runtime rejected a launch";
+        case FQ_ERR_SCRATCH:
+            return "FQ_ERR_SCRATCH: the call needs more than the library's fixed device scratch holds";
         default: return "unknown fq_status";
     }
 }
@@ -264,6 +266,19 @@ fq_status ptf_calibrate(const float* x, int64_t T, int32_t C, int32_t bits, int3
     if (workspace_bytes < fqvit::ptf_calibrate_workspace_bytes(T, C, K)) return FQ_ERR_PARAM;
     fqvit::PtfCalibArgs a{x, T, C, bits, K, s, zp, alpha, workspace};
     return from_hip(fqvit::launch_ptf_calibrate(a, (hipStream_t)stream));
+}
+
+fq_status ptf_calibrate_noalloc(const float* x, int64_t T, int32_t C, int32_t bits, int32_t K,
+                                double* s, int32_t* zp, uint8_t* alpha, void* stream) {
+    ConsumeEvents consume;
+    if (T < 0 || T > kMaxCalibT || C < 1 || C > kMaxC) return FQ_ERR_SHAPE;
+    if (bits < 2 || bits > 8 || K < 0 || K > 7) return FQ_ERR_PARAM;
+    if (T == 0) return FQ_OK;
+    if (!x || !s || !zp || !alpha) return FQ_ERR_NULL;
+    if (fqvit::ptf_calibrate_workspace_bytes(T, C, K) > FQ_NOALLOC_SCRATCH_BYTES)
+        return FQ_ERR_SCRATCH;
+    fqvit::PtfCalibArgs a{x, T, C, bits, K, s, zp, alpha, nullptr};
+    return from_hip(fqvit::launch_ptf_calibrate_noalloc(a, (hipStream_t)stream));
 }
 
 fq_status ptf_quantize_int8(const float* x, int64_t T, int32_t C, const double* s,

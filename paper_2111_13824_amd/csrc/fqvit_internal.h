@@ -139,6 +139,10 @@ struct PtfCalibArgs {
 
 size_t ptf_calibrate_workspace_bytes(int64_t T, int32_t C, int32_t K);
 hipError_t launch_ptf_calibrate(const PtfCalibArgs& a, hipStream_t stream);
+// The same with the workspace in the library's fixed device array (the
+// caller has checked the size against FQ_NOALLOC_SCRATCH_BYTES; a.workspace
+// is ignored).
+hipError_t launch_ptf_calibrate_noalloc(const PtfCalibArgs& a, hipStream_t stream);
 
 struct PtfQuantArgs {
     const float* x;         // [T, C]

@@ -21,7 +21,9 @@
 // -alpha): scaling by a power of two commutes with the rounding of the
 // quotient, which never leaves the normal range for binary32 inputs.
 #include <cmath>
+#include <mutex>
 
+#include "fqvit.h"
 #include "fqvit_launch.h"
 
 namespace fqvit {
@@ -464,6 +466,48 @@ hipError_t launch_requant(const RequantArgs& a, hipStream_t stream) {
     launch_kernel(requant_kernel, dim3(grid_for(a.n, kBlock * 16, 8192)), dim3(kBlock), 0, stream,
                   a.q, a.n, a.N2, a.N1, a.zp, a.bits, vec4, a.y);
     return hipGetLastError();
+}
+
+// Workspace of ptf_calibrate_noalloc: a fixed array on every device the
+// library runs on.  In host code `scratch` names a host-side stand-in, not a
+// device address: its device address is looked up per device once
+// (hipGetSymbolAddress, with that device current) and only that address is
+// passed to kernels.
+static __device__ __align__(256) uint8_t scratch[FQ_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's address of `scratch`.
+hipError_t current_scratch(void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return hipSuccess;
+}
+
+}  // namespace
+
+hipError_t launch_ptf_calibrate_noalloc(const PtfCalibArgs& a, hipStream_t stream) {
+    void* ws = nullptr;
+    const hipError_t e = current_scratch(&ws);
+    if (e != hipSuccess) return e;
+    PtfCalibArgs b = a;
+    b.workspace = ws;
+    return launch_ptf_calibrate(b, stream);
 }
 
 }  // namespace fqvit

@@ -18,6 +18,10 @@ hipError_t launch_lis_qk(const LisArgs&, const QkInput&, hipStream_t) {
 hipError_t launch_attn_v_shift(const AvArgs&, hipStream_t) { ++g_launches; return hipSuccess; }
 hipError_t launch_attn_v_shift_wide(const AvWideArgs&, hipStream_t) { ++g_launches; return hipSuccess; }
 hipError_t launch_ptf_calibrate(const PtfCalibArgs&, hipStream_t) { ++g_launches; return hipSuccess; }
+hipError_t launch_ptf_calibrate_noalloc(const PtfCalibArgs& a, hipStream_t) {
+    ++g_launches;
+    return a.workspace == nullptr ? hipSuccess : hipErrorInvalidValue;
+}
 hipError_t launch_ptf_quantize(const PtfQuantArgs&, hipStream_t) { ++g_launches; return hipSuccess; }
 hipError_t launch_requant(const RequantArgs&, hipStream_t) { ++g_launches; return hipSuccess; }
 

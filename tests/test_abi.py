@@ -48,7 +48,7 @@ def test_header_symbols_exported(lib):
                           "lis_attention_head", "fq_status_str", "fq_version",
                           "fq_time_next_call", "ptf_calibrate", "fq_ptf_calibrate_workspace_bytes",
                           "ptf_quantize_int8", "requant_dyadic_int8", "lis_attention_qk",
-                          "lis_attn_v_shift_wide"}
+                          "lis_attn_v_shift_wide", "ptf_calibrate_noalloc"}
     for n in names:
         assert hasattr(lib, n), f"{n} declared in fqvit.h but not exported"
     # the binding exposes the compute entry points under the same names
@@ -76,7 +76,7 @@ def test_prepared_call_reports_status(lib):
 
 
 def test_status_strings(lib):
-    for s in range(6):
+    for s in range(7):
         assert B.status_str(s).startswith("FQ_")
     assert "unknown" in B.status_str(99)
     assert B.version() == 100
@@ -246,6 +246,32 @@ def test_calibrate_validation(lib):
     assert call(T=0, x=None, s=None) == B.FQ_OK      # empty: nothing enqueued
 
 
+def test_calibrate_noalloc_validation(lib):
+    """Host-side checks of the entry point that allocates nothing: the same
+    argument checks as ptf_calibrate, and sizes whose workspace exceeds the
+    fixed device scratch rejected with FQ_ERR_SCRATCH before any HIP call."""
+    f = lib.ptf_calibrate_noalloc
+    args = dict(x=1, T=100, C=16, bits=8, K=3, s=1, zp=1, alpha=1)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return f(a["x"], a["T"], a["C"], a["bits"], a["K"], a["s"], a["zp"], a["alpha"], NULL)
+
+    assert call(T=-1) == B.FQ_ERR_SHAPE
+    assert call(C=8193) == B.FQ_ERR_SHAPE
+    assert call(bits=9) == B.FQ_ERR_PARAM
+    assert call(K=8) == B.FQ_ERR_PARAM
+    for k in ("x", "s", "zp", "alpha"):
+        assert call(**{k: None}) == B.FQ_ERR_NULL
+    assert call(T=0, x=None) == B.FQ_OK
+    # the largest workloads' calibrations fit; a larger one does not
+    for T, C in ((12608, 768), (9232, 1024), (100352, 96)):
+        assert B.ptf_calibrate_workspace_bytes(T, C, 3) <= B.NOALLOC_SCRATCH_BYTES
+    assert B.ptf_calibrate_workspace_bytes(200000, 768, 3) > B.NOALLOC_SCRATCH_BYTES
+    assert call(T=200000, C=768) == B.FQ_ERR_SCRATCH
+    assert "scratch" in B.status_str(B.FQ_ERR_SCRATCH)
+
+
 def test_quantize_validation(lib):
     f = lib.ptf_quantize_int8
     args = dict(x=1, T=10, C=16, s=1, zp=1, alpha=1, bits=8, y=1)
@@ -343,5 +369,7 @@ def test_valid_calls_reach_exactly_one_launch(lib):
     need = lib.fq_ptf_calibrate_workspace_bytes(100, 16, 3)
     assert launches(lib.ptf_calibrate, 1, 100, 16, 8, 3, 1, 1, 1, 1, need, None) == (0, 1)
     assert launches(lib.ptf_calibrate, 1, 100, 16, 8, 3, 1, 1, 1, 1, need - 1, None)[1] == 0
+    assert launches(lib.ptf_calibrate_noalloc, 1, 100, 16, 8, 3, 1, 1, 1, None) == (0, 1)
+    assert launches(lib.ptf_calibrate_noalloc, 1, 200000, 768, 8, 3, 1, 1, 1, None) == (6, 0)
     assert launches(lib.ptf_quantize_int8, 1, 10, 16, 1, 1, 1, 8, 1, None) == (0, 1)
     assert launches(lib.requant_dyadic_int8, 1, 10, f32(0.5), f32(0.25), 0, 8, 1, None) == (0, 1)
