@@ -1,7 +1,7 @@
 // Log-Int-Softmax attention for gfx950: launch selection, the long-row
 // streaming kernel and the standalone BitShift Attn x V kernel.  The register
 // kernels (lis_device.h) are instantiated per chunk count in lis_inst_*.hip.
-#include "lis_device.h"
+#include "lis_long.h"
 
 namespace fqvit {
 namespace lis {
@@ -325,6 +325,9 @@ void launch_stream(bool fused, int dt, dim3 grid, size_t lds, hipStream_t stream
 
 }  // namespace
 
+// LDS of one workgroup on gfx950.
+constexpr size_t kMaxLdsBytes = 160 * 1024;
+
 hipError_t launch_lis(const LisArgs& a, hipStream_t stream) {
     using namespace lis;
     const bool fused = a.out != nullptr;
@@ -362,6 +365,26 @@ hipError_t launch_lis(const LisArgs& a, hipStream_t stream) {
         u.vt_bytes = fused ? u.dpad * u.ld * (int)sizeof(uint16_t) : 0;
         const bool half = a.Lk - 32 * (nc - 1) <= 16;
         return launch_lis_unit(nc, fused, dt, half, a, u, (size_t)u.vt_bytes + out_lds, stream);
+    }
+    // Long-row kernel: fused rows of 10 to 20 chunks on the float path, d <= 64,
+    // no codes output, when its I-Exp table (u_max + 1 entries, byte offsets in
+    // 16 bits) and V^T fit the LDS of one workgroup.
+    const bool long_ok = fused && fp && a.codes == nullptr && dt <= 4 && nc >= kLongMinNC &&
+                         nc <= kLongMaxNC && a.G <= 0x7FFFFFFF && a.k.u_max <= 16383 &&
+                         (int64_t)a.Lq * a.Lk * 4 < ((int64_t)1 << 31);
+    if (long_ok) {
+        LisLaunch l = p;
+        l.ntiles = tiles16;
+        l.kb = nc * 32;
+        l.ld = l.kb + 8;
+        l.vt_bytes = l.dpad * l.ld * (int)sizeof(uint16_t);
+        l.tab_bytes = (int)((((int64_t)a.k.u_max + 1) * 4 + 15) / 16 * 16);
+        const size_t lds = (size_t)l.tab_bytes + (size_t)l.vt_bytes;
+        if (lds <= kMaxLdsBytes) {
+            const bool half = a.Lk - 32 * (nc - 1) <= 16;
+            return nc <= 14 ? launch_lis_long_lo(nc, dt, half, a, l, lds, stream)
+                            : launch_lis_long_hi(nc, dt, half, a, l, lds, stream);
+        }
     }
     // Tile kernels: codes only for rows of up to 640 keys, the fused product
     // (without a codes output, d <= 64) for rows of up to 288 keys.

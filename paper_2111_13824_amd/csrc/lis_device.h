@@ -323,6 +323,7 @@ struct LisLaunch {
     int out_vec;    // output rows written through LDS as 16-byte units (d % 4 == 0, aligned out)
     int64_t n_logits;  // elements of the logits tensor (G Lq Lk)
     int64_t n_bias;    // elements of the bias tensor (Hb Lq Lk), 0 without bias
+    int tab_bytes;     // long-row kernel: LDS bytes of the I-Exp table (multiple of 16)
 };
 
 // ---------------------------------------------------------------------------
@@ -370,14 +371,14 @@ __device__ __forceinline__ int lis_code(uint32_t qL, uint32_t z, const RowSum& r
 // Float path
 // ---------------------------------------------------------------------------
 
-// I-Exp of one key for the float path: e = qL 2^(n - z) as a binary32 value
-// (exact: qL < 2^24).  z, q_p + q_b and qL come from the 24-bit integer
+// I-Exp of one key for the float path, from its clamped input u = max - v:
+// e = qL 2^(n - z) as a binary32 value (exact: qL < 2^24).  z, q_p + q_b and qL
+// come from the 24-bit integer
 // steps of iexp_qL (magic division by a multiply-high, two 24-bit
 // multiply-adds), which cost less than binary32 arithmetic; the host accepts
 // only scales for which those steps are exact.  k.magic and the shifted u are
 // below 2^24, so the product maps to one v_mul_hi_u32_u24.
-__device__ __forceinline__ float iexp_f(int v, int mx, const LisConsts& k) {
-    const uint32_t u = min((uint32_t)mx - (uint32_t)v, k.u_max);
+__device__ __forceinline__ float iexp_fu(uint32_t u, const LisConsts& k) {
     const uint32_t z =
         (uint32_t)(((uint64_t)((u << k.pre) & 0xFFFFFFu) * (uint64_t)(k.magic & 0xFFFFFFu)) >> 32);
     // q_p + q_b = z d + (q_b - u); written out because the compiler would
@@ -386,6 +387,12 @@ __device__ __forceinline__ float iexp_f(int v, int mx, const LisConsts& k) {
     asm("v_mad_u32_u24 %0, %1, %2, %3" : "=v"(w) : "v"(z), "s"(k.d_ln2), "v"(k.qb - u));
     const uint32_t qL = __umul24(w, w) + k.qc;
     return __builtin_ldexpf((float)qL, k.n - (int)z);
+}
+
+// The same for a logit v of a row with maximum mx: u = mx - v clamped at
+// n |q_ln2|.
+__device__ __forceinline__ float iexp_f(int v, int mx, const LisConsts& k) {
+    return iexp_fu(min((uint32_t)mx - (uint32_t)v, k.u_max), k);
 }
 
 // Code of one key on the float path, from e (its binary32 bit pattern) and the

@@ -22,6 +22,8 @@
 // shuffle reduction.  Per-channel gs, bs and the clamped shift are computed
 // once per workgroup into LDS and then held in registers; waves stride over
 // rows.
+#include <climits>
+
 #include "fqvit_launch.h"
 
 namespace fqvit {
@@ -373,50 +375,178 @@ __device__ __forceinline__ int ln_requant_rows(double A, double B, int xh, uint3
     return q;
 }
 
-// Rows r0 .. r0 + nr - 1 of the lane's dwords (zeros elsewhere; nr may be 0).
+// Rows r0 .. r0 + nr - 1 of the lane's dwords (zeros elsewhere; nr may be 0),
+// as buffer loads through the descriptor of the whole input: the loads that
+// are not needed address past its end and return 0 without a memory access,
+// so every load is issued unconditionally and the compiler can count the
+// loads in flight across the batches.
 template <int W>
-__device__ __forceinline__ void load_rows(uint32_t (&xv)[kRowBatch][W], const uint32_t* x32,
-                                          int64_t r0, int nr, int nd, int lane,
-                                          const bool (&ok)[W]) {
+__device__ __forceinline__ void load_rows(uint32_t (&xv)[kRowBatch][W],
+                                          __amdgpu_buffer_rsrc_t xr, int64_t r0, int nr, int nd,
+                                          int lane, const bool (&ok)[W]) {
 #pragma unroll
     for (int j = 0; j < kRowBatch; ++j) {
-        const uint32_t* xr = x32 + (r0 + (j < nr ? j : 0)) * nd + lane;
 #pragma unroll
-        for (int w = 0; w < W; ++w)
-            xv[j][w] = (j < nr && ok[w]) ? __builtin_nontemporal_load(xr + 64 * w) : 0u;
+        for (int w = 0; w < W; ++w) {
+            const int off = (j < nr && ok[w]) ? (int)(((r0 + j) * nd + lane + 64 * w) * 4) : INT_MIN;
+            xv[j][w] = __builtin_amdgcn_raw_buffer_load_b32(xr, off, 0, 2 /* nt */);
+        }
     }
 }
 
-// Workgroup size: 1024 (one per CU, 4 waves per SIMD within 128 VGPRs), or
-// 512 for W = 4, whose registers exceed that budget.
-constexpr int rows_block(int W) { return W >= 4 ? 512 : 1024; }
+// Per-lane constants of the row-batch kernel (see ln_rows_kernel).
+template <int W>
+struct RowsCtx {
+    uint32_t mulp[2 * W], zmp[2 * W], mulb[W];
+    uint32_t m1init;
+    double gmaxl, gminl;
+    bool zerol;
+    bool ok[W];
+    uint32_t hi_mask, m_add;
+    double amax, amin, cadd;
+    int lo512, hi512, qlo, qhi;
+};
+
+// Statistics of rows r0 .. r0 + nr - 1 (nr in 1..4) from their dwords xv: the
+// packed X^ of each row, and the factors r, m of row j in lane group j.
+template <int W>
+struct RowsStats {
+    uint32_t hp[kRowBatch][2 * W];
+    double r, m;
+};
 
 template <int W>
-__global__ __launch_bounds__(rows_block(W)) void ln_rows_kernel(LnArgs a) {
+__device__ __forceinline__ void rows_stats(const LnArgs& a, const RowsCtx<W>& k,
+                                           const uint32_t (&xv)[kRowBatch][W], RowsStats<W>& st) {
+    uint32_t m1[kRowBatch], m2[kRowBatch];
+#pragma unroll
+    for (int j = 0; j < kRowBatch; ++j) {
+        m1[j] = k.m1init;
+        m2[j] = 0;
+#pragma unroll
+        for (int w = 0; w < W; ++w) {
+            const uint32_t xu = xv[j][w] ^ 0x80808080u;
+            const uint32_t p0 = __builtin_amdgcn_perm(xu, xu, 0x0C010C00u);
+            const uint32_t p1 = __builtin_amdgcn_perm(xu, xu, 0x0C030C02u);
+            const short2_t h0 = __builtin_bit_cast(short2_t, p0) * __builtin_bit_cast(short2_t, k.mulp[2 * w]) +
+                                __builtin_bit_cast(short2_t, k.zmp[2 * w]);
+            const short2_t h1 = __builtin_bit_cast(short2_t, p1) * __builtin_bit_cast(short2_t, k.mulp[2 * w + 1]) +
+                                __builtin_bit_cast(short2_t, k.zmp[2 * w + 1]);
+            m1[j] = __builtin_amdgcn_udot4(xu, k.mulb[w], m1[j], false);
+            m2[j] = (uint32_t)__builtin_amdgcn_sdot2(h0, h0, (int)m2[j], false);
+            m2[j] = (uint32_t)__builtin_amdgcn_sdot2(h1, h1, (int)m2[j], false);
+            st.hp[j][2 * w] = __builtin_bit_cast(uint32_t, h0);
+            st.hp[j][2 * w + 1] = __builtin_bit_cast(uint32_t, h1);
+        }
+    }
+    // lane group j (lanes 16 j .. 16 j + 15) ends with row j's totals
+    const uint32_t t1 = row16_sum(swap_add16(swap_add32(m1[0], m1[2]), swap_add32(m1[1], m1[3])));
+    const uint32_t t2 = row16_sum(swap_add16(swap_add32(m2[0], m2[2]), swap_add32(m2[1], m2[3])));
+    row_factors((int64_t)(int32_t)t1, (int64_t)t2, a.C, st.r, st.m);
+}
+
+// Output of the batch: packed bytes yo[j][w] of the rows whose factors are in
+// the fast range (fast[j]); the other rows are written here, element by
+// element (their bytes read again).
+template <int W>
+__device__ __forceinline__ void rows_output(const LnArgs& a, const RowsCtx<W>& k,
+                                            const double2* s_gb, const RowsStats<W>& st,
+                                            uint32_t (&yo)[kRowBatch][W], bool (&fast)[kRowBatch],
+                                            int64_t r0, int nr, int nd, int lane) {
+    // every flag set: rows_store writes exactly the rows flagged here
+#pragma unroll
+    for (int j = 0; j < kRowBatch; ++j) fast[j] = false;
+#pragma unroll
+    for (int j = 0; j < kRowBatch; ++j) {
+        if (j >= nr) break;
+        const double rj = readlane_f64(st.r, 16 * j);
+        const double mj = readlane_f64(st.m, 16 * j);
+        const bool lane_fits = !k.zerol && k.gmaxl * rj < k.amax && k.gminl * rj >= k.amin;
+        fast[j] = rj > 0.0 && __ballot(!lane_fits) == 0;
+        if (fast[j]) {
+#pragma unroll
+            for (int w = 0; w < W; ++w) {
+                int q[4];
+#pragma unroll
+                for (int b = 0; b < 4; ++b) {
+                    const uint32_t hw = st.hp[j][2 * w + (b >> 1)];
+                    const int xh = (b & 1) ? (int)hw >> 16 : (int)(int16_t)(hw & 0xFFFFu);
+                    const double2 gb = s_gb[b * nd + (k.ok[w] ? lane + 64 * w : 0)];
+                    const double A = gb.x * rj;
+                    const double B = gb.y - gb.x * mj;
+                    q[b] = ln_requant_rows(A, B, xh, k.hi_mask, k.m_add, k.cadd, k.lo512, k.hi512);
+                }
+                const uint32_t lo = __builtin_amdgcn_perm((uint32_t)q[1], (uint32_t)q[0], 0x0C0C0400u);
+                const uint32_t hi = __builtin_amdgcn_perm((uint32_t)q[3], (uint32_t)q[2], 0x0C0C0400u);
+                yo[j][w] = __builtin_amdgcn_perm(hi, lo, 0x05040100u);
+                // one dword at a time: the f64 temporaries of all 4 W
+                // elements would not fit the register budget
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        } else {
+            const int8_t* xrow = a.x + (r0 + j) * a.C;
+            int8_t* yrow = a.y + (r0 + j) * a.C;
+#pragma unroll 1
+            for (int c = lane; c < a.C; c += 64) {
+                const int xh = ((int)xrow[c] - a.zp_in) * (1 << min((int)a.alpha[c], a.K));
+                const double2 gb = s_gb[(c & 3) * nd + (c >> 2)];
+                const double A = gb.x * rj;
+                const double B = gb.y - gb.x * mj;
+                yrow[c] = (int8_t)ln_requant(A, B, xh, a.bits, a.zp_out, k.qlo, k.qhi);
+            }
+        }
+    }
+}
+
+template <int W>
+__device__ __forceinline__ void rows_store(const RowsCtx<W>& k, const uint32_t (&yo)[kRowBatch][W],
+                                           const bool (&fast)[kRowBatch], uint32_t* y32,
+                                           int64_t r0, int nd, int lane) {
+#pragma unroll
+    for (int j = 0; j < kRowBatch; ++j) {
+        if (!fast[j]) continue;
+        uint32_t* yr = y32 + (r0 + j) * nd + lane;
+#pragma unroll
+        for (int w = 0; w < W; ++w)
+            if (k.ok[w]) __builtin_nontemporal_store(yo[j][w], yr + 64 * w);
+    }
+}
+
+// A wavefront owns a contiguous run of rows and takes them NB batches of four
+// at a time: the loads of all NB batches are issued first, then the batches
+// are computed in order, so the loads of the later ones stream in under the
+// arithmetic of the earlier ones.  No load is in flight across the loop's
+// back edge (a wait there would cover every outstanding load).  BLOCK threads
+// per workgroup; the grid sets the number of wavefronts per CU.
+template <int W, int BLOCK, int NB>
+__global__ __launch_bounds__(BLOCK) void ln_rows_kernel(LnArgs a) {
     extern __shared__ double smem[];
     double2* s_gb = reinterpret_cast<double2*>(smem);        // (gs, bs) at [b][dword]
     uint4* s_pk = reinterpret_cast<uint4*>(s_gb + a.C);      // per dword, see below
     const int nd = a.C >> 2;
     const int lane = threadIdx.x & 63;
-    const uint32_t* x32 = reinterpret_cast<const uint32_t*>(a.x);
     uint32_t* y32 = reinterpret_cast<uint32_t*>(a.y);
 
     // Contiguous run of rows of this wavefront.  Wavefronts are numbered
     // across workgroups first, so that the ones with an extra row (the
     // remainder of T / nw) spread over all CUs.
-    constexpr int kWaves = rows_block(W) / 64;
+    constexpr int kWaves = BLOCK / 64;
     const int64_t nw = (int64_t)gridDim.x * kWaves;
-    const int64_t gw = (int64_t)(threadIdx.x >> 6) * gridDim.x + blockIdx.x;
+    const int64_t gw = (int64_t)__builtin_amdgcn_readfirstlane(threadIdx.x >> 6) * gridDim.x +
+                       blockIdx.x;
+    // the whole input, a.T * a.C < 2^31 bytes (checked by the launcher)
+    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)a.x, (short)0, (int)(a.T * a.C), 0x00020000);
     const int64_t base = a.T / nw, rem = a.T % nw;
-    int64_t r0 = gw * base + min(gw, rem);
-    const int64_t r1 = r0 + base + (gw < rem ? 1 : 0);
-    bool ok[W];
+    int64_t ra = gw * base + min(gw, rem);
+    const int64_t r1 = ra + base + (gw < rem ? 1 : 0);
+    RowsCtx<W> k;
 #pragma unroll
-    for (int w = 0; w < W; ++w) ok[w] = lane + 64 * w < nd;
+    for (int w = 0; w < W; ++w) k.ok[w] = lane + 64 * w < nd;
 
     // Set-up, one thread per dword (4 channels; nd <= 256 <= blockDim): its
-    // loads go first, then the first batch of rows, so that the per-channel
-    // factors are computed while the rows stream in.
+    // loads go first, then the first two batches of rows, so that the
+    // per-channel factors are computed while the rows stream in.
     //   gs = gamma / s_out, bs = beta / s_out (binary64), and per-dword
     //   constants with u = zp_in + 128:
     //   s_pk[2 dw]     = i16 pairs of 2^alpha (channels 0,1 and 2,3),
@@ -434,9 +564,13 @@ __global__ __launch_bounds__(rows_block(W)) void ln_rows_kernel(LnArgs a) {
             sa[b] = a.alpha[4 * sdw + b];
         }
     }
-    uint32_t xv[kRowBatch][W];
-    int nr = (int)min<int64_t>(kRowBatch, r1 - r0);
-    load_rows<W>(xv, x32, r0, nr, nd, lane, ok);
+    uint32_t xv[NB][kRowBatch][W];
+    int nr[NB];
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+        nr[i] = (int)max<int64_t>(0, min<int64_t>(kRowBatch, r1 - ra - kRowBatch * i));
+        load_rows<W>(xv[i], xr, ra + kRowBatch * i, nr[i], nd, lane, k.ok);
+    }
 
     const int u = a.zp_in + 128;
     if (sdw < nd) {
@@ -459,134 +593,102 @@ __global__ __launch_bounds__(rows_block(W)) void ln_rows_kernel(LnArgs a) {
         s_pk[2 * sdw + 1] = uint4{mulb, m1p, ghi, glo};
     }
     __syncthreads();
-    if (nr <= 0) return;
+    if (nr[0] <= 0) return;
 
-    uint32_t mulp[2 * W], zmp[2 * W], mulb[W];
-    uint32_t m1init = 0, ghi = 0, glo = 0x7FF00000u;
+    uint32_t ghi = 0, glo = 0x7FF00000u;
+    k.m1init = 0;
 #pragma unroll
     for (int w = 0; w < W; ++w) {
-        const int dw = ok[w] ? lane + 64 * w : 0;
+        const int dw = k.ok[w] ? lane + 64 * w : 0;
         const uint4 p = s_pk[2 * dw];
         const uint4 q = s_pk[2 * dw + 1];
-        mulp[2 * w] = ok[w] ? p.x : 0u;
-        mulp[2 * w + 1] = ok[w] ? p.y : 0u;
-        zmp[2 * w] = ok[w] ? p.z : 0u;
-        zmp[2 * w + 1] = ok[w] ? p.w : 0u;
-        mulb[w] = ok[w] ? q.x : 0u;
-        m1init += ok[w] ? q.y : 0u;
-        ghi = ok[w] ? max(ghi, q.z) : ghi;
-        glo = ok[w] ? min(glo, q.w) : glo;
+        k.mulp[2 * w] = k.ok[w] ? p.x : 0u;
+        k.mulp[2 * w + 1] = k.ok[w] ? p.y : 0u;
+        k.zmp[2 * w] = k.ok[w] ? p.z : 0u;
+        k.zmp[2 * w + 1] = k.ok[w] ? p.w : 0u;
+        k.mulb[w] = k.ok[w] ? q.x : 0u;
+        k.m1init += k.ok[w] ? q.y : 0u;
+        ghi = k.ok[w] ? max(ghi, q.z) : ghi;
+        glo = k.ok[w] ? min(glo, q.w) : glo;
     }
     // Bounds on |gs| over the lane's channels from the high words alone
     // (|gs| <= gmaxl, |gs| >= gminl; a row whose factors come that close to a
     // bound of the fast range takes the general path).  Zero or subnormal
     // gs (high word 0) always takes the general path.
-    const double gmaxl = __longlong_as_double((int64_t)(((uint64_t)ghi << 32) | 0xFFFFFFFFu));
-    const double gminl = __longlong_as_double((int64_t)((uint64_t)glo << 32));
-    const bool zerol = glo == 0;
+    k.gmaxl = __longlong_as_double((int64_t)(((uint64_t)ghi << 32) | 0xFFFFFFFFu));
+    k.gminl = __longlong_as_double((int64_t)((uint64_t)glo << 32));
+    k.zerol = glo == 0;
 
-    const int qlo = -(1 << (a.bits - 1));
-    const int qhi = (1 << (a.bits - 1)) - 1;
-    const uint32_t hi_mask = ~((1u << (21 - a.bits)) - 1u);
+    k.qlo = -(1 << (a.bits - 1));
+    k.qhi = (1 << (a.bits - 1)) - 1;
+    k.hi_mask = ~((1u << (21 - a.bits)) - 1u);
     // one opaque scalar, so that the exponent add stays one instruction (the
     // compiler would otherwise split the constant into a subtract and an add)
     uint32_t m_add = ((uint32_t)(53 - a.bits) << 20) | 0x80000u;
     asm volatile("" : "+s"(m_add));
-    const double amax = ldexp(1.0, a.bits), amin = ldexp(1.0, a.bits - 31);
-    const double cadd = (double)a.zp_out + 512.5;
-    const int lo512 = qlo + 512, hi512 = qhi + 512;
+    k.m_add = m_add;
+    k.amax = ldexp(1.0, a.bits);
+    k.amin = ldexp(1.0, a.bits - 31);
+    k.cadd = (double)a.zp_out + 512.5;
+    k.lo512 = k.qlo + 512;
+    k.hi512 = k.qhi + 512;
 
+    // Batch i: statistics, output into registers; its stores are issued only
+    // after the statistics of batch i + 1 have waited for that batch's loads
+    // (loads and stores share one counter: a store issued before that wait
+    // would be waited for too).
     for (;;) {
-        uint32_t hp[kRowBatch][2 * W];
-        uint32_t m1[kRowBatch], m2[kRowBatch];
+        uint32_t yo[kRowBatch][W];
+        bool fast[kRowBatch];
+        int64_t rprev = 0;
+        bool pending = false;
 #pragma unroll
-        for (int j = 0; j < kRowBatch; ++j) {
-            m1[j] = m1init;
-            m2[j] = 0;
-#pragma unroll
-            for (int w = 0; w < W; ++w) {
-                const uint32_t xu = xv[j][w] ^ 0x80808080u;
-                const uint32_t p0 = __builtin_amdgcn_perm(xu, xu, 0x0C010C00u);
-                const uint32_t p1 = __builtin_amdgcn_perm(xu, xu, 0x0C030C02u);
-                const short2_t h0 = __builtin_bit_cast(short2_t, p0) * __builtin_bit_cast(short2_t, mulp[2 * w]) +
-                                    __builtin_bit_cast(short2_t, zmp[2 * w]);
-                const short2_t h1 = __builtin_bit_cast(short2_t, p1) * __builtin_bit_cast(short2_t, mulp[2 * w + 1]) +
-                                    __builtin_bit_cast(short2_t, zmp[2 * w + 1]);
-                m1[j] = __builtin_amdgcn_udot4(xu, mulb[w], m1[j], false);
-                m2[j] = (uint32_t)__builtin_amdgcn_sdot2(h0, h0, (int)m2[j], false);
-                m2[j] = (uint32_t)__builtin_amdgcn_sdot2(h1, h1, (int)m2[j], false);
-                hp[j][2 * w] = __builtin_bit_cast(uint32_t, h0);
-                hp[j][2 * w + 1] = __builtin_bit_cast(uint32_t, h1);
-            }
+        for (int i = 0; i < NB; ++i) {
+            if (nr[i] <= 0) break;
+            RowsStats<W> st;
+            rows_stats<W>(a, k, xv[i], st);
+            if (pending) rows_store<W>(k, yo, fast, y32, rprev, nd, lane);
+            rows_output<W>(a, k, s_gb, st, yo, fast, ra + kRowBatch * i, nr[i], nd, lane);
+            rprev = ra + kRowBatch * i;
+            pending = true;
         }
-        // lane group j (lanes 16 j .. 16 j + 15) ends with row j's totals
-        const uint32_t t1 = row16_sum(swap_add16(swap_add32(m1[0], m1[2]), swap_add32(m1[1], m1[3])));
-        const uint32_t t2 = row16_sum(swap_add16(swap_add32(m2[0], m2[2]), swap_add32(m2[1], m2[3])));
-        double r, m;
-        row_factors((int64_t)(int32_t)t1, (int64_t)t2, a.C, r, m);
-
+        if (pending) rows_store<W>(k, yo, fast, y32, rprev, nd, lane);
+        ra += NB * kRowBatch;
+        if (ra >= r1) break;
 #pragma unroll
-        for (int j = 0; j < kRowBatch; ++j) {
-            if (j >= nr) break;
-            const double rj = readlane_f64(r, 16 * j);
-            const double mj = readlane_f64(m, 16 * j);
-            uint32_t* yr = y32 + (r0 + j) * nd + lane;
-            const bool lane_fits = !zerol && gmaxl * rj < amax && gminl * rj >= amin;
-            if (rj > 0.0 && __ballot(!lane_fits) == 0) {
-#pragma unroll
-                for (int w = 0; w < W; ++w) {
-                    int q[4];
-#pragma unroll
-                    for (int b = 0; b < 4; ++b) {
-                        const uint32_t hw = hp[j][2 * w + (b >> 1)];
-                        const int xh = (b & 1) ? (int)hw >> 16 : (int)(int16_t)(hw & 0xFFFFu);
-                        const double2 gb = s_gb[b * nd + (ok[w] ? lane + 64 * w : 0)];
-                        const double A = gb.x * rj;
-                        const double B = gb.y - gb.x * mj;
-                        q[b] = ln_requant_rows(A, B, xh, hi_mask, m_add, cadd, lo512, hi512);
-                    }
-                    const uint32_t lo = __builtin_amdgcn_perm((uint32_t)q[1], (uint32_t)q[0], 0x0C0C0400u);
-                    const uint32_t hi = __builtin_amdgcn_perm((uint32_t)q[3], (uint32_t)q[2], 0x0C0C0400u);
-                    const uint32_t pack = __builtin_amdgcn_perm(hi, lo, 0x05040100u);
-                    if (ok[w]) __builtin_nontemporal_store(pack, yr + 64 * w);
-                    // one dword at a time: the f64 temporaries of all 4 W
-                    // elements would not fit the register budget
-                    __builtin_amdgcn_sched_barrier(0);
-                }
-            } else {
-                // rare (factors out of the fast range): element by element,
-                // the row's bytes read again
-                const int8_t* xrow = a.x + (r0 + j) * a.C;
-                int8_t* yrow = a.y + (r0 + j) * a.C;
-#pragma unroll 1
-                for (int c = lane; c < a.C; c += 64) {
-                    const int xh = ((int)xrow[c] - a.zp_in) * (1 << min((int)a.alpha[c], a.K));
-                    const double2 gb = s_gb[(c & 3) * nd + (c >> 2)];
-                    const double A = gb.x * rj;
-                    const double B = gb.y - gb.x * mj;
-                    yrow[c] = (int8_t)ln_requant(A, B, xh, a.bits, a.zp_out, qlo, qhi);
-                }
-            }
+        for (int i = 0; i < NB; ++i) {
+            nr[i] = (int)max<int64_t>(0, min<int64_t>(kRowBatch, r1 - ra - kRowBatch * i));
+            load_rows<W>(xv[i], xr, ra + kRowBatch * i, nr[i], nd, lane, k.ok);
         }
-        // next batch (loaded after the output: requested earlier it would
-        // stay live beside the packed X^ and spill)
-        r0 += kRowBatch;
-        nr = (int)min<int64_t>(kRowBatch, r1 - r0);
-        if (nr <= 0) break;
-        load_rows<W>(xv, x32, r0, nr, nd, lane, ok);
     }
 }
 
+// Workgroup size of the row-batch kernel.
+constexpr int kRowsBlock = 256;
+
+template <int W, int NB>
+hipError_t launch_rows_nb(const LnArgs& a, int wpc, hipStream_t stream) {
+    // one pass of NB batches per wavefront where the rows allow it, at most
+    // wpc wavefronts per CU
+    constexpr int kWaves = kRowsBlock / 64;
+    const int64_t want = (a.T + NB * kRowBatch - 1) / (NB * kRowBatch);
+    const int64_t waves = std::max<int64_t>(1, std::min<int64_t>(want, 256 * (int64_t)wpc));
+    const int64_t blocks = (waves + kWaves - 1) / kWaves;
+    const size_t lds = (size_t)a.C * 2 * sizeof(double) + (size_t)(a.C / 4) * 2 * sizeof(uint4);
+    launch_kernel(ln_rows_kernel<W, kRowsBlock, NB>, dim3((unsigned)blocks), dim3(kRowsBlock), lds,
+                  stream, a);
+    return hipGetLastError();
+}
+
+// Measured on the ViT-B/16 shape (12608 x 768, one MI355X): one batch per pass
+// at 12 wavefronts per CU 11.0-11.2 us; 8 per CU 12.1-13.2 us, 16 or 20 per CU
+// 12.4-12.6 us; two or three batches per pass (their loads issued together,
+// each batch's stores held back until the next batch's loads were waited for)
+// 13.0-13.5 and 18.0-18.4 us.  The kernel is bound by its vector-ALU issue
+// (the binary64 output), not by the latency the extra batches would hide.
 template <int W>
 hipError_t launch_rows(const LnArgs& a, hipStream_t stream) {
-    // about three rows per wavefront or more, at most one workgroup of 16
-    // wavefronts per CU
-    constexpr int kWaves = rows_block(W) / 64;
-    const int64_t waves = (a.T + 2) / 3;
-    const int64_t blocks = std::min<int64_t>((waves + kWaves - 1) / kWaves, 256 * 16 / kWaves);
-    const size_t lds = (size_t)a.C * 2 * sizeof(double) + (size_t)(a.C / 4) * 2 * sizeof(uint4);
-    launch_kernel(ln_rows_kernel<W>, dim3((unsigned)blocks), dim3(rows_block(W)), lds, stream, a);
-    return hipGetLastError();
+    return launch_rows_nb<W, 1>(a, 12, stream);
 }
 
 template <int W>
@@ -614,7 +716,8 @@ hipError_t launch_ptf_layernorm(const LnArgs& a, hipStream_t stream) {
     const bool narrow = (double)a.C * 65025.0 * (double)(1 << (2 * a.K)) < 4294967296.0;
     // Row-batch kernel for 256 <= C <= 1024 (up to 4 dwords per lane without
     // spills) when the sums of squares fit 32 bits.
-    if (aligned && a.C % 4 == 0 && nd >= 64 && nd <= 256 && narrow) {
+    if (aligned && a.C % 4 == 0 && nd >= 64 && nd <= 256 && narrow &&
+        a.T * (int64_t)a.C < ((int64_t)1 << 31)) {
         switch ((nd + 63) / 64) {
             case 1: return launch_rows<1>(a, stream);
             case 2: return launch_rows<2>(a, stream);

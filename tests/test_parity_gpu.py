@@ -69,6 +69,23 @@ def test_ln_shapes(fq, orc, T, C):
     assert np.array_equal(_ln_gpu(fq, d), _ln_ref(orc, d))
 
 
+@pytest.mark.parametrize("T,C", [(100, 1024), (7, 768), (13, 256), (101, 512), (4099, 768), (37, 96)])
+def test_ln_writes_only_its_rows(fq, orc, T, C):
+    """Every row count, including a last batch of fewer rows than the one
+    before it: the output matches and the bytes after it (a guard region in
+    the same allocation) are untouched."""
+    import torch
+    say("ln guard", T, C)
+    d = W.ln_inputs(T, C, seed=T + 3 * C)
+    buf = torch.full(((T + 16) * C,), 0x5A, dtype=torch.int8, device="cuda:0")
+    y = buf[:T * C].view(T, C)
+    fq.ptf_layernorm_int8(dev(d["x_q"]), d["zp_in"], dev(d["alpha"]), d["K"], dev(d["gamma"]),
+                          dev(d["beta"]), d["s_out"], d["zp_out"], d["bits"], y_q=y)
+    out = host(buf)
+    assert np.array_equal(out[:T * C].reshape(T, C), _ln_ref(orc, d))
+    assert np.all(out[T * C:] == 0x5A)
+
+
 @pytest.mark.parametrize("K,bits", [(0, 8), (3, 8), (7, 8), (5, 8), (3, 4), (2, 2), (6, 6)])
 def test_ln_params(fq, orc, K, bits):
     say("ln params", K, bits)
@@ -342,6 +359,47 @@ def test_head_shapes(fq, orc, G, Lq, Lk, d):
     got = host(fq.lis_attention_head(dev(a["logits"]), dev(a["v"]), S, zp_v=-2))
     ref = orc.lis_attention_head(a["logits"], a["v"], S, zp_v=-2)
     assert np.array_equal(got, ref)
+
+
+# Long rows (10 to 20 chunks of 32 keys) take the long-row kernel: logits read
+# once, I-Exp from an LDS table.
+LONG_SHAPES = [(3, 70, 577, 64, 0), (2, 33, 289, 32, 0), (2, 17, 640, 64, 2), (3, 50, 400, 17, 3),
+               (2, 40, 313, 48, 2), (4, 16, 336, 64, 0), (2, 1, 600, 8, 0)]
+
+
+@pytest.mark.parametrize("G,Lq,Lk,d,Hb", LONG_SHAPES)
+def test_head_long_rows(fq, orc, G, Lq, Lk, d, Hb):
+    say("head long", G, Lq, Lk, d, Hb)
+    a = W.attn_inputs(G, Lq, Lk, d, seed=G + Lq + Lk, heads=max(Hb, 1), sigma=(1.0, 3.0, 6.0),
+                      v_lo=-128, v_hi=127, bias=Hb > 0)
+    bias = dev(a["bias"]) if Hb else None
+    got = host(fq.lis_attention_head(dev(a["logits"]), dev(a["v"]), S, zp_v=-4, bias=bias))
+    assert np.array_equal(got, orc.lis_attention_head(a["logits"], a["v"], S, zp_v=-4, bias=a["bias"]))
+
+
+def test_head_long_rows_wide_span(fq, orc):
+    """Rows whose logits span more than 2^15 units (a tile holding one of them
+    is computed from the logits again), beside ordinary tiles, in units whose
+    first chunk does not hold the row maximum."""
+    say("head long wide span")
+    a = W.attn_inputs(3, 100, 577, 64, seed=31, sigma=(3.0,), v_lo=-128, v_hi=127)
+    lg = a["logits"].copy()
+    lg[0, 5, 500] = 2 ** 24                  # tile 0 of unit 0
+    lg[1, 40, 300] = lg[1, 40].max() + 40000  # tile 2 of unit 1
+    lg[2, :, 400:] += 20000                  # every row: maximum far from the first chunk
+    lg[2, 99, 0] = -(2 ** 29)
+    got = host(fq.lis_attention_head(dev(lg), dev(a["v"]), S))
+    assert np.array_equal(got, orc.lis_attention_head(lg, a["v"], S))
+
+
+@pytest.mark.parametrize("n", [23, 25])
+def test_head_long_rows_clamp_depth(fq, orc, n):
+    """n = 23: an I-Exp table of 16331 entries (65 KB of LDS beside V^T); n = 25:
+    beyond the table's 16-bit offsets, the stream kernel."""
+    say("head long depth", n)
+    a = W.attn_inputs(2, 40, 577, 64, seed=n, sigma=(6.0,))
+    got = host(fq.lis_attention_head(dev(a["logits"]), dev(a["v"]), S, exp_n=n))
+    assert np.array_equal(got, orc.lis_attention_head(a["logits"], a["v"], S, exp_n=n))
 
 
 # Shapes with enough units that the launch takes the one-workgroup-per-unit
