@@ -203,7 +203,8 @@ fq_status lis_attention_head(const int32_t* logits, const int32_t* bias, int32_t
  *           lis_attention_head;
  *           s_logit is the scale of the logits (s_q s_k, with any 1/sqrt(dk)
  *           of the softmax folded in).
- * Supported: Lk in [1, 224], d in [1, 64].
+ * Supported: Lk in [1, 640], d in [1, 64] (rows of more than 224 keys: the
+ * logits are recomputed from K in each pass instead of held).
  * Errors: FQ_ERR_NULL, FQ_ERR_SHAPE (sizes, dk, or bias with Hb < 1),
  * FQ_ERR_PARAM (zero points, bits, exp_n, s_logit, or misaligned q / k),
  * FQ_ERR_HEADROOM.

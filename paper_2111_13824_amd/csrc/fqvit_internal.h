@@ -88,7 +88,7 @@ struct QkInput {
     int32_t dk;             // 32 or 64
 };
 
-constexpr int kQkMaxLk = 224;   // keys per unit (7 chunks of 32)
+constexpr int kQkMaxLk = 640;   // keys per unit (20 chunks of 32)
 
 hipError_t launch_lis_qk(const LisArgs& a, const QkInput& in, hipStream_t stream);
 

@@ -109,6 +109,36 @@ __device__ __forceinline__ int long_load_tile(uint32_t (&pk)[NC][4], const LongR
     return row4_max(rmax);
 }
 
+// V^T of a whole unit (keys [0, kp), kp a multiple of 32) staged by a workgroup
+// of NTHREADS threads, as stage_store does: item = (16-column group, key quad).
+template <int DTMAX, int NTHREADS>
+__device__ __forceinline__ void long_stage_vt(uint16_t* vt, int ld, const int8_t* vg, int Lk, int d,
+                                              int kp, int zp, bool vec_ok) {
+    const int nquads = kp / 4;
+    const float off = (float)(128 + zp);
+    for (int idx = threadIdx.x; idx < nquads * DTMAX; idx += NTHREADS) {
+        const int cg = idx / nquads;
+        const int jj = 4 * (idx - cg * nquads);
+        const int dd = 16 * cg;
+        u32x4 w[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+            w[t] = (dd < d && jj + t < Lk) ? load_v16(vg + (int64_t)(jj + t) * d, dd, d, vec_ok)
+                                           : u32x4{0u, 0u, 0u, 0u};
+        const int pos = (jj & ~31) + chunk_pos(jj & 31);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) w[t] ^= 0x80808080u;
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+            float f[4];
+#pragma unroll
+            for (int t = 0; t < 4; ++t) f[t] = (float)((w[t][q >> 2] >> (8 * (q & 3))) & 0xFFu) - off;
+            *reinterpret_cast<u32x2*>(vt + (16 * cg + q) * ld + pos) =
+                u32x2{bf16_pair(f[0], f[1]), bf16_pair(f[2], f[3])};
+        }
+    }
+}
+
 // e (binary32 bits) of the table entry at byte offset off
 __device__ __forceinline__ uint32_t long_table(const uint8_t* smem, uint32_t off) {
     return *reinterpret_cast<const uint32_t*>(smem + off);
@@ -184,33 +214,8 @@ __global__ __launch_bounds__(kLongBlock) void lis_long_kernel(LisArgs a, LisLaun
     k.d_ln2 &= 0xFFFFFFu;
     k.magic &= 0xFFFFFFu;
 
-    // V^T of the unit: item = (16-column group, key quad), as stage_store
-    {
-        const int8_t* vg = a.v + g * (int64_t)Lk * a.d;
-        constexpr int nquads = 8 * NC;
-        const float off = (float)(128 + a.zp_v);
-        for (int idx = threadIdx.x; idx < nquads * DTMAX; idx += kLongBlock) {
-            const int cg = idx / nquads;
-            const int jj = 4 * (idx - cg * nquads);
-            const int dd = 16 * cg;
-            u32x4 w[4];
-#pragma unroll
-            for (int t = 0; t < 4; ++t)
-                w[t] = (dd < a.d && jj + t < Lk) ? load_v16(vg + (int64_t)(jj + t) * a.d, dd, a.d, p.vec_ok)
-                                                 : u32x4{0u, 0u, 0u, 0u};
-            const int pos = (jj & ~31) + chunk_pos(jj & 31);
-#pragma unroll
-            for (int t = 0; t < 4; ++t) w[t] ^= 0x80808080u;
-#pragma unroll
-            for (int q = 0; q < 16; ++q) {
-                float f[4];
-#pragma unroll
-                for (int t = 0; t < 4; ++t) f[t] = (float)((w[t][q >> 2] >> (8 * (q & 3))) & 0xFFu) - off;
-                *reinterpret_cast<u32x2*>(vt + (16 * cg + q) * p.ld + pos) =
-                    u32x2{bf16_pair(f[0], f[1]), bf16_pair(f[2], f[3])};
-            }
-        }
-    }
+    long_stage_vt<DTMAX, kLongBlock>(vt, p.ld, a.v + g * (int64_t)Lk * a.d, Lk, a.d, 32 * NC, a.zp_v,
+                                     p.vec_ok);
     for (uint32_t u = threadIdx.x; u <= k.u_max; u += kLongBlock) tab[u] = __float_as_uint(iexp_fu(u, k));
     __syncthreads();
 

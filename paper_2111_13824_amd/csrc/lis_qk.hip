@@ -1,5 +1,6 @@
-// Host side of the integer-only attention from int8 Q and K (kernel in
-// lis_qk_kernel.h): launch geometry and LDS of one workgroup per unit.
+// Host side of the integer-only attention from int8 Q and K (kernels in
+// lis_qk_kernel.h and lis_qk_long.hip): launch geometry and LDS of one
+// workgroup per unit.
 #include "lis_qk_kernel.h"
 
 namespace fqvit {
@@ -24,6 +25,8 @@ hipError_t launch_lis_qk(const LisArgs& a, const QkInput& in, hipStream_t stream
     const bool half = a.Lk - 32 * (nc - 1) <= 16;
     const bool fp = a.k.fp_ok != 0;
     const QkArgs qa{in.q, in.k, in.zp_q, in.zp_k};
+    // rows beyond 7 chunks: logits recomputed per pass from K in LDS
+    if (nc > 7) return launch_qk_long(in.dk, dt, fp, a, qa, p, lds, stream);
     if (in.dk == 32) return launch_qk_dk32(nc, dt, half, fp, a, qa, p, lds, stream);
     return launch_qk_dk64(nc, dt, half, fp, a, qa, p, lds, stream);
 }

@@ -209,11 +209,16 @@ hipError_t launch_qk_dk(int nc, int dtm, bool half, bool fp, const LisArgs& a, c
         case 4: return launch_qk_nc<DK, 4>(dtm, half, fp, a, qa, p, lds, stream);
         case 5: return launch_qk_nc<DK, 5>(dtm, half, fp, a, qa, p, lds, stream);
         case 6: return launch_qk_nc<DK, 6>(dtm, half, fp, a, qa, p, lds, stream);
-        default: return launch_qk_nc<DK, 7>(dtm, half, fp, a, qa, p, lds, stream);
+        case 7: return launch_qk_nc<DK, 7>(dtm, half, fp, a, qa, p, lds, stream);
+        default: return hipErrorInvalidValue;
     }
 }
 
 hipError_t launch_qk_dk32(int nc, int dtm, bool half, bool fp, const LisArgs& a, const QkArgs& qa,
+                          const LisLaunch& p, size_t lds, hipStream_t stream);
+// Rows of 8 to 20 chunks (lis_qk_long.hip): one workgroup of 12 wavefronts per
+// unit, three passes over K in LDS per tile.
+hipError_t launch_qk_long(int dk, int dtm, bool fp, const LisArgs& a, const QkArgs& qa,
                           const LisLaunch& p, size_t lds, hipStream_t stream);
 hipError_t launch_qk_dk64(int nc, int dtm, bool half, bool fp, const LisArgs& a, const QkArgs& qa,
                           const LisLaunch& p, size_t lds, hipStream_t stream);

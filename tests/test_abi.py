@@ -322,7 +322,7 @@ def test_qk_validation(lib):
 
     assert call(G=-1) == B.FQ_ERR_SHAPE
     assert call(Lk=0) == B.FQ_ERR_SHAPE
-    assert call(Lk=225) == B.FQ_ERR_SHAPE
+    assert call(Lk=641) == B.FQ_ERR_SHAPE
     assert call(d=65) == B.FQ_ERR_SHAPE
     assert call(d=0) == B.FQ_ERR_SHAPE
     assert call(dk=48) == B.FQ_ERR_SHAPE

@@ -53,8 +53,12 @@ SHAPES = [  # G, Lq, Lk, dk, d
     (16, 1, 1, 32, 16),
     (16, 16, 16, 64, 64),       # one half chunk
     (16, 17, 17, 64, 40),       # chunk of 17 keys
-    (8, 50, 224, 64, 64),       # largest supported row
+    (8, 50, 224, 64, 64),       # longest row held in registers
     (8, 33, 100, 32, 20),
+    (4, 40, 225, 64, 64),       # shortest row of the three-pass kernel
+    (3, 50, 577, 64, 64),       # ViT-L/16 at 384 px
+    (2, 33, 640, 32, 20),       # longest supported row
+    (2, 17, 300, 64, 48),
 ]
 
 
@@ -90,6 +94,21 @@ def test_qk_saturated_operands(fq, orc):
     s = 0.5
     got = host(fq.lis_attention_qk(dev(q), dev(k), dev(v), s, 127, -128))
     assert np.array_equal(got, orc.lis_attention_qk(q, k, v, s, 127, -128))
+
+
+def test_qk_long_rows_zero_points_and_bias(fq, orc):
+    """The three-pass kernel with asymmetric Q and K, a V zero point and a
+    per-head bias on rows of 577 keys."""
+    say("qk long zero points + bias")
+    _check(fq, orc, 4, 33, 577, 64, 64, 2.0 ** -10, sigma=25.0, zp_q=-20, zp_k=13, zp_v=3,
+           heads=2, bias=True, seed=17)
+    _check(fq, orc, 4, 20, 400, 32, 32, 1e-3, zp_q=9, zp_k=-4, seed=18)
+
+
+def test_qk_full_vit_large(fq, orc):
+    """The ViT-L/16 at 384 px attention shape: 256 units of 577 x 577, dk = d = 64."""
+    say("qk full vit_l")
+    _check(fq, orc, 256, 577, 577, 64, 64, 2.0 ** -10, seed=3)
 
 
 def test_qk_full_vit_base(fq, orc):
