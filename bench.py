@@ -32,14 +32,16 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 METRIC = "tokens/s and achieved HBM GB/s for PTF-LayerNorm + LIS attention, ViT-B bs64"
-TRAFFIC_WORKLOAD = "vit_base16_224_b64"
+BENCH_WORKLOAD = "vit_base16_224_b64"
 N_SETS = 4
 EVENT_SAMPLES = 64
 COPY_BYTES = 512 * 2 ** 20
 COPY_REPS = 3
-# Summary of the counter runs of the fused head; its traffic figure is used only
-# while the hash of the LIS sources matches the one recorded with it.
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "lis_attention_head_vit_base16_224_b64_traffic.txt")
+# Summary of the counter runs of a workload (profiles/traffic_<workload>.txt);
+# its traffic figure for the fused head is used only while the hash of the LIS
+# sources matches the one recorded with it.
+def traffic_file(workload):
+    return os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
 LIS_SOURCES = ["lis_device.h", "lis_attention.hip", "lis_inst_lo.hip", "lis_inst_hi.hip",
                "lis_inst_unit.hip", "fqvit_internal.h", "fqvit_launch.h"]
 
@@ -80,13 +82,14 @@ def lis_sources_sha256():
     return h.hexdigest()
 
 
-def recorded_traffic():
-    """HBM bytes per head launch from the counter summary, or None when the
-    summary is missing or was taken on other LIS sources."""
-    if not os.path.exists(TRAFFIC_FILE):
+def recorded_traffic(workload):
+    """HBM bytes per head launch from the workload's counter summary, or None
+    when the summary is missing or was taken on other LIS sources."""
+    path = traffic_file(workload)
+    if not os.path.exists(path):
         return None
     fields = {}
-    with open(TRAFFIC_FILE) as f:
+    with open(path) as f:
         for line in f:
             if ":" in line:
                 key, val = line.split(":", 1)
@@ -99,59 +102,135 @@ def recorded_traffic():
         return None
 
 
-def pmc_summary(fetch_dir, write_dir):
-    """Per-dispatch FETCH_SIZE / WRITE_SIZE (KiB) of the LayerNorm and head
-    kernels, scaled by the same counter on the calibration copies (the copy
-    dispatches after the last head dispatch, COPY_BYTES read and written each)."""
+def kernel_class(name):
+    """The entry point a dispatched kernel belongs to, from its name."""
+    if "lis_qk" in name:
+        return "lis_attention_qk"
+    if "fqvit::lis::" in name and "attn_v_shift" not in name:
+        return "lis_attention_head"
+    if "ln_" in name and "fqvit::" in name:
+        return "ptf_layernorm_int8"
+    for k in ("minmax_partial", "calib_params", "alpha_partial", "alpha_select"):
+        if k in name:
+            return "ptf_calibrate"
+    if "quantize_kernel" in name:
+        return "ptf_quantize_int8"
+    if "requant_kernel" in name:
+        return "requant_dyadic_int8"
+    return None
+
+
+def short_kernel_name(name):
+    """A kernel's name without its return type, anonymous namespace and parameters."""
+    return name.replace("void ", "").replace("(anonymous namespace)::", "").split("(")[0]
+
+
+def _counter_rows(d, counter=None):
     import csv
     import glob
+    rows = []
+    for fn in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        with open(fn) as f:
+            rows += [r for r in csv.DictReader(f) if counter is None or r["Counter_Name"] == counter]
+    rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+    return rows
+
+
+def pmc_summary(fetch_dir, write_dir, workload):
+    """Per-dispatch FETCH_SIZE / WRITE_SIZE (KiB) of every kernel of the hot
+    path and of the operations around it, averaged per kernel and summed per
+    entry point, scaled by the same counter on the calibration copies (the
+    first COPY_REPS copy dispatches after the timed steps, COPY_BYTES read and
+    written each)."""
+    import workloads as W
+    cfg = W.BY_NAME[workload]
 
     def load(d, counter):
-        rows = []
-        for fn in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
-            with open(fn) as f:
-                rows += [r for r in csv.DictReader(f) if r["Counter_Name"] == counter]
-        rows.sort(key=lambda r: int(r["Dispatch_Id"]))
-        groups = {"head": [], "ln": [], "copy": []}
-        def is_head(name):
-            return "fqvit::lis::" in name and "lis_qk_kernel" not in name
-
-        def is_ln(name):
-            return "fqvit::" in name and "ln_" in name
-
-        last_head = max((int(r["Dispatch_Id"]) for r in rows if is_head(r["Kernel_Name"])),
-                        default=-1)
+        rows = _counter_rows(d, counter)
+        last_head = max((int(r["Dispatch_Id"]) for r in rows
+                         if kernel_class(r["Kernel_Name"]) == "lis_attention_head"), default=-1)
+        per_kernel, copies = {}, []
         for r in rows:
             name, v = r["Kernel_Name"], float(r["Counter_Value"])
-            if is_head(name):
-                groups["head"].append(v)
-            elif is_ln(name):
-                groups["ln"].append(v)
+            cls = kernel_class(name)
+            if cls:
+                per_kernel.setdefault((cls, short_kernel_name(name)), []).append(v)
             elif ("copy" in name.lower() and int(r["Dispatch_Id"]) > last_head
-                  and len(groups["copy"]) < COPY_REPS):
-                groups["copy"].append(v)
-        return {k: (sum(v) / len(v) if v else float("nan"), len(v)) for k, v in groups.items()}
+                  and len(copies) < COPY_REPS):
+                copies.append(v)
+        return per_kernel, copies
 
-    fetch, write = load(fetch_dir, "FETCH_SIZE"), load(write_dir, "WRITE_SIZE")
+    fetch, fcopy = load(fetch_dir, "FETCH_SIZE")
+    write, wcopy = load(write_dir, "WRITE_SIZE")
     copy_kib = COPY_BYTES / 1024.0
-    f_scale = copy_kib / fetch["copy"][0]
-    w_scale = copy_kib / write["copy"][0]
-    cfg_bytes = algorithmic_bytes(__import__("workloads").BY_NAME["vit_base16_224_b64"])
-    out = []
-    out.append(f"calibration copy: {COPY_BYTES} B read + written per dispatch, "
-               f"FETCH_SIZE {fetch['copy'][0]:.1f} KiB (n={fetch['copy'][1]}), "
-               f"WRITE_SIZE {write['copy'][0]:.1f} KiB (n={write['copy'][1]})")
-    out.append(f"scale: fetch x{f_scale:.4f}, write x{w_scale:.4f}")
-    for key, alg in (("ln", cfg_bytes[0]), ("head", cfg_bytes[1])):
-        fb = fetch[key][0] * 1024.0 * f_scale
-        wb = write[key][0] * 1024.0 * w_scale
-        out.append(f"{key}: FETCH_SIZE {fetch[key][0]:.1f} KiB (n={fetch[key][1]}), "
-                   f"WRITE_SIZE {write[key][0]:.1f} KiB (n={write[key][1]}); scaled read {fb:.0f} B"
-                   f" + write {wb:.0f} B = {fb + wb:.0f} B per launch; algorithmic {alg} B"
-                   f" (ratio {(fb + wb) / alg:.3f})")
-        if key == "head":
-            out.append(f"traffic_bytes_per_launch: {fb + wb:.0f}")
+    f_scale = copy_kib / (sum(fcopy) / len(fcopy))
+    w_scale = copy_kib / (sum(wcopy) / len(wcopy))
+    ln_b, head_b = algorithmic_bytes(cfg)
+    n_el = cfg.T * cfg.channels
+    alg = {"ptf_layernorm_int8": ln_b, "lis_attention_head": head_b,
+           # q, k, v int8 (dk = d) and the int32 output
+           "lis_attention_qk": cfg.G * (cfg.Lq * cfg.d + 2 * cfg.Lk * cfg.d + 4 * cfg.Lq * cfg.d),
+           "ptf_calibrate": 2 * 4 * n_el + cfg.channels, "ptf_quantize_int8": 5 * n_el,
+           "requant_dyadic_int8": 5 * cfg.G * cfg.Lq * cfg.d}
+    out = [f"workload: {workload}",
+           f"calibration copy: {COPY_BYTES} B read + written per dispatch, FETCH_SIZE "
+           f"{sum(fcopy) / len(fcopy):.1f} KiB (n={len(fcopy)}), WRITE_SIZE "
+           f"{sum(wcopy) / len(wcopy):.1f} KiB (n={len(wcopy)})",
+           f"scale: fetch x{f_scale:.4f}, write x{w_scale:.4f}", ""]
+    totals = {}
+    for (cls, kname), fv in sorted(fetch.items()):
+        wv = write.get((cls, kname), [0.0])
+        fb = sum(fv) / len(fv) * 1024.0 * f_scale
+        wb = sum(wv) / len(wv) * 1024.0 * w_scale
+        out.append(f"{kname}: FETCH_SIZE {sum(fv) / len(fv):.1f} KiB (n={len(fv)}), WRITE_SIZE "
+                   f"{sum(wv) / len(wv):.1f} KiB; scaled read {fb:.0f} B + write {wb:.0f} B")
+        t = totals.setdefault(cls, [0.0, 0.0])
+        t[0] += fb
+        t[1] += wb
+    out.append("")
+    for cls, (fb, wb) in sorted(totals.items()):
+        out.append(f"{cls}: {fb + wb:.0f} B per call (read {fb:.0f} + write {wb:.0f}); algorithmic "
+                   f"{alg[cls]} B (ratio {(fb + wb) / alg[cls]:.3f})")
+    if "lis_attention_head" in totals:
+        out.append(f"traffic_bytes_per_launch: {sum(totals['lis_attention_head']):.0f}")
     out.append(f"lis_sources_sha256: {lis_sources_sha256()}")
+    print("\n".join(out))
+
+
+def sq_summary(dirs):
+    """Average of every collected counter per dispatch, per kernel, over
+    rocprofv3 --pmc output directories (the SQ cycle counters are device
+    totals in quad-cycles, summed over SIMDs)."""
+    acc = {}
+    for d in dirs:
+        for r in _counter_rows(d):
+            cls = kernel_class(r["Kernel_Name"])
+            if not cls:
+                continue
+            key = (cls, short_kernel_name(r["Kernel_Name"]))
+            acc.setdefault(key, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    out = []
+    for (cls, kname), cs in sorted(acc.items()):
+        n = max(len(v) for v in cs.values())
+        out.append(f"== {cls}: {kname} (n={n})")
+        for c, v in sorted(cs.items()):
+            out.append(f"   {c:28s} {sum(v) / len(v):18.1f}")
+    print("\n".join(out))
+
+
+def trace_summary(stats_csv):
+    """The kernel statistics of a rocprofv3 --kernel-trace --stats run, with
+    each kernel's entry point."""
+    import csv
+    with open(stats_csv) as f:
+        rows = list(csv.DictReader(f))
+    out = [f"{'kernel':<84}  {'entry point':<22} calls    avg us    min us    max us"]
+    for r in rows:
+        name = short_kernel_name(r["Name"])
+        cls = kernel_class(r["Name"]) or "-"
+        out.append(f"{name[:84]:<84}  {cls:<22} {int(r['Calls']):5d}  "
+                   f"{float(r['AverageNs']) / 1e3:8.2f}  {float(r['MinNs']) / 1e3:8.2f}  "
+                   f"{float(r['MaxNs']) / 1e3:8.2f}")
     print("\n".join(out))
 
 
@@ -169,7 +248,12 @@ def parse():
                         "(the known-size kernel that scales the traffic counters)")
     p.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                    help="no GPU: summarise two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) "
-                        "of this script with --copy-calibration and print the traffic per launch")
+                        "of this script with --copy-calibration on --config and print the "
+                        "traffic per call of every entry point")
+    p.add_argument("--sq-summary", nargs="+", metavar="DIR",
+                   help="no GPU: average every counter of rocprofv3 --pmc runs per kernel")
+    p.add_argument("--trace-summary", metavar="STATS_CSV",
+                   help="no GPU: the kernel statistics of a rocprofv3 --kernel-trace --stats run")
     return p.parse_args()
 
 
@@ -368,7 +452,13 @@ class HipEvents:
 def main():
     args = parse()
     if args.pmc_summary:
-        pmc_summary(*args.pmc_summary)
+        pmc_summary(*args.pmc_summary, args.config)
+        return
+    if args.sq_summary:
+        sq_summary(args.sq_summary)
+        return
+    if args.trace_summary:
+        trace_summary(args.trace_summary)
         return
     if args.gpus != 1:
         print(f"bench.py: the benchmark measures one GPU only (asked for --gpus {args.gpus}); "
@@ -456,8 +546,8 @@ def main():
 
     ln_bytes, head_bytes = algorithmic_bytes(cfg)
     achieved = head_bytes / (head_avg * 1e-3) / 1e9
-    # the counter summary covers the ViT-B/16 batch-64 workload only
-    traffic = recorded_traffic() if cfg.name == TRAFFIC_WORKLOAD else None
+    # from the workload's counter summary, while it describes these sources
+    traffic = recorded_traffic(cfg.name)
     if args.copy_calibration:
         src = torch.empty(COPY_BYTES // 4, dtype=torch.int32, device=dev).fill_(1)
         dst = torch.empty_like(src)
@@ -467,7 +557,7 @@ def main():
         torch.cuda.synchronize()
 
     result = {
-        "metric": METRIC if cfg.name == TRAFFIC_WORKLOAD else
+        "metric": METRIC if cfg.name == BENCH_WORKLOAD else
                   f"tokens/s and achieved HBM GB/s for PTF-LayerNorm + LIS attention, {cfg.name}",
         "value": cfg.T / (ms_step * 1e-3),
         "unit": "tokens/s",
