@@ -306,8 +306,9 @@ __global__ __launch_bounds__(kBlock) void ln_generic_kernel(LnArgs a) {
 // Row-batch kernel for rows of 256..1024 channels (C % 4 == 0, dword-aligned)
 // whose sums of squares fit 32 bits (C (255 2^K)^2 < 2^32).
 //
-// A wavefront owns a contiguous run of rows, taken four at a time; lane l owns
-// dwords l, l + 64, ... of each row (coalesced dword loads and stores).  The
+// A wavefront owns a contiguous run of rows, taken R = 1, 2 or 4 at a time (a
+// batch); lane l owns dwords l, l + 64, ... of each row (coalesced dword loads
+// and stores).  The
 // per-channel (gs, bs) pairs stay in LDS in [byte][dword] order, so that the
 // 16-byte reads of a wavefront are consecutive.  Per dword, with xu = x + 128 (the byte with
 // its sign bit flipped, 0..255) and u = zp_in + 128:
@@ -316,11 +317,11 @@ __global__ __launch_bounds__(kBlock) void ln_generic_kernel(LnArgs a) {
 //   M1 lane  += dot4(xu bytes, 2^alpha bytes), the -u sum_c 2^alpha part of
 //               every row being a per-lane constant
 //   M2 lane  += dot2(X^ pair, X^ pair), twice
-// The 4 x 2 per-row totals are reduced together: a 32-lane swap-add and a
-// 16-lane swap-add leave row j's partial sums in lanes 16 j .. 16 j + 15,
-// four row rotations finish them, and one evaluation of the square root and
-// the two divisions serves the four rows (lane group j).  The per-row factors
-// reach every lane as scalars.
+// The R x 2 per-row totals are reduced together: a 32-lane swap-add and a
+// 16-lane swap-add leave row j's partial sums in lane group j (64 / R lanes
+// from lane 64 j / R), four row rotations finish them, and one evaluation of
+// the square root and the two divisions serves the R rows.  The per-row
+// factors reach every lane as scalars.
 //
 // Output, when the row's factors fit (see ln_requant_fast): with
 // c = zp_out + 1/2 + 512, v = At X^ + (Bg + c) is exact (multiples of 2^-N1
@@ -328,8 +329,6 @@ __global__ __launch_bounds__(kBlock) void ln_generic_kernel(LnArgs a) {
 // (floor for v >= 0) and saturates, and a clamp to [qlo + 512, qhi + 512]
 // (both positive, so a negative v lands on the lower bound either way) gives
 // Y + 512, whose low byte is Y's.
-constexpr int kRowBatch = 4;
-
 typedef short short2_t __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ uint32_t swap_add32(uint32_t a, uint32_t b) {
@@ -380,12 +379,12 @@ __device__ __forceinline__ int ln_requant_rows(double A, double B, int xh, uint3
 // are not needed address past its end and return 0 without a memory access,
 // so every load is issued unconditionally and the compiler can count the
 // loads in flight across the batches.
-template <int W>
-__device__ __forceinline__ void load_rows(uint32_t (&xv)[kRowBatch][W],
+template <int W, int R>
+__device__ __forceinline__ void load_rows(uint32_t (&xv)[R][W],
                                           __amdgpu_buffer_rsrc_t xr, int64_t r0, int nr, int nd,
                                           int lane, const bool (&ok)[W]) {
 #pragma unroll
-    for (int j = 0; j < kRowBatch; ++j) {
+    for (int j = 0; j < R; ++j) {
 #pragma unroll
         for (int w = 0; w < W; ++w) {
             const int off = (j < nr && ok[w]) ? (int)(((r0 + j) * nd + lane + 64 * w) * 4) : INT_MIN;
@@ -407,20 +406,33 @@ struct RowsCtx {
     int lo512, hi512, qlo, qhi;
 };
 
-// Statistics of rows r0 .. r0 + nr - 1 (nr in 1..4) from their dwords xv: the
+// Statistics of rows r0 .. r0 + nr - 1 (nr in 1..R) from their dwords xv: the
 // packed X^ of each row, and the factors r, m of row j in lane group j.
-template <int W>
+template <int W, int R>
 struct RowsStats {
-    uint32_t hp[kRowBatch][2 * W];
+    uint32_t hp[R][2 * W];
     double r, m;
 };
 
-template <int W>
+// Lane group j's totals of row j: v[j] summed over the wavefront, for R rows.
+template <int R>
+__device__ __forceinline__ uint32_t rows_total(const uint32_t (&v)[R]) {
+    if constexpr (R == 4) return row16_sum(swap_add16(swap_add32(v[0], v[2]), swap_add32(v[1], v[3])));
+    else if constexpr (R == 2) {
+        const uint32_t h = swap_add32(v[0], v[1]);   // row j in lanes 32 j .. 32 j + 31
+        return row16_sum(swap_add16(h, h));
+    } else {
+        const uint32_t h = swap_add32(v[0], v[0]);
+        return row16_sum(swap_add16(h, h));
+    }
+}
+
+template <int W, int R>
 __device__ __forceinline__ void rows_stats(const LnArgs& a, const RowsCtx<W>& k,
-                                           const uint32_t (&xv)[kRowBatch][W], RowsStats<W>& st) {
-    uint32_t m1[kRowBatch], m2[kRowBatch];
+                                           const uint32_t (&xv)[R][W], RowsStats<W, R>& st) {
+    uint32_t m1[R], m2[R];
 #pragma unroll
-    for (int j = 0; j < kRowBatch; ++j) {
+    for (int j = 0; j < R; ++j) {
         m1[j] = k.m1init;
         m2[j] = 0;
 #pragma unroll
@@ -439,28 +451,27 @@ __device__ __forceinline__ void rows_stats(const LnArgs& a, const RowsCtx<W>& k,
             st.hp[j][2 * w + 1] = __builtin_bit_cast(uint32_t, h1);
         }
     }
-    // lane group j (lanes 16 j .. 16 j + 15) ends with row j's totals
-    const uint32_t t1 = row16_sum(swap_add16(swap_add32(m1[0], m1[2]), swap_add32(m1[1], m1[3])));
-    const uint32_t t2 = row16_sum(swap_add16(swap_add32(m2[0], m2[2]), swap_add32(m2[1], m2[3])));
+    const uint32_t t1 = rows_total<R>(m1);
+    const uint32_t t2 = rows_total<R>(m2);
     row_factors((int64_t)(int32_t)t1, (int64_t)t2, a.C, st.r, st.m);
 }
 
 // Output of the batch: packed bytes yo[j][w] of the rows whose factors are in
 // the fast range (fast[j]); the other rows are written here, element by
 // element (their bytes read again).
-template <int W>
+template <int W, int R>
 __device__ __forceinline__ void rows_output(const LnArgs& a, const RowsCtx<W>& k,
-                                            const double2* s_gb, const RowsStats<W>& st,
-                                            uint32_t (&yo)[kRowBatch][W], bool (&fast)[kRowBatch],
+                                            const double2* s_gb, const RowsStats<W, R>& st,
+                                            uint32_t (&yo)[R][W], bool (&fast)[R],
                                             int64_t r0, int nr, int nd, int lane) {
     // every flag set: rows_store writes exactly the rows flagged here
 #pragma unroll
-    for (int j = 0; j < kRowBatch; ++j) fast[j] = false;
+    for (int j = 0; j < R; ++j) fast[j] = false;
 #pragma unroll
-    for (int j = 0; j < kRowBatch; ++j) {
+    for (int j = 0; j < R; ++j) {
         if (j >= nr) break;
-        const double rj = readlane_f64(st.r, 16 * j);
-        const double mj = readlane_f64(st.m, 16 * j);
+        const double rj = readlane_f64(st.r, (64 / R) * j);
+        const double mj = readlane_f64(st.m, (64 / R) * j);
         const bool lane_fits = !k.zerol && k.gmaxl * rj < k.amax && k.gminl * rj >= k.amin;
         fast[j] = rj > 0.0 && __ballot(!lane_fits) == 0;
         if (fast[j]) {
@@ -498,12 +509,12 @@ __device__ __forceinline__ void rows_output(const LnArgs& a, const RowsCtx<W>& k
     }
 }
 
-template <int W>
-__device__ __forceinline__ void rows_store(const RowsCtx<W>& k, const uint32_t (&yo)[kRowBatch][W],
-                                           const bool (&fast)[kRowBatch], uint32_t* y32,
+template <int W, int R>
+__device__ __forceinline__ void rows_store(const RowsCtx<W>& k, const uint32_t (&yo)[R][W],
+                                           const bool (&fast)[R], uint32_t* y32,
                                            int64_t r0, int nd, int lane) {
 #pragma unroll
-    for (int j = 0; j < kRowBatch; ++j) {
+    for (int j = 0; j < R; ++j) {
         if (!fast[j]) continue;
         uint32_t* yr = y32 + (r0 + j) * nd + lane;
 #pragma unroll
@@ -512,13 +523,13 @@ __device__ __forceinline__ void rows_store(const RowsCtx<W>& k, const uint32_t (
     }
 }
 
-// A wavefront owns a contiguous run of rows and takes them NB batches of four
+// A wavefront owns a contiguous run of rows and takes them NB batches of R rows
 // at a time: the loads of all NB batches are issued first, then the batches
 // are computed in order, so the loads of the later ones stream in under the
 // arithmetic of the earlier ones.  No load is in flight across the loop's
 // back edge (a wait there would cover every outstanding load).  BLOCK threads
 // per workgroup; the grid sets the number of wavefronts per CU.
-template <int W, int BLOCK, int NB>
+template <int W, int R, int BLOCK, int NB>
 __global__ __launch_bounds__(BLOCK) void ln_rows_kernel(LnArgs a) {
     extern __shared__ double smem[];
     double2* s_gb = reinterpret_cast<double2*>(smem);        // (gs, bs) at [b][dword]
@@ -564,12 +575,12 @@ __global__ __launch_bounds__(BLOCK) void ln_rows_kernel(LnArgs a) {
             sa[b] = a.alpha[4 * sdw + b];
         }
     }
-    uint32_t xv[NB][kRowBatch][W];
+    uint32_t xv[NB][R][W];
     int nr[NB];
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
-        nr[i] = (int)max<int64_t>(0, min<int64_t>(kRowBatch, r1 - ra - kRowBatch * i));
-        load_rows<W>(xv[i], xr, ra + kRowBatch * i, nr[i], nd, lane, k.ok);
+        nr[i] = (int)max<int64_t>(0, min<int64_t>(R, r1 - ra - R * i));
+        load_rows<W, R>(xv[i], xr, ra + R * i, nr[i], nd, lane, k.ok);
     }
 
     const int u = a.zp_in + 128;
@@ -638,27 +649,27 @@ __global__ __launch_bounds__(BLOCK) void ln_rows_kernel(LnArgs a) {
     // (loads and stores share one counter: a store issued before that wait
     // would be waited for too).
     for (;;) {
-        uint32_t yo[kRowBatch][W];
-        bool fast[kRowBatch];
+        uint32_t yo[R][W];
+        bool fast[R];
         int64_t rprev = 0;
         bool pending = false;
 #pragma unroll
         for (int i = 0; i < NB; ++i) {
             if (nr[i] <= 0) break;
-            RowsStats<W> st;
-            rows_stats<W>(a, k, xv[i], st);
-            if (pending) rows_store<W>(k, yo, fast, y32, rprev, nd, lane);
-            rows_output<W>(a, k, s_gb, st, yo, fast, ra + kRowBatch * i, nr[i], nd, lane);
-            rprev = ra + kRowBatch * i;
+            RowsStats<W, R> st;
+            rows_stats<W, R>(a, k, xv[i], st);
+            if (pending) rows_store<W, R>(k, yo, fast, y32, rprev, nd, lane);
+            rows_output<W, R>(a, k, s_gb, st, yo, fast, ra + R * i, nr[i], nd, lane);
+            rprev = ra + R * i;
             pending = true;
         }
-        if (pending) rows_store<W>(k, yo, fast, y32, rprev, nd, lane);
-        ra += NB * kRowBatch;
+        if (pending) rows_store<W, R>(k, yo, fast, y32, rprev, nd, lane);
+        ra += NB * R;
         if (ra >= r1) break;
 #pragma unroll
         for (int i = 0; i < NB; ++i) {
-            nr[i] = (int)max<int64_t>(0, min<int64_t>(kRowBatch, r1 - ra - kRowBatch * i));
-            load_rows<W>(xv[i], xr, ra + kRowBatch * i, nr[i], nd, lane, k.ok);
+            nr[i] = (int)max<int64_t>(0, min<int64_t>(R, r1 - ra - R * i));
+            load_rows<W, R>(xv[i], xr, ra + R * i, nr[i], nd, lane, k.ok);
         }
     }
 }
@@ -666,29 +677,35 @@ __global__ __launch_bounds__(BLOCK) void ln_rows_kernel(LnArgs a) {
 // Workgroup size of the row-batch kernel.
 constexpr int kRowsBlock = 256;
 
-template <int W, int NB>
-hipError_t launch_rows_nb(const LnArgs& a, int wpc, hipStream_t stream) {
-    // one pass of NB batches per wavefront where the rows allow it, at most
-    // wpc wavefronts per CU
+template <int W, int R, int NB>
+hipError_t launch_rows_rb(const LnArgs& a, int wpc, hipStream_t stream) {
+    // one pass of NB batches of R rows per wavefront where the rows allow it,
+    // at most wpc wavefronts per CU
     constexpr int kWaves = kRowsBlock / 64;
-    const int64_t want = (a.T + NB * kRowBatch - 1) / (NB * kRowBatch);
+    const int64_t want = (a.T + NB * R - 1) / (NB * R);
     const int64_t waves = std::max<int64_t>(1, std::min<int64_t>(want, 256 * (int64_t)wpc));
     const int64_t blocks = (waves + kWaves - 1) / kWaves;
     const size_t lds = (size_t)a.C * 2 * sizeof(double) + (size_t)(a.C / 4) * 2 * sizeof(uint4);
-    launch_kernel(ln_rows_kernel<W, kRowsBlock, NB>, dim3((unsigned)blocks), dim3(kRowsBlock), lds,
-                  stream, a);
+    launch_kernel(ln_rows_kernel<W, R, kRowsBlock, NB>, dim3((unsigned)blocks), dim3(kRowsBlock),
+                  lds, stream, a);
     return hipGetLastError();
 }
 
-// Measured on the ViT-B/16 shape (12608 x 768, one MI355X): one batch per pass
-// at 12 wavefronts per CU 11.0-11.2 us; 8 per CU 12.1-13.2 us, 16 or 20 per CU
-// 12.4-12.6 us; two or three batches per pass (their loads issued together,
-// each batch's stores held back until the next batch's loads were waited for)
-// 13.0-13.5 and 18.0-18.4 us.  The kernel is bound by its vector-ALU issue
-// (the binary64 output), not by the latency the extra batches would hide.
+// Measured on the ViT-B/16 shape (12608 x 768, one MI355X): batches of four
+// rows, one per pass, at 12 wavefronts per CU 11.0-11.2 us; 8 per CU 12.1-13.2
+// us, 16 or 20 per CU 12.4-12.6 us; two or three batches of four per pass
+// (their loads issued together, each batch's stores held back until the next
+// batch's loads were waited for) 13.0-13.5 and 18.0-18.4 us.  Smaller batches,
+// whose earlier loads arrive sooner, at 8, 12 or 16 wavefronts per CU: two rows
+// with one, two or three batches per pass 12.4-14.3, 11.4-12.8 and 12.7-14.3
+// us, single rows with one, two or four batches 13.0-15.3, 13.0-14.8 and
+// 12.4-14.1 us (ViT-L/16, 9232 x 1024: all within 12.0-15.3 us, four-row
+// batches 12.4 us).  The kernel is bound by its vector-ALU issue (the
+// binary64 output, about 6.7 us of issue per SIMD), not by the latency that
+// smaller or more batches would hide.
 template <int W>
 hipError_t launch_rows(const LnArgs& a, hipStream_t stream) {
-    return launch_rows_nb<W, 1>(a, 12, stream);
+    return launch_rows_rb<W, 4, 1>(a, 12, stream);
 }
 
 template <int W>
