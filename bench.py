@@ -339,7 +339,9 @@ def cpu_baseline(cfg, inp, min_s=10.0, max_steps=12, max_threads=16):
 def extras(cfg, inp, out, fq, torch, reps=24, n_sets=8):
     """Kernel times of the operations on either side of the hot path, on the
     same workload: PTF calibration and quantization of the LayerNorm input
-    (float32 [T, C]) and the dyadic requantization of the head's int32 output.
+    (float32 [T, C]), the dyadic requantization of the head's int32 output,
+    the integer-only attention from int8 Q and K, and the unfused head
+    (lis_softmax_log4, then lis_attn_v_shift on its codes).
     Each is timed with the library's own kernel events (calibration: first to
     last of its four kernels) over `n_sets` rotated inputs."""
     import numpy as np
@@ -364,7 +366,22 @@ def extras(cfg, inp, out, fq, torch, reps=24, n_sets=8):
         qk_in = W.qk_inputs(G, Lq, Lk, dk, d, seed=100 + i, sigma=19.6)
         qks.append({key: torch.from_numpy(qk_in[key]).to(dev) for key in ("q", "k", "v")})
     out_qk = torch.empty((G, Lq, d), dtype=torch.int32, device=dev)
+    # the unfused path on the head's inputs: Log-Int-Softmax codes to HBM, then
+    # the standalone BitShift product reading them back
+    a_in = inp["attn"]
+    lg0 = torch.from_numpy(a_in["logits"]).to(dev)
+    lgs = [lg0] + [lg0.clone() for _ in range(1, 4)]
+    v_av = torch.from_numpy(a_in["v"]).to(dev)
+    bias = torch.from_numpy(a_in["bias"]).to(dev) if a_in["bias"] is not None else None
+    ld = fq.codes_ld(Lk, a_in["bits"])
+    codes = [torch.empty((G, Lq, ld), dtype=torch.uint8, device=dev) for _ in lgs]
+    out_av = torch.empty((G, Lq, d), dtype=torch.int32, device=dev)
     calls = {
+        "lis_softmax_log4": [fq.lis_softmax_log4(lg, a_in["s_logit"], a_in["bits"], a_in["exp_n"],
+                                                 bias=bias, codes=cd, prepare=True)
+                             for lg, cd in zip(lgs, codes)],
+        "lis_attn_v_shift": [fq.lis_attn_v_shift(cd, v_av, Lk, a_in["zp_v"], a_in["bits"],
+                                                 out=out_av, prepare=True) for cd in codes],
         "lis_attention_qk": [fq.lis_attention_qk(t["q"], t["k"], t["v"], 2.0 ** -10, out=out_qk,
                                                  prepare=True) for t in qks],
         "ptf_calibrate": [fq.ptf_calibrate(x, 8, 3, s, zp, alpha, ws, prepare=True) for x in xs],
@@ -373,7 +390,10 @@ def extras(cfg, inp, out, fq, torch, reps=24, n_sets=8):
                                 for o in outs],
     }
     n_el = T * C
-    nbytes = {"lis_attention_qk": G * (Lq * dk + Lk * dk + Lk * d + 4 * Lq * d),
+    n_bias = 4 * bias.numel() if bias is not None else 0
+    nbytes = {"lis_softmax_log4": 4 * G * Lq * Lk + n_bias + G * Lq * ld,
+              "lis_attn_v_shift": G * Lq * ld + G * Lk * d + 4 * G * Lq * d,
+              "lis_attention_qk": G * (Lq * dk + Lk * dk + Lk * d + 4 * Lq * d),
               "ptf_calibrate": 2 * 4 * n_el + C,          # x read twice (min/max, then alpha)
               "ptf_quantize_int8": 4 * n_el + n_el,       # float in, int8 out
               "requant_dyadic_int8": 5 * out.numel()}     # int32 in, int8 out
@@ -386,7 +406,7 @@ def extras(cfg, inp, out, fq, torch, reps=24, n_sets=8):
         ev = HipEvents(reps)
         for i in range(reps):
             time_next(*ev.pairs[i])
-            cs[i % n_sets]()
+            cs[i % len(cs)]()
         torch.cuda.synchronize()
         us = sum(ev.elapsed_ms(i) for i in range(reps)) / reps * 1e3
         ev.close()
@@ -409,6 +429,7 @@ def extras(cfg, inp, out, fq, torch, reps=24, n_sets=8):
     res["device_copy"] = {"us": us, "bytes_read_and_written": 2 * COPY_BYTES,
                           "gbs": 2 * COPY_BYTES / (us * 1e-6) / 1e9}
     del src, dst
+    del lgs, codes
     res["shapes"] = (f"x float32 [{T}, {C}], K = 3, b = 8; requant of int32 {list(out.shape)};"
                      f" qk: q [{G}, {Lq}, {dk}], k [{G}, {Lk}, {dk}], v [{G}, {Lk}, {d}] int8,"
                      f" s_logit 2^-10")
@@ -479,6 +500,20 @@ def main():
 
     def to_dev(x):
         return torch.from_numpy(np.ascontiguousarray(x)).to(dev)
+
+    if not cfg.alpha_uniform:
+        # The LayerNorm input as the method makes it, before the timed region:
+        # the float activations calibrated by the library (s, zp of eq. 9-10,
+        # each channel's alpha the argmin of eq. 11) and PTF-quantized (eq. 8).
+        # The CPU baseline takes the same integers.
+        xf = to_dev(ln["x_float"].astype(np.float32))
+        s_d, zp_d, al_d = fq.ptf_calibrate(xf, 8, ln["K"])
+        xq_d = fq.ptf_quantize_int8(xf, s_d, zp_d, al_d, 8)
+        torch.cuda.synchronize()
+        ln = dict(ln, x_q=xq_d.cpu().numpy(), alpha=al_d.cpu().numpy(),
+                  zp_in=int(zp_d.cpu().numpy()[0]), calibrated=True)
+        inp = dict(inp, ln=ln)
+        del xf, xq_d
 
     base = {
         "x": to_dev(ln["x_q"]), "alpha": to_dev(ln["alpha"]), "gamma": to_dev(ln["gamma"]),
@@ -576,6 +611,9 @@ def main():
                         f" 4-bit codes",
             "tokens_per_step": cfg.T,
             "input_sets_rotated": N_SETS,
+            "ln_input": ("PTF int8 from the library's calibration (eq. 9-11) and quantizer (eq. 8) "
+                         "of the float activations" if ln.get("calibrated") else
+                         "PTF int8 with per-channel factors drawn uniformly in {0..K}"),
         },
         "step_gbs": (ln_bytes + head_bytes) / (ms_step * 1e-3) / 1e9,
         "step_hbm_frac": (ln_bytes + head_bytes) / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS,

@@ -138,7 +138,8 @@ fq_status lis_softmax_log4(const int32_t* logits, int64_t G, int32_t Lq, int32_t
  *   bits    b in [1, 4] (shifts of at most 15).
  *   out     [G, Lq, d] int32, scale s_V / 2^(2^b - 1).
  * The sum is exact; it wraps modulo 2^32 only if it leaves int32, which codes
- * produced by Log-Int-Softmax never do for Lk <= 4096.
+ * produced by Log-Int-Softmax never do for Lk <= 4096.  Codes above 2^b - 1
+ * (never written by lis_softmax_log4) give an unspecified result.
  * Errors: FQ_ERR_NULL, FQ_ERR_SHAPE (G or Lq < 0, Lk outside [1, 4096], d
  * outside [1, 256], ld_codes < ceil(Lk/2)), FQ_ERR_PARAM (bits, zp_v).
  */

@@ -14,7 +14,7 @@ LIB = os.path.join(HERE, "libfqvit.so")
 SOURCES = ["ptf_layernorm.hip", "lis_attention.hip", "lis_inst_lo.hip", "lis_inst_hi.hip",
            "lis_inst_unit.hip", "ptf_quant.hip", "lis_qk.hip", "lis_qk_dk32.hip",
            "lis_qk_dk64.hip", "lis_long_lo.hip", "lis_long_hi.hip",
-           "lis_qk_long.hip",
+           "lis_qk_long.hip", "lis_attn_v.hip",
            "fqvit_abi.cpp"]
 OBJDIR = os.path.join(HERE, "_build")
 

@@ -105,6 +105,21 @@ struct AvArgs {
 
 hipError_t launch_attn_v_shift(const AvArgs& a, hipStream_t stream);
 
+// The same product on the int8 matrix cores (rows of up to kAvMfmaMaxLk keys,
+// d <= 64); hipErrorNotSupported for other shapes.
+constexpr int kAvMfmaMaxLk = 1024;
+struct AvMfma {
+    uint32_t lut[3][4];   // P_k bytes for codes 0..15, four per dword
+    int kp;               // keys padded to a multiple of 64
+    int nks;              // kp / 64
+    int ldv;              // LDS row stride of V^T in bytes (kp + 16)
+    int ntiles;           // 16-row tiles per unit
+    int unit_bytes;       // code bytes a unit spans: (Lq - 1) ld_codes + ceil(Lk / 2)
+    int vec_out;          // 16-byte output stores (d % 4 == 0, 16-byte aligned out)
+    int vec_v;            // V rows read as 16-byte units (d % 16 == 0, 16-byte aligned V)
+};
+hipError_t launch_attn_v_mfma(const AvArgs& a, hipStream_t stream);
+
 // BitShift product for codes of any width: int64 output at scale s_V / 2^W.
 struct AvWideArgs {
     const uint8_t* codes;

@@ -285,6 +285,62 @@ def test_attn_v_shift_any_codes(fq, orc):
         assert np.array_equal(got, orc.lis_attn_v_shift(codes, v, zp_v=-3, bits=bits, Lk=65))
 
 
+# The product on the int8 matrix cores (rows of up to 1024 keys, d <= 64):
+# code rows that start at every byte alignment and with padded strides, key
+# counts on and around the 64-key steps, one- to four-range splits of P
+# (bits 1..4), row counts that leave ragged tiles, every zero point sign;
+# rows of more than 1024 keys or d > 64 take the vector-ALU kernel.
+AV_MFMA = [(3, 33, 64, 64, 4, 0, 5), (2, 17, 65, 48, 4, 1, -128), (2, 40, 127, 20, 3, 2, 127),
+           (5, 16, 128, 64, 2, 3, 0), (2, 9, 1024, 32, 4, 5, -1), (3, 20, 300, 64, 1, 0, 9),
+           (2, 50, 197, 33, 4, 7, -4), (2, 3, 1025, 64, 4, 0, 2), (2, 10, 200, 80, 4, 1, 3)]
+
+
+@pytest.mark.parametrize("G,Lq,Lk,d,bits,shift,zp", AV_MFMA)
+def test_attn_v_shift_layouts(fq, orc, G, Lq, Lk, d, bits, shift, zp):
+    """Arbitrary codes of b bits in a buffer whose rows start `shift` bytes
+    into an allocation and are `shift` bytes longer than ceil(Lk/2) (the
+    bytes between rows and the unused high nibble of an odd row hold
+    garbage)."""
+    import torch
+    say("av layouts", G, Lq, Lk, d, bits, shift, zp)
+    rng = np.random.default_rng(Lk * 7 + d + bits)
+    nb = (Lk + 1) // 2
+    ld = nb + shift
+    codes = rng.integers(0, 2 ** bits, size=(G, Lq, Lk))
+    packed = rng.integers(0, 256, size=(G, Lq, ld)).astype(np.uint8)
+    packed[..., :nb] = 0
+    for j in range(Lk):
+        packed[..., j // 2] |= (codes[..., j] << (4 * (j % 2))).astype(np.uint8)
+    if Lk % 2:
+        packed[..., nb - 1] |= (rng.integers(0, 16, size=(G, Lq)) << 4).astype(np.uint8)
+    v = rng.integers(-128, 128, size=(G, Lk, d)).astype(np.int8)
+    buf = torch.zeros(G * Lq * ld + shift + 64, dtype=torch.uint8, device="cuda")
+    buf[shift:shift + G * Lq * ld] = dev(packed.reshape(-1))
+    view = buf[shift:shift + G * Lq * ld].view(G, Lq, ld)
+    got = host(fq.lis_attn_v_shift(view, dev(v), Lk, zp_v=zp, bits=bits))
+    assert np.array_equal(got, orc.lis_attn_v_shift(packed, v, zp_v=zp, bits=bits, Lk=Lk))
+
+
+def test_attn_v_shift_full_vit_base(fq, orc):
+    """The unfused head of the ViT-B/16 batch-64 workload: GPU codes, then the
+    standalone product, against the oracle on every unit (threads)."""
+    import concurrent.futures as cf
+    import os
+    say("av full vit_b")
+    cfg = W.BY_NAME["vit_base16_224_b64"]
+    a = W.config_inputs(cfg, "attn")["attn"]
+    codes = fq.lis_softmax_log4(dev(a["logits"]), a["s_logit"])
+    got = host(fq.lis_attn_v_shift(codes, dev(a["v"]), cfg.Lk, zp_v=a["zp_v"]))
+    ch = host(codes)
+    parts = np.array_split(np.arange(cfg.G), min(16, os.cpu_count() or 1))
+    def one(ix):
+        return orc.lis_attn_v_shift(np.ascontiguousarray(ch[ix]), np.ascontiguousarray(a["v"][ix]),
+                                    zp_v=a["zp_v"], Lk=cfg.Lk)
+    with cf.ThreadPoolExecutor(len(parts)) as ex:
+        ref = np.concatenate(list(ex.map(one, parts)))
+    assert np.array_equal(got, ref)
+
+
 def _stored_codes(codes, bits):
     """[..., Lk] codes -> stored form (nibbles for bits <= 4, bytes above)."""
     if bits > 4:
