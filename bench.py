@@ -102,12 +102,27 @@ def recorded_traffic(workload):
         return None
 
 
+def _lis_fused(name):
+    """Whether a Log-Int-Softmax kernel instance is the fused head (its FUSED
+    template argument: second of lis_unit_kernel and lis_kernel, first of
+    lis_kernel_stream; the long-row kernel is fused only)."""
+    if "lis_long_kernel" in name:
+        return True
+    args = name.split("<", 1)[1].split(">", 1)[0].split(",")
+    pos = 0 if "lis_kernel_stream" in name else 1
+    return args[pos].strip() == "true"
+
+
 def kernel_class(name):
     """The entry point a dispatched kernel belongs to, from its name."""
     if "lis_qk" in name:
         return "lis_attention_qk"
-    if "fqvit::lis::" in name and "attn_v_shift" not in name:
-        return "lis_attention_head"
+    if "attn_v_shift_wide" in name:
+        return "lis_attn_v_shift_wide"
+    if "attn_v_shift" in name or "attn_v_mfma" in name:
+        return "lis_attn_v_shift"
+    if "fqvit::lis::" in name:
+        return "lis_attention_head" if _lis_fused(name) else "lis_softmax_log4"
     if "ln_" in name and "fqvit::" in name:
         return "ptf_layernorm_int8"
     for k in ("minmax_partial", "calib_params", "alpha_partial", "alpha_select"):
@@ -167,7 +182,11 @@ def pmc_summary(fetch_dir, write_dir, workload):
     w_scale = copy_kib / (sum(wcopy) / len(wcopy))
     ln_b, head_b = algorithmic_bytes(cfg)
     n_el = cfg.T * cfg.channels
+    nbc = (cfg.Lk + 1) // 2                      # packed 4-bit code bytes per row
+    n_bias = 4 * cfg.heads * cfg.Lq * cfg.Lk if cfg.bias else 0
     alg = {"ptf_layernorm_int8": ln_b, "lis_attention_head": head_b,
+           "lis_softmax_log4": 4 * cfg.G * cfg.Lq * cfg.Lk + n_bias + cfg.G * cfg.Lq * nbc,
+           "lis_attn_v_shift": cfg.G * (cfg.Lq * nbc + cfg.Lk * cfg.d + 4 * cfg.Lq * cfg.d),
            # q, k, v int8 (dk = d) and the int32 output
            "lis_attention_qk": cfg.G * (cfg.Lq * cfg.d + 2 * cfg.Lk * cfg.d + 4 * cfg.Lq * cfg.d),
            "ptf_calibrate": 2 * 4 * n_el + cfg.channels, "ptf_quantize_int8": 5 * n_el,
