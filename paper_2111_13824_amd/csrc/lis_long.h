@@ -33,8 +33,10 @@
 namespace fqvit {
 namespace lis {
 
+// Measured on ViT-L/16 at 384 px (256 x 577 x 577, one MI355X): 8 wavefronts
+// with 2, 4, 6 or 8 chunks in flight 122-131 us, all within noise of each
+// other; 12 wavefronts (168 VGPRs) spill 115 to 172 registers.
 constexpr int kLongWaves = 8;                  // 2 wavefronts per SIMD (256 VGPRs)
-constexpr int kLongBlock = 64 * kLongWaves;
 constexpr int kLongPF = 4;                     // chunks in flight per wavefront
 constexpr int kLongMinNC = 10;
 constexpr int kLongMaxNC = 20;
@@ -85,14 +87,14 @@ __device__ __forceinline__ void long_convert(uint32_t (&pk)[4], const int (&x)[8
         pk[w] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pk_i16(d[2 * w], d[2 * w + 1]));
 }
 
-// Loads and converts all NC chunks of one tile (a window of kLongPF chunks in
+// Loads and converts all NC chunks of one tile (a window of PF chunks in
 // flight); returns the row's delta (lane-group uniform).
-template <int NC>
+template <int NC, int PF>
 __device__ __forceinline__ int long_load_tile(uint32_t (&pk)[NC][4], const LongRows& lr, int roff,
                                               int kg, uint32_t valid) {
-    int raw[kLongPF][8];
+    int raw[PF][8];
 #pragma unroll
-    for (int q = 0; q < kLongPF; ++q) long_load(raw[q], lr, roff, q, kg);
+    for (int q = 0; q < PF; ++q) long_load(raw[q], lr, roff, q, kg);
     int m0 = 0, rmax = INT_MIN;
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
@@ -102,9 +104,9 @@ __device__ __forceinline__ int long_load_tile(uint32_t (&pk)[NC][4], const LongR
             for (int t = 1; t < 8; ++t) mx = max(mx, raw[0][t]);
             m0 = row4_max(mx);
         }
-        if (c == NC - 1) long_convert<true>(pk[c], raw[c % kLongPF], m0, rmax, valid);
-        else long_convert<false>(pk[c], raw[c % kLongPF], m0, rmax, valid);
-        if (c + kLongPF < NC) long_load(raw[c % kLongPF], lr, roff, c + kLongPF, kg);
+        if (c == NC - 1) long_convert<true>(pk[c], raw[c % PF], m0, rmax, valid);
+        else long_convert<false>(pk[c], raw[c % PF], m0, rmax, valid);
+        if (c + PF < NC) long_load(raw[c % PF], lr, roff, c + PF, kg);
     }
     return row4_max(rmax);
 }
@@ -195,8 +197,9 @@ __device__ void long_tile_exact(f32x4 (&acc)[DTMAX], const RowPtrs& rp, const Li
     }
 }
 
-template <int NC, int DTMAX, bool HALF>
-__global__ __launch_bounds__(kLongBlock) void lis_long_kernel(LisArgs a, LisLaunch p) {
+// WAVES wavefronts per workgroup, PF chunks in flight per wavefront.
+template <int NC, int DTMAX, bool HALF, int WAVES, int PF>
+__global__ __launch_bounds__(64 * WAVES) void lis_long_kernel(LisArgs a, LisLaunch p) {
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
     // LDS: the I-Exp table at offset 0 (so that 4 u is its entry's address),
     // then V^T
@@ -214,9 +217,9 @@ __global__ __launch_bounds__(kLongBlock) void lis_long_kernel(LisArgs a, LisLaun
     k.d_ln2 &= 0xFFFFFFu;
     k.magic &= 0xFFFFFFu;
 
-    long_stage_vt<DTMAX, kLongBlock>(vt, p.ld, a.v + g * (int64_t)Lk * a.d, Lk, a.d, 32 * NC, a.zp_v,
+    long_stage_vt<DTMAX, 64 * WAVES>(vt, p.ld, a.v + g * (int64_t)Lk * a.d, Lk, a.d, 32 * NC, a.zp_v,
                                      p.vec_ok);
-    for (uint32_t u = threadIdx.x; u <= k.u_max; u += kLongBlock) tab[u] = __float_as_uint(iexp_fu(u, k));
+    for (uint32_t u = threadIdx.x; u <= k.u_max; u += 64 * WAVES) tab[u] = __float_as_uint(iexp_fu(u, k));
     __syncthreads();
 
     LongRows lr;
@@ -243,11 +246,11 @@ __global__ __launch_bounds__(kLongBlock) void lis_long_kernel(LisArgs a, LisLaun
     uint32_t pk[NC][4];
     int delta = 0;
     bool have = false;
-    for (int tile = wave; tile < p.ntiles; tile += kLongWaves) {
+    for (int tile = wave; tile < p.ntiles; tile += WAVES) {
         const int i0 = 16 * tile;
         const int i = min(i0 + r, a.Lq - 1);
-        if (!have) delta = long_load_tile<NC>(pk, lr, i * Lk * 4, kg, valid);
-        const int next = tile + kLongWaves;
+        if (!have) delta = long_load_tile<NC, PF>(pk, lr, i * Lk * 4, kg, valid);
+        const int next = tile + WAVES;
         const bool has_next = next < p.ntiles;
         f32x4 acc[DTMAX];
 #pragma unroll
@@ -302,9 +305,9 @@ __global__ __launch_bounds__(kLongBlock) void lis_long_kernel(LisArgs a, LisLaun
         // codes and the product, the next tile streaming in
         const int inext = min(16 * next + r, a.Lq - 1);
         const int roffn = has_next ? inext * Lk * 4 : -1;
-        int raw[kLongPF][8];
+        int raw[PF][8];
 #pragma unroll
-        for (int q = 0; q < kLongPF; ++q) long_load(raw[q], lr, roffn, q, kg);
+        for (int q = 0; q < PF; ++q) long_load(raw[q], lr, roffn, q, kg);
         int m0n = 0, rmaxn = INT_MIN;
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
@@ -319,26 +322,26 @@ __global__ __launch_bounds__(kLongBlock) void lis_long_kernel(LisArgs a, LisLaun
                               (ex[4] | (ex[5] << 16)) << 7, (ex[6] | (ex[7] << 16)) << 7};
             if (HALF && c == NC - 1) chunk_mfma<DTMAX, true>(acc, pb, vt, p.ld, c, r, kg);
             else chunk_mfma<DTMAX, false>(acc, pb, vt, p.ld, c, r, kg);
-            // the next tile's chunk c - kLongPF + 1 into the registers chunk
+            // the next tile's chunk c - PF + 1 into the registers chunk
             // c has just freed
-            const int j = c - kLongPF + 1 >= 0 ? c - kLongPF + 1 : 0;
-            if (c - kLongPF + 1 >= 0) {
+            const int j = c - PF + 1 >= 0 ? c - PF + 1 : 0;
+            if (c - PF + 1 >= 0) {
                 if (j == 0) {
                     int mx = raw[0][0];
 #pragma unroll
                     for (int t = 1; t < 8; ++t) mx = max(mx, raw[0][t]);
                     m0n = row4_max(mx);
                 }
-                if (j == NC - 1) long_convert<true>(pk[j], raw[j % kLongPF], m0n, rmaxn, valid);
-                else long_convert<false>(pk[j], raw[j % kLongPF], m0n, rmaxn, valid);
-                if (j + kLongPF < NC) long_load(raw[j % kLongPF], lr, roffn, j + kLongPF, kg);
+                if (j == NC - 1) long_convert<true>(pk[j], raw[j % PF], m0n, rmaxn, valid);
+                else long_convert<false>(pk[j], raw[j % PF], m0n, rmaxn, valid);
+                if (j + PF < NC) long_load(raw[j % PF], lr, roffn, j + PF, kg);
             }
             __builtin_amdgcn_sched_barrier(0);
         }
 #pragma unroll
-        for (int j = NC - kLongPF + 1; j < NC; ++j) {
-            if (j == NC - 1) long_convert<true>(pk[j], raw[j % kLongPF], m0n, rmaxn, valid);
-            else long_convert<false>(pk[j], raw[j % kLongPF], m0n, rmaxn, valid);
+        for (int j = NC - PF + 1; j < NC; ++j) {
+            if (j == NC - 1) long_convert<true>(pk[j], raw[j % PF], m0n, rmaxn, valid);
+            else long_convert<false>(pk[j], raw[j % PF], m0n, rmaxn, valid);
         }
         store_out<DTMAX>(acc, a, g, i0, r, kg);
         delta = row4_max(rmaxn);
@@ -347,12 +350,12 @@ __global__ __launch_bounds__(kLongBlock) void lis_long_kernel(LisArgs a, LisLaun
 }
 
 // Launch for exactly NC chunks (kLongMinNC <= NC <= kLongMaxNC), DTMAX 2 or 4.
-template <int NC>
+template <int NC, int WAVES = kLongWaves, int PF = kLongPF>
 hipError_t launch_long_nc(int dtm, bool half, const LisArgs& a, const LisLaunch& p, size_t lds,
                           hipStream_t s) {
-#define FQ_LONG(DTM, HALF)                                                                \
-    launch_kernel(lis_long_kernel<NC, DTM, HALF>, dim3((unsigned)a.G), dim3(kLongBlock), lds, \
-                  s, a, p)
+#define FQ_LONG(DTM, HALF)                                                              \
+    launch_kernel(lis_long_kernel<NC, DTM, HALF, WAVES, PF>, dim3((unsigned)a.G),         \
+                  dim3(64 * WAVES), lds, s, a, p)
     if (dtm == 2) {
         if (half) FQ_LONG(2, true);
         else FQ_LONG(2, false);
