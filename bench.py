@@ -395,12 +395,21 @@ def extras(cfg, inp, out, fq, torch, reps=24, n_sets=8):
     ld = fq.codes_ld(Lk, a_in["bits"])
     codes = [torch.empty((G, Lq, ld), dtype=torch.uint8, device=dev) for _ in lgs]
     out_av = torch.empty((G, Lq, d), dtype=torch.int32, device=dev)
+    codes8 = [torch.empty((G, Lq, Lk), dtype=torch.uint8, device=dev) for _ in range(2)]
+    out_w = torch.empty((G, Lq, d), dtype=torch.int64, device=dev)
     calls = {
         "lis_softmax_log4": [fq.lis_softmax_log4(lg, a_in["s_logit"], a_in["bits"], a_in["exp_n"],
                                                  bias=bias, codes=cd, prepare=True)
                              for lg, cd in zip(lgs, codes)],
         "lis_attn_v_shift": [fq.lis_attn_v_shift(cd, v_av, Lk, a_in["zp_v"], a_in["bits"],
                                                  out=out_av, prepare=True) for cd in codes],
+        # the 8/8/8 setting: 8-bit codes (a byte each), then the wide product
+        "lis_softmax_log4_b8": [fq.lis_softmax_log4(lg, a_in["s_logit"], 8, a_in["exp_n"],
+                                                    bias=bias, codes=cd, prepare=True)
+                                for lg, cd in zip(lgs, codes8)],
+        "lis_attn_v_shift_wide_b8": [fq.lis_attn_v_shift_wide(cd, v_av, Lk, a_in["zp_v"], 8,
+                                                              out=out_w, prepare=True)
+                                     for cd in codes8],
         "lis_attention_qk": [fq.lis_attention_qk(t["q"], t["k"], t["v"], 2.0 ** -10, out=out_qk,
                                                  prepare=True) for t in qks],
         "ptf_calibrate": [fq.ptf_calibrate(x, 8, 3, s, zp, alpha, ws, prepare=True) for x in xs],
@@ -412,6 +421,8 @@ def extras(cfg, inp, out, fq, torch, reps=24, n_sets=8):
     n_bias = 4 * bias.numel() if bias is not None else 0
     nbytes = {"lis_softmax_log4": 4 * G * Lq * Lk + n_bias + G * Lq * ld,
               "lis_attn_v_shift": G * Lq * ld + G * Lk * d + 4 * G * Lq * d,
+              "lis_softmax_log4_b8": 4 * G * Lq * Lk + n_bias + G * Lq * Lk,
+              "lis_attn_v_shift_wide_b8": G * Lq * Lk + G * Lk * d + 8 * G * Lq * d,
               "lis_attention_qk": G * (Lq * dk + Lk * dk + Lk * d + 4 * Lq * d),
               "ptf_calibrate": 2 * 4 * n_el + C,          # x read twice (min/max, then alpha)
               "ptf_quantize_int8": 4 * n_el + n_el,       # float in, int8 out
@@ -448,7 +459,7 @@ def extras(cfg, inp, out, fq, torch, reps=24, n_sets=8):
     res["device_copy"] = {"us": us, "bytes_read_and_written": 2 * COPY_BYTES,
                           "gbs": 2 * COPY_BYTES / (us * 1e-6) / 1e9}
     del src, dst
-    del lgs, codes
+    del lgs, codes, codes8, out_w
     res["shapes"] = (f"x float32 [{T}, {C}], K = 3, b = 8; requant of int32 {list(out.shape)};"
                      f" qk: q [{G}, {Lq}, {dk}], k [{G}, {Lk}, {dk}], v [{G}, {Lk}, {d}] int8,"
                      f" s_logit 2^-10")

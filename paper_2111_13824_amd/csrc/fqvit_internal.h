@@ -106,7 +106,8 @@ struct AvArgs {
 hipError_t launch_attn_v_shift(const AvArgs& a, hipStream_t stream);
 
 // The same product on the int8 matrix cores (rows of up to kAvMfmaMaxLk keys,
-// d <= 64); hipErrorNotSupported for other shapes.
+// d <= 64); hipErrorNotSupported for other shapes.  AvMfma: its launch
+// parameters (both products).
 constexpr int kAvMfmaMaxLk = 1024;
 struct AvMfma {
     uint32_t lut[3][4];   // P_k bytes for codes 0..15, four per dword
@@ -134,6 +135,9 @@ struct AvWideArgs {
 };
 
 hipError_t launch_attn_v_shift_wide(const AvWideArgs& a, hipStream_t stream);
+// The wide product on the int8 matrix cores (same shape limits as
+// launch_attn_v_mfma); hipErrorNotSupported for other shapes.
+hipError_t launch_attn_v_wide_mfma(const AvWideArgs& a, hipStream_t stream);
 
 // ---------------------------------------------------------------------------
 // PTF calibration / quantization and dyadic requantization

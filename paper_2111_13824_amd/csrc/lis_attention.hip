@@ -423,6 +423,8 @@ hipError_t launch_attn_v_shift(const AvArgs& a, hipStream_t stream) {
 
 hipError_t launch_attn_v_shift_wide(const AvWideArgs& a, hipStream_t stream) {
     using lis::kBlock;
+    const hipError_t mf = launch_attn_v_wide_mfma(a, stream);
+    if (mf != hipErrorNotSupported) return mf;
     int tpr = 1;
     while (16 * tpr < a.d) tpr <<= 1;          // threads per row, 16 columns each
     const int rows = kBlock / tpr;
