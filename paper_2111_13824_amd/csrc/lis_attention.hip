@@ -349,6 +349,8 @@ hipError_t launch_lis(const LisArgs& a, hipStream_t stream) {
     const size_t out_lds = p.out_vec ? (size_t)4 * 16 * (p.dpad + 4) * sizeof(int32_t) : 0;
     p.n_logits = a.G * (int64_t)a.Lq * a.Lk;
     p.n_bias = a.bias ? (int64_t)a.Hb * a.Lq * a.Lk : 0;
+    p.tab_bytes = 0;
+    p.codes_ldw = 0;
     const int64_t blocks = a.G * (int64_t)p.ntiles;
     const dim3 grid((unsigned)blocks);
     const bool fp = a.k.fp_ok != 0;
@@ -363,8 +365,16 @@ hipError_t launch_lis(const LisArgs& a, hipStream_t stream) {
         u.kb = nc * 32;
         u.ld = u.kb + 8;
         u.vt_bytes = fused ? u.dpad * u.ld * (int)sizeof(uint16_t) : 0;
+        size_t lds = (size_t)u.vt_bytes + out_lds;
+        // codes only, dense rows: each wavefront gathers its tile's code rows
+        // in LDS and writes them as one span
+        const int row_bytes = a.k.top > 15 ? a.Lk : (a.Lk + 1) / 2;
+        if (!fused && a.ld_codes == row_bytes) {
+            u.codes_ldw = (16 * row_bytes + 8 + 15) / 16 * 16;
+            lds += (size_t)4 * u.codes_ldw;
+        }
         const bool half = a.Lk - 32 * (nc - 1) <= 16;
-        return launch_lis_unit(nc, fused, dt, half, a, u, (size_t)u.vt_bytes + out_lds, stream);
+        return launch_lis_unit(nc, fused, dt, half, a, u, lds, stream);
     }
     // Long-row kernel: fused rows of 10 to 20 chunks on the float path, d <= 64,
     // no codes output, when its I-Exp table (u_max + 1 entries, byte offsets in

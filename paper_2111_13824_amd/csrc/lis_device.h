@@ -324,6 +324,8 @@ struct LisLaunch {
     int64_t n_logits;  // elements of the logits tensor (G Lq Lk)
     int64_t n_bias;    // elements of the bias tensor (Hb Lq Lk), 0 without bias
     int tab_bytes;     // long-row kernel: LDS bytes of the I-Exp table (multiple of 16)
+    int codes_ldw;     // unit kernel, codes only: LDS bytes per wavefront of the tile's
+                       // code rows (dense rows, ld_codes = row bytes), 0: direct stores
 };
 
 // ---------------------------------------------------------------------------
@@ -814,6 +816,38 @@ __device__ __forceinline__ void unit_tile(int (&cur)[NC][8], int (&nxt)[NC][8], 
         }
         if (p.out_vec) store_out_rows<DTMAX>(acc, ot, a, g, i0, lane, r, kg);
         else store_out<DTMAX>(acc, a, g, i0, r, kg);
+    } else if (p.codes_ldw != 0) {
+        // Dense code rows: the tile's rows are one contiguous span of the codes
+        // tensor.  They are gathered in LDS at the span's offset from a dword
+        // boundary (mis), then written as whole aligned dwords, the partial
+        // dwords at both ends byte by byte.
+        const int i = i0 + r;
+        const int nbr = k.top > 15 ? a.Lk : (a.Lk + 1) >> 1;
+        const int rows = min(16, a.Lq - i0);
+        uint8_t* cl = reinterpret_cast<uint8_t*>(ot);
+        uint8_t* span = a.codes + (g * a.Lq + i0) * (int64_t)nbr;
+        const int mis = (int)(reinterpret_cast<uintptr_t>(span) & 3);
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            int code[8];
+            chunk_codes<NC, true, NT>(code, cur, zb, st, k, c);
+            if (i < a.Lq) store_codes_row(cl + mis + r * nbr, a.Lk, k.top, c, kg, code);
+            if (PF + c < NC) load_one_chunk<NC, HALF>(nxt, rn, PF + c, kg, a.Lk);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        __builtin_amdgcn_wave_barrier();
+        uint8_t* gb = span - mis;
+        const int end = mis + rows * nbr;
+        for (int p0 = 4 * lane; p0 < end; p0 += 256) {
+            if (p0 >= mis && p0 + 4 <= end) {
+                *reinterpret_cast<uint32_t*>(gb + p0) = *reinterpret_cast<const uint32_t*>(cl + p0);
+            } else {
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+                    if (p0 + t >= mis && p0 + t < end) gb[p0 + t] = cl[p0 + t];
+            }
+        }
+        __builtin_amdgcn_wave_barrier();
     } else {
         const int i = i0 + r;
         uint8_t* crow = a.codes + (g * a.Lq + min(i, a.Lq - 1)) * (int64_t)a.ld_codes;
@@ -858,7 +892,9 @@ __global__ __launch_bounds__(kBlock, 3) void lis_unit_kernel(LisArgs a, LisLaunc
         stage_store(sr, vt, p.ld, DTMAX, 32 * NC, a.zp_v);
         __syncthreads();
     }
-    int32_t* ot = reinterpret_cast<int32_t*>(smem + p.vt_bytes) + wave * out_lds_dwords<DTMAX>();
+    // LDS per wavefront: the output transpose (fused) or the tile's code rows
+    int32_t* ot = FUSED ? reinterpret_cast<int32_t*>(smem + p.vt_bytes) + wave * out_lds_dwords<DTMAX>()
+                        : reinterpret_cast<int32_t*>(smem + wave * p.codes_ldw);
     while (tile < p.ntiles) {
         unit_tile<NC, FUSED, DTMAX, HALF>(bufA, bufB, a, p, k, vt, ot, ub, g, tile, lane, r, kg);
         tile += 4;

@@ -477,6 +477,27 @@ def test_head_unit_kernel(fq, orc, G, Lq, Lk, d):
     assert np.array_equal(got, ref)
 
 
+@pytest.mark.parametrize("G,Lq,Lk,bits,shift", [(512, 70, 197, 4, 1), (1024, 20, 100, 8, 3),
+                                                 (600, 33, 197, 8, 2), (2048, 1, 33, 5, 1),
+                                                 (512, 17, 63, 4, 0)])
+def test_codes_unit_kernel_dense_rows(fq, orc, G, Lq, Lk, bits, shift):
+    """Dense code rows (ld_codes = row bytes) are gathered per 16-row tile in
+    LDS and written as one span: a codes tensor starting 0..3 bytes past a
+    dword boundary, guard bytes before and after it left untouched."""
+    import torch
+    say("codes unit dense", G, Lq, Lk, bits, shift)
+    a = W.attn_inputs(G, Lq, Lk, 1, seed=5 * G + Lk + bits, heads=G, sigma=(1.0, 3.0, 6.0))
+    nb = Lk if bits > 4 else (Lk + 1) // 2
+    n = G * Lq * nb
+    buf = torch.full((n + shift + 64,), 0xA5, dtype=torch.uint8, device="cuda")
+    codes = buf[shift:shift + n].view(G, Lq, nb)
+    fq.lis_softmax_log4(dev(a["logits"]), S, bits=bits, codes=codes)
+    got = host(buf)
+    assert np.all(got[:shift] == 0xA5) and np.all(got[shift + n:] == 0xA5)
+    ref = orc.lis_softmax_log4(a["logits"], S, bits=bits)
+    assert np.array_equal(got[shift:shift + n].reshape(G, Lq, nb), ref[..., :nb])
+
+
 @pytest.mark.parametrize("G,Lq,Lk", [(1024, 17, 16), (1024, 20, 100), (512, 70, 197),
                                      (2048, 1, 33)])
 def test_codes_unit_kernel(fq, orc, G, Lq, Lk):
