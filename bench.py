@@ -119,7 +119,10 @@ def kernel_class(name):
         return "lis_attention_qk"
     if "attn_v_shift_wide" in name:
         return "lis_attn_v_shift_wide"
-    if "attn_v_shift" in name or "attn_v_mfma" in name:
+    if "attn_v_mfma" in name:   # attn_v_mfma_kernel<DT, CB, ZS, WIDE>
+        wide = name.split("<", 1)[1].split(">", 1)[0].split(",")[3].strip() == "true"
+        return "lis_attn_v_shift_wide" if wide else "lis_attn_v_shift"
+    if "attn_v_shift" in name:
         return "lis_attn_v_shift"
     if "fqvit::lis::" in name:
         return "lis_attention_head" if _lis_fused(name) else "lis_softmax_log4"
@@ -141,6 +144,10 @@ def short_kernel_name(name):
 
 
 def _counter_rows(d, counter=None):
+    """Counter rows of a rocprofv3 --pmc run in dispatch order, each with its
+    entry point in "Class": kernel_class, except that the second contiguous
+    run of codes-only dispatches (the bench's 8-bit codes, after the 4-bit
+    ones) is "lis_softmax_log4_b8"."""
     import csv
     import glob
     rows = []
@@ -148,6 +155,17 @@ def _counter_rows(d, counter=None):
         with open(fn) as f:
             rows += [r for r in csv.DictReader(f) if counter is None or r["Counter_Name"] == counter]
     rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+    runs, prev = 0, None
+    for r in rows:
+        cls = kernel_class(r["Kernel_Name"])
+        if cls == "lis_softmax_log4":
+            if prev != cls:
+                runs += 1
+            if runs >= 2:
+                cls = "lis_softmax_log4_b8"
+        if cls is not None:
+            prev = cls if cls != "lis_softmax_log4_b8" else "lis_softmax_log4"
+        r["Class"] = cls
     return rows
 
 
@@ -163,11 +181,11 @@ def pmc_summary(fetch_dir, write_dir, workload):
     def load(d, counter):
         rows = _counter_rows(d, counter)
         last_head = max((int(r["Dispatch_Id"]) for r in rows
-                         if kernel_class(r["Kernel_Name"]) == "lis_attention_head"), default=-1)
+                         if r["Class"] == "lis_attention_head"), default=-1)
         per_kernel, copies = {}, []
         for r in rows:
             name, v = r["Kernel_Name"], float(r["Counter_Value"])
-            cls = kernel_class(name)
+            cls = r["Class"]
             if cls:
                 per_kernel.setdefault((cls, short_kernel_name(name)), []).append(v)
             elif ("copy" in name.lower() and int(r["Dispatch_Id"]) > last_head
@@ -187,6 +205,8 @@ def pmc_summary(fetch_dir, write_dir, workload):
     alg = {"ptf_layernorm_int8": ln_b, "lis_attention_head": head_b,
            "lis_softmax_log4": 4 * cfg.G * cfg.Lq * cfg.Lk + n_bias + cfg.G * cfg.Lq * nbc,
            "lis_attn_v_shift": cfg.G * (cfg.Lq * nbc + cfg.Lk * cfg.d + 4 * cfg.Lq * cfg.d),
+           "lis_softmax_log4_b8": 4 * cfg.G * cfg.Lq * cfg.Lk + n_bias + cfg.G * cfg.Lq * cfg.Lk,
+           "lis_attn_v_shift_wide": cfg.G * (cfg.Lq * cfg.Lk + cfg.Lk * cfg.d + 8 * cfg.Lq * cfg.d),
            # q, k, v int8 (dk = d) and the int32 output
            "lis_attention_qk": cfg.G * (cfg.Lq * cfg.d + 2 * cfg.Lk * cfg.d + 4 * cfg.Lq * cfg.d),
            "ptf_calibrate": 2 * 4 * n_el + cfg.channels, "ptf_quantize_int8": 5 * n_el,
@@ -223,7 +243,7 @@ def sq_summary(dirs):
     acc = {}
     for d in dirs:
         for r in _counter_rows(d):
-            cls = kernel_class(r["Kernel_Name"])
+            cls = r["Class"]
             if not cls:
                 continue
             key = (cls, short_kernel_name(r["Kernel_Name"]))
