@@ -86,6 +86,8 @@ __device__ __forceinline__ void row_factors(int64_t m1, int64_t m2, int C, doubl
     }
 }
 
+typedef short short2_t __attribute__((ext_vector_type(2)));
+
 // Output of one element when A = gs r is known to lie in [2^(b-31), 2^b): then
 // N1 = b - 1 - floor(log2 |A|) needs no clamp and sign(A) N2 / 2^N1 is A with
 // its significand cut to b bits, a mask on the high word (b <= 8 keeps the
@@ -95,16 +97,22 @@ __device__ __forceinline__ void row_factors(int64_t m1, int64_t m2, int C, doubl
 // larger B (and the oracle's clamp of B 2^N1 at 2^62) saturate the output
 // either way, since |A X^| < 2^(E + 12).  Same result as ln_requant.
 // m_add = (53 - b) << 20 | 0x80000 builds M's high word from A's exponent
-// field; dlo, dhi: the output bounds minus zp_out.
-__device__ __forceinline__ int ln_requant_fast(double A, double B, int xh, uint32_t hi_mask,
-                                               uint32_t m_add, int zp_out, double dlo,
-                                               double dhi) {
+// field.  With c = zp_out + 1/2 + 512, v = At X^ + (Bg + c) is exact and
+// floor(v) = Y + 512 when unclamped; v_cvt_i32_f64 truncates (floor for
+// v >= 0) and saturates, and the clamp to [lo, hi] = [qlo + 512, qhi + 512]
+// (both positive, so a negative v lands on the lower bound either way)
+// returns Y + 512, whose low byte is Y's.
+__device__ __forceinline__ int ln_requant_rows(double A, double B, int xh, uint32_t hi_mask,
+                                               uint32_t m_add, double c, int lo, int hi) {
     const uint32_t hiA = (uint32_t)((uint64_t)__double_as_longlong(A) >> 32);
     const double At = __longlong_as_double((int64_t)((uint64_t)(hiA & hi_mask) << 32));
     const double M = __longlong_as_double((int64_t)((uint64_t)((hiA & 0x7FF00000u) + m_add) << 32));
-    const double Bg = (B + M) - M;
-    const double val = fma(At, (double)xh, Bg + 0.5);
-    return (int)floor(fmin(fmax(val, dlo), dhi)) + zp_out;
+    const double Bc = ((B + M) - M) + c;
+    const double v = fma(At, (double)xh, Bc);
+    int q;
+    asm("v_cvt_i32_f64 %0, %1" : "=v"(q) : "v"(v));
+    asm("v_med3_i32 %0, %1, %2, %3" : "=v"(q) : "v"(q), "s"(lo), "v"(hi));
+    return q;
 }
 
 // Fast path: C % 4 == 0, dword-aligned rows, W dwords per lane (W <= 8).
@@ -171,12 +179,36 @@ __global__ __launch_bounds__(kBlock) void ln_fast_kernel(LnArgs a, int lshift) {
         }
     }
 
+    // packed-statistics constants per dword (u = zp_in + 128): i16 pairs of
+    // 2^alpha and of -u 2^alpha, bytes of 2^alpha, and sum -u 2^alpha
+    uint32_t mulp[2 * W], zmp[2 * W], mulb[W];
+    uint32_t m1init = 0;
+    const int u_in = a.zp_in + 128;
+#pragma unroll
+    for (int w = 0; w < W; ++w) {
+        mulb[w] = 0;
+        mulp[2 * w] = mulp[2 * w + 1] = 0;
+        zmp[2 * w] = zmp[2 * w + 1] = 0;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            const uint32_t mb = (uint32_t)mul[4 * w + b];              // 0 past C
+            const uint32_t zm = (uint32_t)(-u_in) * mb;
+            mulb[w] |= mb << (8 * b);
+            mulp[2 * w + (b >> 1)] |= mb << (16 * (b & 1));
+            zmp[2 * w + (b >> 1)] |= (zm & 0xFFFFu) << (16 * (b & 1));
+            m1init += zm;
+        }
+    }
+
     const int qlo = -(1 << (a.bits - 1));
     const int qhi = (1 << (a.bits - 1)) - 1;
     const uint32_t hi_mask = ~((1u << (21 - a.bits)) - 1u);   // keep sign, exponent, b-1 bits
-    const uint32_t m_add = ((uint32_t)(53 - a.bits) << 20) | 0x80000u;
+    // one opaque scalar, so that the exponent add stays one instruction
+    uint32_t m_add = ((uint32_t)(53 - a.bits) << 20) | 0x80000u;
+    asm volatile("" : "+s"(m_add));
     const double amax = ldexp(1.0, a.bits), amin = ldexp(1.0, a.bits - 31);
-    const double dlo = (double)(qlo - a.zp_out), dhi = (double)(qhi - a.zp_out);
+    const double cadd = (double)a.zp_out + 512.5;
+    const int lo512 = qlo + 512, hi512 = qhi + 512;
     const int64_t gw = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
     const int64_t nw = ((int64_t)gridDim.x * blockDim.x) >> 6;
 
@@ -204,28 +236,46 @@ __global__ __launch_bounds__(kBlock) void ln_fast_kernel(LnArgs a, int lshift) {
         }
 
         int xh[4 * W];
-        int m1 = 0;
-        uint32_t m2 = 0;
-        int64_t m2w = 0;
-#pragma unroll
-        for (int w = 0; w < W; ++w) {
-#pragma unroll
-            for (int b = 0; b < 4; ++b) {
-                const int x = (int)(int8_t)(xv[w] >> (8 * b));
-                const int h = __mul24(x - a.zp_in, mul[4 * w + b]);   // 0 past C
-                xh[4 * w + b] = h;
-                m1 += h;
-                if (WIDE) m2w += (int64_t)h * h;
-                else m2 += (uint32_t)__mul24(h, h);
-            }
-        }
         int64_t M1, M2;
         if (WIDE) {
+            int m1 = 0;
+            int64_t m2w = 0;
+#pragma unroll
+            for (int w = 0; w < W; ++w) {
+#pragma unroll
+                for (int b = 0; b < 4; ++b) {
+                    const int x = (int)(int8_t)(xv[w] >> (8 * b));
+                    const int h = __mul24(x - a.zp_in, mul[4 * w + b]);   // 0 past C
+                    xh[4 * w + b] = h;
+                    m1 += h;
+                    m2w += (int64_t)h * h;
+                }
+            }
             M1 = seg_sum<int>(m1, L);
             M2 = seg_sum<int64_t>(m2w, L);
         } else {
+            // packed i16 X^ pairs, M1 by byte dot products, M2 by i16 pair dot
+            // products (as in the row-batch kernel; exact, |X^| < 2^15)
+            uint32_t m1 = m1init, m2 = 0;
+#pragma unroll
+            for (int w = 0; w < W; ++w) {
+                const uint32_t xu = xv[w] ^ 0x80808080u;
+                const uint32_t p0 = __builtin_amdgcn_perm(xu, xu, 0x0C010C00u);
+                const uint32_t p1 = __builtin_amdgcn_perm(xu, xu, 0x0C030C02u);
+                const short2_t h0 = __builtin_bit_cast(short2_t, p0) * __builtin_bit_cast(short2_t, mulp[2 * w]) +
+                                    __builtin_bit_cast(short2_t, zmp[2 * w]);
+                const short2_t h1 = __builtin_bit_cast(short2_t, p1) * __builtin_bit_cast(short2_t, mulp[2 * w + 1]) +
+                                    __builtin_bit_cast(short2_t, zmp[2 * w + 1]);
+                m1 = __builtin_amdgcn_udot4(xu, mulb[w], m1, false);
+                m2 = (uint32_t)__builtin_amdgcn_sdot2(h0, h0, (int)m2, false);
+                m2 = (uint32_t)__builtin_amdgcn_sdot2(h1, h1, (int)m2, false);
+                xh[4 * w + 0] = h0.x;
+                xh[4 * w + 1] = h0.y;
+                xh[4 * w + 2] = h1.x;
+                xh[4 * w + 3] = h1.y;
+            }
             // per-lane m2 < 2^31: sum its 16-bit halves separately in 32 bits
-            M1 = dpp_seg_sum(m1, L);
+            M1 = dpp_seg_sum((int)m1, L);
             const int lo = dpp_seg_sum((int)(m2 & 0xFFFFu), L);
             const int hi = dpp_seg_sum((int)(m2 >> 16), L);
             M2 = ((int64_t)hi << 16) + lo;
@@ -238,15 +288,18 @@ __global__ __launch_bounds__(kBlock) void ln_fast_kernel(LnArgs a, int lshift) {
         if (fast) {
 #pragma unroll
             for (int w = 0; w < W; ++w) {
-                uint32_t pack = 0;
+                int q[4];
 #pragma unroll
                 for (int b = 0; b < 4; ++b) {
                     const int k = 4 * w + b;
                     const double A = gs[k] * r;
                     const double B = bs[k] - gs[k] * m;
-                    const int q = ln_requant_fast(A, B, xh[k], hi_mask, m_add, a.zp_out, dlo, dhi);
-                    pack |= ((uint32_t)q & 0xFFu) << (8 * b);
+                    q[b] = ln_requant_rows(A, B, xh[k], hi_mask, m_add, cadd, lo512, hi512);
                 }
+                // the low bytes of Y + 512 are Y's
+                const uint32_t lo = __builtin_amdgcn_perm((uint32_t)q[1], (uint32_t)q[0], 0x0C0C0400u);
+                const uint32_t hi = __builtin_amdgcn_perm((uint32_t)q[3], (uint32_t)q[2], 0x0C0C0400u);
+                const uint32_t pack = __builtin_amdgcn_perm(hi, lo, 0x05040100u);
                 if (rok && ok[w]) __builtin_nontemporal_store(pack, yr + li + (w << lshift));
             }
         } else {
@@ -323,13 +376,12 @@ __global__ __launch_bounds__(kBlock) void ln_generic_kernel(LnArgs a) {
 // the square root and the two divisions serves the R rows.  The per-row
 // factors reach every lane as scalars.
 //
-// Output, when the row's factors fit (see ln_requant_fast): with
+// Output, when the row's factors fit (see ln_requant_rows): with
 // c = zp_out + 1/2 + 512, v = At X^ + (Bg + c) is exact (multiples of 2^-N1
 // below 2^53 2^-N1) and floor(v) = w + zp_out + 512; v_cvt_i32_f64 truncates
 // (floor for v >= 0) and saturates, and a clamp to [qlo + 512, qhi + 512]
 // (both positive, so a negative v lands on the lower bound either way) gives
 // Y + 512, whose low byte is Y's.
-typedef short short2_t __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ uint32_t swap_add32(uint32_t a, uint32_t b) {
     // lanes 0-31: a summed over lanes l and l + 32; lanes 32-63: the same for b
@@ -357,21 +409,6 @@ __device__ __forceinline__ double readlane_f64(double v, int lane) {
     const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)b, lane);
     const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(b >> 32), lane);
     return __longlong_as_double((int64_t)(((uint64_t)hi << 32) | lo));
-}
-
-// ln_requant_fast with the zero point, the 1/2 and a 512 offset folded into
-// the addend; returns Y + 512.
-__device__ __forceinline__ int ln_requant_rows(double A, double B, int xh, uint32_t hi_mask,
-                                               uint32_t m_add, double c, int lo, int hi) {
-    const uint32_t hiA = (uint32_t)((uint64_t)__double_as_longlong(A) >> 32);
-    const double At = __longlong_as_double((int64_t)((uint64_t)(hiA & hi_mask) << 32));
-    const double M = __longlong_as_double((int64_t)((uint64_t)((hiA & 0x7FF00000u) + m_add) << 32));
-    const double Bc = ((B + M) - M) + c;
-    const double v = fma(At, (double)xh, Bc);
-    int q;
-    asm("v_cvt_i32_f64 %0, %1" : "=v"(q) : "v"(v));
-    asm("v_med3_i32 %0, %1, %2, %3" : "=v"(q) : "v"(q), "s"(lo), "v"(hi));
-    return q;
 }
 
 // Rows r0 .. r0 + nr - 1 of the lane's dwords (zeros elsewhere; nr may be 0),
