@@ -371,6 +371,38 @@ def test_attn_v_shift_wide(fq, orc, G, Lq, Lk, d, bits):
         assert np.array_equal(got, orc.lis_attn_v_shift_wide(codes, a["v"], zp_v=-5, bits=bits, Lk=Lk))
 
 
+@pytest.mark.parametrize("bits,d", [(1, 1), (2, 4), (3, 40)])
+def test_attn_v_wide_nibbles_above_N(fq, orc, bits, d):
+    """Nibble codes of b <= 3 bits with stored values above N = 2^b - 1 (never
+    written by Log-Int-Softmax): the units holding one are computed again
+    term by term (the floor of the shifted value), beside units without."""
+    say("av wide nibbles above N", bits, d)
+    rng = np.random.default_rng(90 + bits)
+    G, Lq, Lk = 6, 21, 130
+    codes = rng.integers(0, 2 ** bits, size=(G, Lq, Lk))
+    codes[1, 3, 7] = 15
+    codes[4, :, 100:] = rng.integers(0, 16, size=(Lq, Lk - 100))
+    pk = _stored_codes(codes, 4)
+    v = rng.integers(-128, 128, size=(G, Lk, d)).astype(np.int8)
+    got = host(fq.lis_attn_v_shift_wide(dev(pk), dev(v), Lk, zp_v=6, bits=bits))
+    assert np.array_equal(got, orc.lis_attn_v_shift_wide(pk, v, zp_v=6, bits=bits, Lk=Lk))
+
+
+@pytest.mark.parametrize("d,zp", [(1, 0), (4, -3), (8, 7)])
+def test_attn_v_shift_small_head_dims(fq, orc, d, zp):
+    """Head dimensions that take the byte-wise V^T staging and the scalar
+    output stores of the matrix-core product."""
+    say("av small d", d, zp)
+    rng = np.random.default_rng(d + 40)
+    a = W.attn_inputs(3, 37, 150, d, seed=d, v_lo=-128, v_hi=127)
+    codes = orc.lis_softmax_log4(a["logits"], S)
+    got = host(fq.lis_attn_v_shift(dev(codes), dev(a["v"]), 150, zp_v=zp))
+    assert np.array_equal(got, orc.lis_attn_v_shift(codes, a["v"], zp_v=zp, Lk=150))
+    anyc = _random_codes(rng, 3, 37, 150)
+    got = host(fq.lis_attn_v_shift(dev(anyc), dev(a["v"]), 150, zp_v=zp))
+    assert np.array_equal(got, orc.lis_attn_v_shift(anyc, a["v"], zp_v=zp, Lk=150))
+
+
 def test_attention_888_full_vit_base(fq, orc):
     """The 8/8/8 attention of the ViT-B/16 batch-64 workload: 8-bit
     Log-Int-Softmax codes on the GPU, then the wide BitShift product, against
