@@ -328,6 +328,16 @@ void launch_stream(bool fused, int dt, dim3 grid, size_t lds, hipStream_t stream
 // LDS of one workgroup on gfx950.
 constexpr size_t kMaxLdsBytes = 160 * 1024;
 
+// Wavefronts per unit of the unit kernel: units of at most four 16-row tiles
+// (and rows of at most four chunks, whose V^T 64 threads can stage) get one
+// wavefront per tile up to two, so that the per-wavefront set-up serves
+// several tiles.  Measured on Swin-S (6144 units of 49 x 49, d = 32): two
+// wavefronts per unit 41.4 us, one 43.7 us, four 46.6-47.3 us.
+int unit_waves(int nc, int tiles16) {
+    if (nc > 4 || tiles16 > 4) return 4;
+    return tiles16 == 1 ? 1 : 2;
+}
+
 hipError_t launch_lis(const LisArgs& a, hipStream_t stream) {
     using namespace lis;
     const bool fused = a.out != nullptr;
@@ -365,16 +375,17 @@ hipError_t launch_lis(const LisArgs& a, hipStream_t stream) {
         u.kb = nc * 32;
         u.ld = u.kb + 8;
         u.vt_bytes = fused ? u.dpad * u.ld * (int)sizeof(uint16_t) : 0;
-        size_t lds = (size_t)u.vt_bytes + out_lds;
+        const int wpu = unit_waves(nc, tiles16);
+        size_t lds = (size_t)u.vt_bytes + out_lds / 4 * wpu;
         // codes only, dense rows: each wavefront gathers its tile's code rows
         // in LDS and writes them as one span
         const int row_bytes = a.k.top > 15 ? a.Lk : (a.Lk + 1) / 2;
         if (!fused && a.ld_codes == row_bytes) {
             u.codes_ldw = (16 * row_bytes + 8 + 15) / 16 * 16;
-            lds += (size_t)4 * u.codes_ldw;
+            lds += (size_t)wpu * u.codes_ldw;
         }
         const bool half = a.Lk - 32 * (nc - 1) <= 16;
-        return launch_lis_unit(nc, fused, dt, half, a, u, lds, stream);
+        return launch_lis_unit(nc, fused, dt, half, wpu, a, u, lds, stream);
     }
     // Long-row kernel: fused rows of 10 to 20 chunks on the float path, d <= 64,
     // no codes output, when its I-Exp table (u_max + 1 entries, byte offsets in

@@ -152,13 +152,14 @@ __device__ __forceinline__ u32x4 load_v16(const int8_t* vrow, int dd, int d, boo
     return w;
 }
 
+template <int NTHREADS = kBlock>
 __device__ __forceinline__ void stage_load(StageRegs& sr, const int8_t* vg, int Lk, int d,
                                            int ncg, int k0, int kcnt, bool vec_ok) {
     const int nquads = kcnt >> 2;
     const int nitems = nquads * ncg;
 #pragma unroll
     for (int it = 0; it < kStageItems; ++it) {
-        const int idx = (int)threadIdx.x + it * kBlock;
+        const int idx = (int)threadIdx.x + it * NTHREADS;
         const int cg = idx / nquads;
         const int j = k0 + 4 * (idx - cg * nquads);
         const int dd = 16 * cg;
@@ -175,6 +176,7 @@ __device__ __forceinline__ uint32_t bf16_pair(float lo, float hi) {
     return __builtin_amdgcn_perm(__float_as_uint(hi), __float_as_uint(lo), 0x07060302u);
 }
 
+template <int NTHREADS = kBlock>
 __device__ __forceinline__ void stage_store(const StageRegs& sr, uint16_t* vt, int ld, int ncg,
                                             int kcnt, int zp) {
     const int nquads = kcnt >> 2;
@@ -182,7 +184,7 @@ __device__ __forceinline__ void stage_store(const StageRegs& sr, uint16_t* vt, i
     const float off = (float)(128 + zp);
 #pragma unroll
     for (int it = 0; it < kStageItems; ++it) {
-        const int idx = (int)threadIdx.x + it * kBlock;
+        const int idx = (int)threadIdx.x + it * NTHREADS;
         if (idx >= nitems) continue;
         const int cg = idx / nquads;
         const int jj = 4 * (idx - cg * nquads);
@@ -782,7 +784,7 @@ __device__ __forceinline__ void load_one_chunk(int (&lg)[NC][8], const RowPtrs& 
     else load_chunk<HALF>(lg[NC - 1], rp.row, rp.brow, NC - 1, kg, Lk, rp.tail_vec);
 }
 
-template <int NC, bool FUSED, int DTMAX, bool HALF>
+template <int NC, bool FUSED, int DTMAX, bool HALF, int WPU>
 __device__ __forceinline__ void unit_tile(int (&cur)[NC][8], int (&nxt)[NC][8], const LisArgs& a,
                                           const LisLaunch& p, const LisConsts& k, const uint16_t* vt,
                                           int32_t* ot, const UnitBase& ub, int64_t g, int tile,
@@ -793,7 +795,7 @@ __device__ __forceinline__ void unit_tile(int (&cur)[NC][8], int (&nxt)[NC][8], 
     // Always prefetch (a conditional load would keep the stale buffer live
     // across the loop); past the last tile the current rows, still in cache,
     // are read again.
-    const int nt = tile + 4 < p.ntiles ? tile + 4 : tile;
+    const int nt = tile + WPU < p.ntiles ? tile + WPU : tile;
     const RowPtrs rn = unit_row<NC>(a, p, ub, min(16 * nt + r, a.Lq - 1));
     uint32_t zb[NC][2];
     const RowState st = tile_iexp<NC, true, NT>(cur, zb, k);
@@ -862,8 +864,10 @@ __device__ __forceinline__ void unit_tile(int (&cur)[NC][8], int (&nxt)[NC][8], 
     }
 }
 
-template <int NC, bool FUSED, int DTMAX, bool HALF>
-__global__ __launch_bounds__(kBlock, 3) void lis_unit_kernel(LisArgs a, LisLaunch p) {
+// WPU wavefronts per unit (4, or fewer for units of few tiles, so that each
+// wavefront walks several; V^T staged by those 64 WPU threads).
+template <int NC, bool FUSED, int DTMAX, bool HALF, int WPU = 4>
+__global__ __launch_bounds__(64 * WPU, 12 / WPU) void lis_unit_kernel(LisArgs a, LisLaunch p) {
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
     uint16_t* vt = reinterpret_cast<uint16_t*>(smem);
     const int64_t g = blockIdx.x;
@@ -879,28 +883,28 @@ __global__ __launch_bounds__(kBlock, 3) void lis_unit_kernel(LisArgs a, LisLaunc
 
     StageRegs sr;
     if constexpr (FUSED)
-        stage_load(sr, a.v + g * (int64_t)a.Lk * a.d, a.Lk, a.d, DTMAX, 0, 32 * NC, p.vec_ok);
+        stage_load<64 * WPU>(sr, a.v + g * (int64_t)a.Lk * a.d, a.Lk, a.d, DTMAX, 0, 32 * NC, p.vec_ok);
 
     UnitBase ub;
     ub.loff = g * a.Lq * (int64_t)a.Lk;
     ub.boff = a.bias ? (g % a.Hb) * a.Lq * (int64_t)a.Lk : 0;
     int bufA[NC][8], bufB[NC][8];
-    int tile = (wave + (int)(g & 3)) & 3;
+    int tile = (wave + (int)(g % WPU)) % WPU;
     if (tile < p.ntiles)
         tile_load<NC, HALF>(bufA, unit_row<NC>(a, p, ub, min(16 * tile + r, a.Lq - 1)), kg, a.Lk);
     if constexpr (FUSED) {
-        stage_store(sr, vt, p.ld, DTMAX, 32 * NC, a.zp_v);
+        stage_store<64 * WPU>(sr, vt, p.ld, DTMAX, 32 * NC, a.zp_v);
         __syncthreads();
     }
     // LDS per wavefront: the output transpose (fused) or the tile's code rows
     int32_t* ot = FUSED ? reinterpret_cast<int32_t*>(smem + p.vt_bytes) + wave * out_lds_dwords<DTMAX>()
                         : reinterpret_cast<int32_t*>(smem + wave * p.codes_ldw);
     while (tile < p.ntiles) {
-        unit_tile<NC, FUSED, DTMAX, HALF>(bufA, bufB, a, p, k, vt, ot, ub, g, tile, lane, r, kg);
-        tile += 4;
+        unit_tile<NC, FUSED, DTMAX, HALF, WPU>(bufA, bufB, a, p, k, vt, ot, ub, g, tile, lane, r, kg);
+        tile += WPU;
         if (tile >= p.ntiles) break;
-        unit_tile<NC, FUSED, DTMAX, HALF>(bufB, bufA, a, p, k, vt, ot, ub, g, tile, lane, r, kg);
-        tile += 4;
+        unit_tile<NC, FUSED, DTMAX, HALF, WPU>(bufB, bufA, a, p, k, vt, ot, ub, g, tile, lane, r, kg);
+        tile += WPU;
     }
 }
 
@@ -1030,11 +1034,11 @@ hipError_t launch_lis_nc(bool fused, int dtm, bool fp, const LisArgs& a, const L
 // Launch of the unit kernel for exactly NC chunks (NC <= kUnitMaxNC).
 constexpr int kUnitMaxNC = 7;
 
-template <int NC>
-hipError_t launch_unit_nc(bool fused, int dtm, bool half, const LisArgs& a, const LisLaunch& p,
-                          size_t lds, hipStream_t s) {
-#define FQ_UNIT(FUSED, DTM, HALF)                                                           \
-    launch_kernel(lis_unit_kernel<NC, FUSED, DTM, HALF>, dim3((unsigned)a.G), dim3(kBlock), \
+template <int NC, int WPU>
+hipError_t launch_unit_nc_w(bool fused, int dtm, bool half, const LisArgs& a, const LisLaunch& p,
+                            size_t lds, hipStream_t s) {
+#define FQ_UNIT(FUSED, DTM, HALF)                                                                  \
+    launch_kernel(lis_unit_kernel<NC, FUSED, DTM, HALF, WPU>, dim3((unsigned)a.G), dim3(64 * WPU), \
                   lds, s, a, p)
     if (!fused) {
         if (half) FQ_UNIT(false, 1, true);
@@ -1050,13 +1054,24 @@ hipError_t launch_unit_nc(bool fused, int dtm, bool half, const LisArgs& a, cons
     return hipGetLastError();
 }
 
+// wpu: wavefronts per unit, 1 or 2 for rows of up to 4 chunks, else 4.
+template <int NC>
+hipError_t launch_unit_nc(bool fused, int dtm, bool half, int wpu, const LisArgs& a,
+                          const LisLaunch& p, size_t lds, hipStream_t s) {
+    if constexpr (NC <= 4) {
+        if (wpu == 1) return launch_unit_nc_w<NC, 1>(fused, dtm, half, a, p, lds, s);
+        if (wpu == 2) return launch_unit_nc_w<NC, 2>(fused, dtm, half, a, p, lds, s);
+    }
+    return launch_unit_nc_w<NC, 4>(fused, dtm, half, a, p, lds, s);
+}
+
 // Per chunk-count launchers, instantiated in lis_inst_lo.hip (1..10 chunks),
 // lis_inst_hi.hip (11..20 chunks) and lis_inst_unit.hip (unit kernel, 1..7).
 hipError_t launch_lis_regs_lo(int nc, bool fused, int dtm, bool fp, const LisArgs& a,
                               const LisLaunch& p, dim3 grid, size_t lds, hipStream_t stream);
 hipError_t launch_lis_regs_hi(int nc, bool fused, int dtm, bool fp, const LisArgs& a,
                               const LisLaunch& p, dim3 grid, size_t lds, hipStream_t stream);
-hipError_t launch_lis_unit(int nc, bool fused, int dtm, bool half, const LisArgs& a,
+hipError_t launch_lis_unit(int nc, bool fused, int dtm, bool half, int wpu, const LisArgs& a,
                            const LisLaunch& p, size_t lds, hipStream_t stream);
 
 }  // namespace lis
