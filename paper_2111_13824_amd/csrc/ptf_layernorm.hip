@@ -493,25 +493,23 @@ __device__ __forceinline__ void rows_stats(const LnArgs& a, const RowsCtx<W>& k,
     row_factors((int64_t)(int32_t)t1, (int64_t)t2, a.C, st.r, st.m);
 }
 
-// Output of the batch: packed bytes yo[j][w] of the rows whose factors are in
-// the fast range (fast[j]); the other rows are written here, element by
-// element (their bytes read again).
+// Output of the batch.  A row whose factors are in the fast range is packed
+// into bytes and stored as soon as it is computed, so that the stores of a
+// wavefront spread over its arithmetic instead of leaving together at its end;
+// the other rows are written element by element (their bytes read again).
 template <int W, int R>
 __device__ __forceinline__ void rows_output(const LnArgs& a, const RowsCtx<W>& k,
                                             const double2* s_gb, const RowsStats<W, R>& st,
-                                            uint32_t (&yo)[R][W], bool (&fast)[R],
-                                            int64_t r0, int nr, int nd, int lane) {
-    // every flag set: rows_store writes exactly the rows flagged here
-#pragma unroll
-    for (int j = 0; j < R; ++j) fast[j] = false;
+                                            int64_t r0, int nr, int nd, int lane,
+                                            uint32_t* y32) {
 #pragma unroll
     for (int j = 0; j < R; ++j) {
         if (j >= nr) break;
         const double rj = readlane_f64(st.r, (64 / R) * j);
         const double mj = readlane_f64(st.m, (64 / R) * j);
         const bool lane_fits = !k.zerol && k.gmaxl * rj < k.amax && k.gminl * rj >= k.amin;
-        fast[j] = rj > 0.0 && __ballot(!lane_fits) == 0;
-        if (fast[j]) {
+        if (rj > 0.0 && __ballot(!lane_fits) == 0) {
+            uint32_t yo[W];
 #pragma unroll
             for (int w = 0; w < W; ++w) {
                 int q[4];
@@ -526,11 +524,15 @@ __device__ __forceinline__ void rows_output(const LnArgs& a, const RowsCtx<W>& k
                 }
                 const uint32_t lo = __builtin_amdgcn_perm((uint32_t)q[1], (uint32_t)q[0], 0x0C0C0400u);
                 const uint32_t hi = __builtin_amdgcn_perm((uint32_t)q[3], (uint32_t)q[2], 0x0C0C0400u);
-                yo[j][w] = __builtin_amdgcn_perm(hi, lo, 0x05040100u);
+                yo[w] = __builtin_amdgcn_perm(hi, lo, 0x05040100u);
                 // one dword at a time: the f64 temporaries of all 4 W
                 // elements would not fit the register budget
                 __builtin_amdgcn_sched_barrier(0);
             }
+            uint32_t* yr = y32 + (r0 + j) * nd + lane;
+#pragma unroll
+            for (int w = 0; w < W; ++w)
+                if (k.ok[w]) __builtin_nontemporal_store(yo[w], yr + 64 * w);
         } else {
             const int8_t* xrow = a.x + (r0 + j) * a.C;
             int8_t* yrow = a.y + (r0 + j) * a.C;
@@ -543,20 +545,6 @@ __device__ __forceinline__ void rows_output(const LnArgs& a, const RowsCtx<W>& k
                 yrow[c] = (int8_t)ln_requant(A, B, xh, a.bits, a.zp_out, k.qlo, k.qhi);
             }
         }
-    }
-}
-
-template <int W, int R>
-__device__ __forceinline__ void rows_store(const RowsCtx<W>& k, const uint32_t (&yo)[R][W],
-                                           const bool (&fast)[R], uint32_t* y32,
-                                           int64_t r0, int nd, int lane) {
-#pragma unroll
-    for (int j = 0; j < R; ++j) {
-        if (!fast[j]) continue;
-        uint32_t* yr = y32 + (r0 + j) * nd + lane;
-#pragma unroll
-        for (int w = 0; w < W; ++w)
-            if (k.ok[w]) __builtin_nontemporal_store(yo[j][w], yr + 64 * w);
     }
 }
 
@@ -681,26 +669,17 @@ __global__ __launch_bounds__(BLOCK) void ln_rows_kernel(LnArgs a) {
     k.lo512 = k.qlo + 512;
     k.hi512 = k.qhi + 512;
 
-    // Batch i: statistics, output into registers; its stores are issued only
-    // after the statistics of batch i + 1 have waited for that batch's loads
-    // (loads and stores share one counter: a store issued before that wait
-    // would be waited for too).
+    // Batch i: statistics, then each row's output and stores.  The loads of
+    // every batch of the pass were issued before the first store, so waiting
+    // for a later batch's loads never waits for an earlier batch's stores.
     for (;;) {
-        uint32_t yo[R][W];
-        bool fast[R];
-        int64_t rprev = 0;
-        bool pending = false;
 #pragma unroll
         for (int i = 0; i < NB; ++i) {
             if (nr[i] <= 0) break;
             RowsStats<W, R> st;
             rows_stats<W, R>(a, k, xv[i], st);
-            if (pending) rows_store<W, R>(k, yo, fast, y32, rprev, nd, lane);
-            rows_output<W, R>(a, k, s_gb, st, yo, fast, ra + R * i, nr[i], nd, lane);
-            rprev = ra + R * i;
-            pending = true;
+            rows_output<W, R>(a, k, s_gb, st, ra + R * i, nr[i], nd, lane, y32);
         }
-        if (pending) rows_store<W, R>(k, yo, fast, y32, rprev, nd, lane);
         ra += NB * R;
         if (ra >= r1) break;
 #pragma unroll
@@ -711,38 +690,47 @@ __global__ __launch_bounds__(BLOCK) void ln_rows_kernel(LnArgs a) {
     }
 }
 
-// Workgroup size of the row-batch kernel.
-constexpr int kRowsBlock = 256;
-
-template <int W, int R, int NB>
+template <int W, int R, int NB, bool SPREAD, int BLOCK>
 hipError_t launch_rows_rb(const LnArgs& a, int wpc, hipStream_t stream) {
-    // one pass of NB batches of R rows per wavefront where the rows allow it,
-    // at most wpc wavefronts per CU
-    constexpr int kWaves = kRowsBlock / 64;
-    const int64_t want = (a.T + NB * R - 1) / (NB * R);
+    // one pass of NB batches of R rows per wavefront where the rows allow it
+    // (SPREAD: one batch of R rows per wavefront, the later batches of a pass
+    // holding the remainder), at most wpc wavefronts per CU
+    constexpr int kWaves = BLOCK / 64;
+    const int64_t want = SPREAD ? (a.T + R - 1) / R : (a.T + NB * R - 1) / (NB * R);
     const int64_t waves = std::max<int64_t>(1, std::min<int64_t>(want, 256 * (int64_t)wpc));
     const int64_t blocks = (waves + kWaves - 1) / kWaves;
     const size_t lds = (size_t)a.C * 2 * sizeof(double) + (size_t)(a.C / 4) * 2 * sizeof(uint4);
-    launch_kernel(ln_rows_kernel<W, R, kRowsBlock, NB>, dim3((unsigned)blocks), dim3(kRowsBlock),
+    launch_kernel(ln_rows_kernel<W, R, BLOCK, NB>, dim3((unsigned)blocks), dim3(BLOCK),
                   lds, stream, a);
     return hipGetLastError();
 }
 
-// Measured on the ViT-B/16 shape (12608 x 768, one MI355X): batches of four
-// rows, one per pass, at 12 wavefronts per CU 11.0-11.2 us; 8 per CU 12.1-13.2
-// us, 16 or 20 per CU 12.4-12.6 us; two or three batches of four per pass
-// (their loads issued together, each batch's stores held back until the next
-// batch's loads were waited for) 13.0-13.5 and 18.0-18.4 us.  Smaller batches,
-// whose earlier loads arrive sooner, at 8, 12 or 16 wavefronts per CU: two rows
-// with one, two or three batches per pass 12.4-14.3, 11.4-12.8 and 12.7-14.3
-// us, single rows with one, two or four batches 13.0-15.3, 13.0-14.8 and
-// 12.4-14.1 us (ViT-L/16, 9232 x 1024: all within 12.0-15.3 us, four-row
-// batches 12.4 us).  The kernel is bound by its vector-ALU issue (the
-// binary64 output, about 6.7 us of issue per SIMD), not by the latency that
-// smaller or more batches would hide.
+// Twelve wavefronts per CU.  Where the rows fill all of them, one workgroup of
+// twelve wavefronts per CU: the per-channel set-up (binary64 divisions, packed
+// constants) then runs once per CU instead of once per four wavefronts.  Rows
+// come in batches of four where there are at least four per wavefront, else in
+// batches of two (two per pass, the second holding the remainder), which gives
+// more wavefronts.  Measured on one MI355X, kernel events, all bit-identical:
+//   ViT-B/16 (12608 x 768): 11.3 us with 256-thread workgroups and each
+//   batch's stores held back until the next batch's loads had arrived; 11.0 us
+//   with each row stored as soon as it is computed; 10.4 us with one
+//   workgroup per CU (two-row batches 10.7 us; 512-thread workgroups 11.7-12.2
+//   us; 16 wavefronts per CU 11.7-16.0 us).
+//   ViT-L/16 (9232 x 1024): 12.5 us before; four-row batches 12.2 us
+//   (2308 wavefronts); two-row batches 11.2 us with 256-thread workgroups and
+//   10.5 us with one workgroup per CU.
+//   DeiT-S (1576 x 384): 5.4 us before; two-row batches 4.1 us with 256-thread
+//   workgroups, 5.2 us with 768 (66 CUs busy instead of 197).
+// Three or more batches per pass, single-row batches, or eight or sixteen
+// wavefronts per CU were slower on every shape.  The kernel stays bound by
+// its vector-ALU issue (the binary64 output).
 template <int W>
 hipError_t launch_rows(const LnArgs& a, hipStream_t stream) {
-    return launch_rows_rb<W, 4, 1>(a, 12, stream);
+    constexpr int kWpc = 12;
+    const int64_t full = 256 * (int64_t)kWpc;
+    if ((a.T + 3) / 4 >= full) return launch_rows_rb<W, 4, 1, false, 64 * kWpc>(a, kWpc, stream);
+    if ((a.T + 1) / 2 >= full) return launch_rows_rb<W, 2, 2, true, 64 * kWpc>(a, kWpc, stream);
+    return launch_rows_rb<W, 2, 2, true, 256>(a, kWpc, stream);
 }
 
 template <int W>

@@ -69,7 +69,10 @@ def test_ln_shapes(fq, orc, T, C):
     assert np.array_equal(_ln_gpu(fq, d), _ln_ref(orc, d))
 
 
-@pytest.mark.parametrize("T,C", [(100, 1024), (7, 768), (13, 256), (101, 512), (4099, 768), (37, 96)])
+# (7001, 512) and (13001, 256) take the row-batch kernel's workgroups of one
+# per CU, with two-row and four-row batches
+@pytest.mark.parametrize("T,C", [(100, 1024), (7, 768), (13, 256), (101, 512), (4099, 768), (37, 96),
+                                 (7001, 512), (13001, 256)])
 def test_ln_writes_only_its_rows(fq, orc, T, C):
     """Every row count, including a last batch of fewer rows than the one
     before it: the output matches and the bytes after it (a guard region in
@@ -123,17 +126,19 @@ def test_ln_edge_rows(fq, orc):
         assert np.array_equal(_ln_gpu(fq, d, **over), _ln_ref(orc, d, **over)), s_out
 
 
-def test_ln_mixed_fast_and_general_rows(fq, orc):
+@pytest.mark.parametrize("T", [4099, 7001, 13001])
+def test_ln_mixed_fast_and_general_rows(fq, orc, T):
     """Rows whose factors leave the fast range (near-constant rows: tiny
-    variance, huge 1/sigma) between ordinary rows, so that batches of four
-    rows mix both output paths."""
-    say("ln mixed rows")
-    d = W.ln_inputs(4099, 768, seed=12)
+    variance, huge 1/sigma) between ordinary rows, so that batches of two or
+    four rows mix both output paths (T picks the batch size and workgroup
+    shape of the row-batch kernel)."""
+    say("ln mixed rows", T)
+    d = W.ln_inputs(T, 768, seed=12)
     x = d["x_q"].copy()
     rng = np.random.default_rng(12)
     unshifted = np.flatnonzero(np.minimum(d["alpha"], d["K"]) == 0)
     assert unshifted.size > 0
-    for i in rng.choice(4099, size=300, replace=False):
+    for i in rng.choice(T, size=300, replace=False):
         x[i] = d["zp_in"]
         x[i, int(rng.choice(unshifted))] += 1 if d["zp_in"] < 127 else -1
     over = dict(x_q=x)
