@@ -16,12 +16,13 @@
 // whatever the rounding.  The whole file is compiled with -ffp-contract=off so
 // that A and B are each rounded exactly as written.
 //
-// Layout: one row is handled by L lanes (L a power of two <= 64, 64/L rows per
-// wavefront), each lane owning W 4-channel dwords of the row, so that the
-// loads are coalesced dwords and the row statistics are a segmented
-// shuffle reduction.  Per-channel gs, bs and the clamped shift are computed
-// once per workgroup into LDS and then held in registers; waves stride over
-// rows.
+// Kernels: ln_rows_kernel (256 <= C <= 1024: a wavefront per row, batches of
+// rows), ln_seg_kernel (C < 256: L lanes per row, the factors of several rows
+// computed together), ln_fast_kernel (other aligned shapes: L lanes per row,
+// per-channel gs, bs and shifts held in registers) and ln_generic_kernel (any
+// C and alignment).  In each, a lane owns whole 4-channel dwords of a row, so
+// that loads and stores are coalesced dwords and the row statistics are
+// shuffle reductions.
 #include <climits>
 
 #include "fqvit_launch.h"
@@ -690,6 +691,267 @@ __global__ __launch_bounds__(BLOCK) void ln_rows_kernel(LnArgs a) {
     }
 }
 
+// Rows of fewer than 64 dwords (C < 256, C % 4 = 0, dword-aligned rows) whose
+// per-lane sums of squares fit 32 bits.  L lanes own a row (R = 64 / L rows
+// per pass, lane li holding dwords li, li + L, ...), and P passes form a
+// batch.  The statistics of every pass are reduced over the row's L lanes;
+// lane li < P of each row group keeps those of pass li, so that one square
+// root and two divisions give the factors of P rows, which are broadcast back
+// to the row's lanes pass by pass (ds_swizzle, no memory access).  The
+// per-channel (gs, bs) pairs are read from LDS per element as in the
+// row-batch kernel; a wavefront owns a contiguous run of rows in units of R.
+template <int L>
+__device__ __forceinline__ uint32_t seg_bcast(uint32_t v, int p) {
+    static_assert(L >= 8 && L <= 32, "segments within a 32-lane swizzle group");
+    // bitmask swizzle: lane' = (lane & and_mask) | or_mask within 32 lanes;
+    // p is a constant once the callers' pass loops are unrolled
+    constexpr int kAnd = 0x1F & ~(L - 1);
+    int r;
+    switch (p) {
+        case 0: r = __builtin_amdgcn_ds_swizzle((int)v, kAnd | (0 << 5)); break;
+        case 1: r = __builtin_amdgcn_ds_swizzle((int)v, kAnd | (1 << 5)); break;
+        case 2: r = __builtin_amdgcn_ds_swizzle((int)v, kAnd | (2 << 5)); break;
+        case 3: r = __builtin_amdgcn_ds_swizzle((int)v, kAnd | (3 << 5)); break;
+        case 4: r = __builtin_amdgcn_ds_swizzle((int)v, kAnd | (4 << 5)); break;
+        case 5: r = __builtin_amdgcn_ds_swizzle((int)v, kAnd | (5 << 5)); break;
+        case 6: r = __builtin_amdgcn_ds_swizzle((int)v, kAnd | (6 << 5)); break;
+        default: r = __builtin_amdgcn_ds_swizzle((int)v, kAnd | (7 << 5)); break;
+    }
+    return (uint32_t)r;
+}
+
+template <int L>
+__device__ __forceinline__ double seg_bcast_f64(double v, int p) {
+    const uint64_t u = (uint64_t)__double_as_longlong(v);
+    const uint64_t lo = seg_bcast<L>((uint32_t)u, p), hi = seg_bcast<L>((uint32_t)(u >> 32), p);
+    return __longlong_as_double((int64_t)((hi << 32) | lo));
+}
+
+// The lane's dwords of the batch's rows (pass p: row seg + p R of the batch;
+// zeros for rows past nr and lanes past the row), as buffer loads that
+// address past the input when not needed.  dw0 is the dword index of the
+// lane's first dword in the batch's first row group (T C < 2^31 bytes).
+template <int W, int L, int P>
+__device__ __forceinline__ void load_seg(uint32_t (&xv)[P][W], __amdgpu_buffer_rsrc_t xr,
+                                         int dw0, int nr, int nd, int seg,
+                                         const bool (&ok)[W]) {
+    constexpr int R = 64 / L;
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+#pragma unroll
+        for (int w = 0; w < W; ++w) {
+            const int off = (p * R + seg < nr && ok[w]) ? (dw0 + p * R * nd + L * w) * 4 : INT_MIN;
+            xv[p][w] = __builtin_amdgcn_raw_buffer_load_b32(xr, off, 0, 2 /* nt */);
+        }
+    }
+}
+
+template <int W, int L, int P, int BLOCK>
+__global__ __launch_bounds__(BLOCK) void ln_seg_kernel(LnArgs a) {
+    static_assert(P <= L && P <= 8, "lane li < P of a row group keeps pass li");
+    constexpr int R = 64 / L;
+    extern __shared__ double smem[];
+    // all of it dynamic, so that the 16-byte entries stay 16-byte aligned
+    double2* s_gb = reinterpret_cast<double2*>(smem);        // (gs, bs) at [b][dword]
+    uint4* s_pk = reinterpret_cast<uint4*>(s_gb + a.C);      // per dword, as ln_rows_kernel
+    const int nd = a.C >> 2;
+    uint32_t* s_bnd = reinterpret_cast<uint32_t*>(s_pk + 2 * nd);   // bounds of |gs|
+    const int lane = threadIdx.x & 63;
+    const int seg = lane / L, li = lane % L;
+
+    // contiguous run of units of R rows; wavefronts numbered across
+    // workgroups first
+    constexpr int kWaves = BLOCK / 64;
+    const int64_t nw = (int64_t)gridDim.x * kWaves;
+    const int64_t gw = (int64_t)__builtin_amdgcn_readfirstlane(threadIdx.x >> 6) * gridDim.x +
+                       blockIdx.x;
+    const int64_t units = (a.T + R - 1) / R;
+    const int64_t ub = units / nw, urem = units % nw;
+    const int64_t u0 = gw * ub + min(gw, urem);
+    int64_t ra = u0 * R;
+    const int64_t r1 = min<int64_t>(a.T, (u0 + ub + (gw < urem ? 1 : 0)) * R);
+    // the whole input and output, a.T * a.C < 2^31 bytes (checked by the
+    // launcher)
+    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)a.x, (short)0, (int)(a.T * a.C), 0x00020000);
+    const __amdgpu_buffer_rsrc_t yrs = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)a.y, (short)0, (int)(a.T * a.C), 0x00020000);
+    RowsCtx<W> k;
+#pragma unroll
+    for (int w = 0; w < W; ++w) k.ok[w] = li + L * w < nd;
+    int dw0 = ((int)ra + seg) * nd + li;
+
+    // set-up as in ln_rows_kernel: one thread per dword (nd < 64), and the
+    // bounds of |gs| over the whole row
+    const int sdw = threadIdx.x;
+    float sg[4], sb[4];
+    int sa[4];
+    if (sdw < nd) {
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            sg[b] = a.gamma[4 * sdw + b];
+            sb[b] = a.beta[4 * sdw + b];
+            sa[b] = a.alpha[4 * sdw + b];
+        }
+    }
+    uint32_t xv[P][W];
+    int nr = (int)max<int64_t>(0, min<int64_t>(P * R, r1 - ra));
+    load_seg<W, L, P>(xv, xr, dw0, nr, nd, seg, k.ok);
+
+    const int u = a.zp_in + 128;
+    uint32_t dhi = 0, dlo = 0x7FF00000u;
+    if (sdw < nd) {
+        uint32_t mulp[2] = {0, 0}, zmp[2] = {0, 0}, mulb = 0, m1p = 0;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            const double gs = (double)sg[b] / (double)a.s_out;
+            s_gb[b * nd + sdw] = double2{gs, (double)sb[b] / (double)a.s_out};
+            const int sh = min(sa[b], a.K);
+            const uint32_t zm = (uint32_t)(-u) << sh;
+            mulb |= (1u << sh) << (8 * b);
+            mulp[b >> 1] |= (1u << sh) << (16 * (b & 1));
+            zmp[b >> 1] |= (zm & 0xFFFFu) << (16 * (b & 1));
+            m1p += zm;
+            const uint32_t h = (uint32_t)((uint64_t)__double_as_longlong(gs) >> 32) & 0x7FFFFFFFu;
+            dhi = max(dhi, h);
+            dlo = min(dlo, h);
+        }
+        s_pk[2 * sdw] = uint4{mulp[0], mulp[1], zmp[0], zmp[1]};
+        s_pk[2 * sdw + 1] = uint4{mulb, m1p, 0u, 0u};
+    }
+    if (threadIdx.x < 64) {   // wave 0 holds every dword (nd < 64)
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            dhi = max(dhi, (uint32_t)__shfl_xor((int)dhi, off, 64));
+            dlo = min(dlo, (uint32_t)__shfl_xor((int)dlo, off, 64));
+        }
+        if (threadIdx.x == 0) {
+            s_bnd[0] = dhi;
+            s_bnd[1] = dlo;
+        }
+    }
+    __syncthreads();
+    if (nr <= 0) return;
+
+    k.m1init = 0;
+#pragma unroll
+    for (int w = 0; w < W; ++w) {
+        const int dw = k.ok[w] ? li + L * w : 0;
+        const uint4 p = s_pk[2 * dw];
+        const uint4 q = s_pk[2 * dw + 1];
+        k.mulp[2 * w] = k.ok[w] ? p.x : 0u;
+        k.mulp[2 * w + 1] = k.ok[w] ? p.y : 0u;
+        k.zmp[2 * w] = k.ok[w] ? p.z : 0u;
+        k.zmp[2 * w + 1] = k.ok[w] ? p.w : 0u;
+        k.mulb[w] = k.ok[w] ? q.x : 0u;
+        k.m1init += k.ok[w] ? q.y : 0u;
+    }
+    // bounds of |gs| over the whole row from the high words (as in
+    // ln_rows_kernel, here for every channel of the row)
+    const uint32_t ghi = s_bnd[0], glo = s_bnd[1];
+    k.gmaxl = __longlong_as_double((int64_t)(((uint64_t)ghi << 32) | 0xFFFFFFFFu));
+    k.gminl = __longlong_as_double((int64_t)((uint64_t)glo << 32));
+    k.zerol = glo == 0;
+    k.qlo = -(1 << (a.bits - 1));
+    k.qhi = (1 << (a.bits - 1)) - 1;
+    k.hi_mask = ~((1u << (21 - a.bits)) - 1u);
+    uint32_t m_add = ((uint32_t)(53 - a.bits) << 20) | 0x80000u;
+    asm volatile("" : "+s"(m_add));
+    k.m_add = m_add;
+    k.amax = ldexp(1.0, a.bits);
+    k.amin = ldexp(1.0, a.bits - 31);
+    k.cadd = (double)a.zp_out + 512.5;
+    k.lo512 = k.qlo + 512;
+    k.hi512 = k.qhi + 512;
+
+    for (;;) {
+        // statistics of every pass; lane li keeps those of pass li
+        uint32_t hp[P][2 * W];
+        int cm1 = 0, clo = 0, chi = 0;
+#pragma unroll
+        for (int p = 0; p < P; ++p) {
+            if (p * R >= nr) break;
+            uint32_t m1 = k.m1init, m2 = 0;
+#pragma unroll
+            for (int w = 0; w < W; ++w) {
+                const uint32_t xu = xv[p][w] ^ 0x80808080u;
+                const uint32_t p0 = __builtin_amdgcn_perm(xu, xu, 0x0C010C00u);
+                const uint32_t p1 = __builtin_amdgcn_perm(xu, xu, 0x0C030C02u);
+                const short2_t h0 = __builtin_bit_cast(short2_t, p0) * __builtin_bit_cast(short2_t, k.mulp[2 * w]) +
+                                    __builtin_bit_cast(short2_t, k.zmp[2 * w]);
+                const short2_t h1 = __builtin_bit_cast(short2_t, p1) * __builtin_bit_cast(short2_t, k.mulp[2 * w + 1]) +
+                                    __builtin_bit_cast(short2_t, k.zmp[2 * w + 1]);
+                m1 = __builtin_amdgcn_udot4(xu, k.mulb[w], m1, false);
+                m2 = (uint32_t)__builtin_amdgcn_sdot2(h0, h0, (int)m2, false);
+                m2 = (uint32_t)__builtin_amdgcn_sdot2(h1, h1, (int)m2, false);
+                hp[p][2 * w] = __builtin_bit_cast(uint32_t, h0);
+                hp[p][2 * w + 1] = __builtin_bit_cast(uint32_t, h1);
+            }
+            // per-lane m2 < 2^32: its 16-bit halves are summed separately
+            const int s1 = dpp_seg_sum((int)m1, L);
+            const int slo = dpp_seg_sum((int)(m2 & 0xFFFFu), L);
+            const int shi = dpp_seg_sum((int)(m2 >> 16), L);
+            cm1 = li == p ? s1 : cm1;
+            clo = li == p ? slo : clo;
+            chi = li == p ? shi : chi;
+        }
+        double r, m;
+        row_factors((int64_t)cm1, ((int64_t)chi << 16) + clo, a.C, r, m);
+        const uint32_t fast = (r > 0.0 && !k.zerol && k.gmaxl * r < k.amax && k.gminl * r >= k.amin) ? 1u : 0u;
+
+#pragma unroll
+        for (int p = 0; p < P; ++p) {
+            if (p * R >= nr) break;
+            const double rp = seg_bcast_f64<L>(r, p);
+            const double mp = seg_bcast_f64<L>(m, p);
+            const bool fp = seg_bcast<L>(fast, p) != 0u;
+            const int j = p * R + seg;
+            const int yoff = (dw0 + p * R * nd) * 4;   // the lane's first dword of the row
+            if (j < nr && fp) {
+#pragma unroll
+                for (int w = 0; w < W; ++w) {
+                    int q[4];
+#pragma unroll
+                    for (int b = 0; b < 4; ++b) {
+                        const uint32_t hw = hp[p][2 * w + (b >> 1)];
+                        const int xh = (b & 1) ? (int)hw >> 16 : (int)(int16_t)(hw & 0xFFFFu);
+                        const double2 gb = s_gb[b * nd + (k.ok[w] ? li + L * w : 0)];
+                        const double A = gb.x * rp;
+                        const double B = gb.y - gb.x * mp;
+                        q[b] = ln_requant_rows(A, B, xh, k.hi_mask, k.m_add, k.cadd, k.lo512, k.hi512);
+                    }
+                    const uint32_t lo = __builtin_amdgcn_perm((uint32_t)q[1], (uint32_t)q[0], 0x0C0C0400u);
+                    const uint32_t hi = __builtin_amdgcn_perm((uint32_t)q[3], (uint32_t)q[2], 0x0C0C0400u);
+                    const uint32_t pack = __builtin_amdgcn_perm(hi, lo, 0x05040100u);
+                    if (k.ok[w]) __builtin_amdgcn_raw_buffer_store_b32(pack, yrs, yoff + 4 * L * w, 0, 2 /* nt */);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            } else if (j < nr) {
+#pragma unroll
+                for (int w = 0; w < W; ++w) {
+                    uint32_t pack = 0;
+#pragma unroll
+                    for (int b = 0; b < 4; ++b) {
+                        const uint32_t hw = hp[p][2 * w + (b >> 1)];
+                        const int xh = (b & 1) ? (int)hw >> 16 : (int)(int16_t)(hw & 0xFFFFu);
+                        const double2 gb = s_gb[b * nd + (k.ok[w] ? li + L * w : 0)];
+                        const double A = gb.x * rp;
+                        const double B = gb.y - gb.x * mp;
+                        const int q = ln_requant(A, B, xh, a.bits, a.zp_out, k.qlo, k.qhi);
+                        pack |= ((uint32_t)q & 0xFFu) << (8 * b);
+                    }
+                    if (k.ok[w]) __builtin_amdgcn_raw_buffer_store_b32(pack, yrs, yoff + 4 * L * w, 0, 2 /* nt */);
+                }
+            }
+        }
+        ra += P * R;
+        dw0 += P * R * nd;
+        if (ra >= r1) break;
+        nr = (int)max<int64_t>(0, min<int64_t>(P * R, r1 - ra));
+        load_seg<W, L, P>(xv, xr, dw0, nr, nd, seg, k.ok);
+    }
+}
+
 template <int W, int R, int NB, bool SPREAD, int BLOCK>
 hipError_t launch_rows_rb(const LnArgs& a, int wpc, hipStream_t stream) {
     // one pass of NB batches of R rows per wavefront where the rows allow it
@@ -731,6 +993,51 @@ hipError_t launch_rows(const LnArgs& a, hipStream_t stream) {
     if ((a.T + 3) / 4 >= full) return launch_rows_rb<W, 4, 1, false, 64 * kWpc>(a, kWpc, stream);
     if ((a.T + 1) / 2 >= full) return launch_rows_rb<W, 2, 2, true, 64 * kWpc>(a, kWpc, stream);
     return launch_rows_rb<W, 2, 2, true, 256>(a, kWpc, stream);
+}
+
+template <int W, int L, int P, int BLOCK>
+hipError_t launch_seg_b(const LnArgs& a, int wpc, hipStream_t stream) {
+    constexpr int kWaves = BLOCK / 64;
+    constexpr int R = 64 / L;
+    const int64_t want = (a.T + R * P - 1) / (R * P);
+    const int64_t waves = std::max<int64_t>(1, std::min<int64_t>(want, 256 * (int64_t)wpc));
+    const int64_t blocks = (waves + kWaves - 1) / kWaves;
+    const size_t lds =
+        (size_t)a.C * 2 * sizeof(double) + (size_t)(a.C / 4) * 2 * sizeof(uint4) + sizeof(uint4);
+    launch_kernel(ln_seg_kernel<W, L, P, BLOCK>, dim3((unsigned)blocks), dim3(BLOCK), lds, stream,
+                  a);
+    return hipGetLastError();
+}
+
+// Twelve wavefronts per CU.  Where batches of four passes fill them all (or
+// else of two), one workgroup per CU; fewer rows take single passes, which
+// gives the most wavefronts.  Measured on one MI355X, kernel events, all
+// bit-identical:
+//   Swin-S (100352 x 96, L = 8): 15.3 us with the earlier kernel (factors of
+//   every pass computed on their own, gs and bs held in registers); batches
+//   of 1, 2, 4 or 8 passes 13.8, 11.8, 11.4 and 14.3 us with one workgroup
+//   per CU (256-thread workgroups 0.3-0.8 us slower; 16 wavefronts per CU
+//   slower still).  The static LDS of an earlier form left the 16-byte
+//   (gs, bs) entries 8-byte aligned: 21-22 us.
+//   DeiT-Ti (197 x 192, L = 16): 4.4 us before; 1, 2, 4 or 8 passes 4.0,
+//   4.2, 5.4 and 7.8 us.
+template <int W, int L>
+hipError_t launch_seg_l(const LnArgs& a, hipStream_t stream) {
+    constexpr int kWpc = 12;
+    constexpr int R = 64 / L;
+    const int64_t full = 256 * (int64_t)kWpc;
+    if ((a.T + 4 * R - 1) / (4 * R) >= full) return launch_seg_b<W, L, 4, 64 * kWpc>(a, kWpc, stream);
+    if ((a.T + 2 * R - 1) / (2 * R) >= full) return launch_seg_b<W, L, 2, 64 * kWpc>(a, kWpc, stream);
+    return launch_seg_b<W, L, 1, 256>(a, kWpc, stream);
+}
+
+template <int W>
+hipError_t launch_seg(const LnArgs& a, int lshift, hipStream_t stream) {
+    switch (lshift) {
+        case 3: return launch_seg_l<W, 8>(a, stream);
+        case 4: return launch_seg_l<W, 16>(a, stream);
+        default: return launch_seg_l<W, 32>(a, stream);
+    }
 }
 
 template <int W>
@@ -788,6 +1095,15 @@ hipError_t launch_ptf_layernorm(const LnArgs& a, hipStream_t stream) {
     }
     // Per-lane sums of squares: 4W values of at most (255 * 2^K)^2 each.
     const bool wide = (double)(4 * best_w) * 65025.0 * (double)(1 << (2 * a.K)) >= 2147483647.0;
+    if (!wide && best_l >= 3 && best_l <= 5 && best_w <= 4 &&
+        a.T * (int64_t)a.C < ((int64_t)1 << 31)) {
+        switch (best_w) {
+            case 1: return launch_seg<1>(a, best_l, stream);
+            case 2: return launch_seg<2>(a, best_l, stream);
+            case 3: return launch_seg<3>(a, best_l, stream);
+            default: return launch_seg<4>(a, best_l, stream);
+        }
+    }
     switch (best_w) {
         case 1: return launch_fast<1>(a, best_l, wide, stream);
         case 2: return launch_fast<2>(a, best_l, wide, stream);

@@ -59,7 +59,10 @@ LN_SHAPES = [(1, 192), (7, 96), (197, 192), (333, 384), (64, 768), (100, 1024), 
              (9, 13), (5, 2048), (3, 4096), (2, 8192), (65, 4), (3, 1), (70, 2000),
              # row-batch kernel (256 <= C <= 1024): one row, partial batches,
              # several batches per wavefront, idle lanes in the last dword
-             (1, 768), (5, 256), (4099, 260), (20000, 256), (9001, 1020), (16400, 512)]
+             (1, 768), (5, 256), (4099, 260), (20000, 256), (9001, 1020), (16400, 512),
+             # rows of < 64 dwords: 8, 16 or 32 lanes per row, four passes per
+             # batch, partial batches and idle lanes
+             (1001, 96), (50, 128), (3000, 64), (77, 32), (4099, 192), (130, 112)]
 
 
 @pytest.mark.parametrize("T,C", LN_SHAPES)
@@ -72,7 +75,7 @@ def test_ln_shapes(fq, orc, T, C):
 # (7001, 512) and (13001, 256) take the row-batch kernel's workgroups of one
 # per CU, with two-row and four-row batches
 @pytest.mark.parametrize("T,C", [(100, 1024), (7, 768), (13, 256), (101, 512), (4099, 768), (37, 96),
-                                 (7001, 512), (13001, 256)])
+                                 (7001, 512), (13001, 256), (1001, 96), (333, 192), (130, 112)])
 def test_ln_writes_only_its_rows(fq, orc, T, C):
     """Every row count, including a last batch of fewer rows than the one
     before it: the output matches and the bytes after it (a guard region in
@@ -126,14 +129,14 @@ def test_ln_edge_rows(fq, orc):
         assert np.array_equal(_ln_gpu(fq, d, **over), _ln_ref(orc, d, **over)), s_out
 
 
-@pytest.mark.parametrize("T", [4099, 7001, 13001])
-def test_ln_mixed_fast_and_general_rows(fq, orc, T):
+@pytest.mark.parametrize("T,C", [(4099, 768), (7001, 768), (13001, 768), (5003, 96), (2001, 192)])
+def test_ln_mixed_fast_and_general_rows(fq, orc, T, C):
     """Rows whose factors leave the fast range (near-constant rows: tiny
-    variance, huge 1/sigma) between ordinary rows, so that batches of two or
-    four rows mix both output paths (T picks the batch size and workgroup
-    shape of the row-batch kernel)."""
-    say("ln mixed rows", T)
-    d = W.ln_inputs(T, 768, seed=12)
+    variance, huge 1/sigma) between ordinary rows, so that batches of rows
+    mix both output paths (T and C pick the kernel, its batch size and its
+    workgroup shape)."""
+    say("ln mixed rows", T, C)
+    d = W.ln_inputs(T, C, seed=12)
     x = d["x_q"].copy()
     rng = np.random.default_rng(12)
     unshifted = np.flatnonzero(np.minimum(d["alpha"], d["K"]) == 0)
