@@ -864,10 +864,21 @@ __device__ __forceinline__ void unit_tile(int (&cur)[NC][8], int (&nxt)[NC][8], 
     }
 }
 
+// Minimum wavefronts per SIMD the register allocation is held to (the second
+// argument of __launch_bounds__): three for four wavefronts per unit (168
+// registers); for the small units that take one or two, six where the kernel
+// fits 80 registers (fused rows of up to two chunks with d <= 32, codes-only
+// rows of one chunk), so that as many units are in flight as the CU holds,
+// and four otherwise (128 registers: at 80 those spilled).
+constexpr int unit_waves_per_simd(int NC, bool FUSED, int DTMAX, int WPU) {
+    return WPU == 4 ? 3 : ((FUSED ? (NC <= 2 && DTMAX <= 2) : NC <= 1) ? 6 : 4);
+}
+
 // WPU wavefronts per unit (4, or fewer for units of few tiles, so that each
 // wavefront walks several; V^T staged by those 64 WPU threads).
 template <int NC, bool FUSED, int DTMAX, bool HALF, int WPU = 4>
-__global__ __launch_bounds__(64 * WPU, 12 / WPU) void lis_unit_kernel(LisArgs a, LisLaunch p) {
+__global__ __launch_bounds__(64 * WPU, unit_waves_per_simd(NC, FUSED, DTMAX, WPU)) void lis_unit_kernel(
+    LisArgs a, LisLaunch p) {
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
     uint16_t* vt = reinterpret_cast<uint16_t*>(smem);
     const int64_t g = blockIdx.x;
