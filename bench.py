@@ -684,6 +684,10 @@ def main():
     }
     if not args.no_extras:
         result["extras"] = extras(cfg, inp, sets[0]["out"], fq, torch)
+        # the head against the rate a plain device copy reaches on this GPU
+        copy_gbs = result["extras"]["device_copy"]["gbs"]
+        result["roofline"]["measured_copy_gbs"] = copy_gbs
+        result["roofline"]["frac_of_measured_copy"] = achieved / copy_gbs
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(cfg, inp)
     print(json.dumps(result), flush=True)
