@@ -34,7 +34,8 @@ HBM_PEAK_GBS = 8000.0
 METRIC = "tokens/s and achieved HBM GB/s for PTF-LayerNorm + LIS attention, ViT-B bs64"
 BENCH_WORKLOAD = "vit_base16_224_b64"
 N_SETS = 4
-EVENT_SAMPLES = 64
+# kernel-duration samples after the timed region (at least this many)
+EVENT_SAMPLES = 200
 COPY_BYTES = 512 * 2 ** 20
 COPY_REPS = 3
 # Summary of the counter runs of a workload (profiles/traffic_<workload>.txt);
