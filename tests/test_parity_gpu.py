@@ -106,11 +106,31 @@ def test_ln_params(fq, orc, K, bits):
     assert np.array_equal(_ln_gpu(fq, d, **over), _ln_ref(orc, d, **over))
 
 
-def test_ln_edge_rows(fq, orc):
+@pytest.mark.parametrize("C", [96, 192, 128])
+@pytest.mark.parametrize("K,bits", [(0, 8), (3, 4), (5, 8), (6, 8), (7, 6), (2, 2)])
+def test_ln_params_small_rows(fq, orc, C, K, bits):
+    """Rows of fewer than 256 channels: the batched-factor kernel while the
+    per-lane sums of squares fit 32 bits (K <= 5 at C = 96), the per-lane
+    factor kernel beyond."""
+    say("ln params small rows", C, K, bits)
+    rng = np.random.default_rng(K * 100 + bits * 10 + C)
+    T = 777
+    d = W.ln_inputs(T, C, seed=C + K)
+    half = 2 ** (bits - 1)
+    x = rng.integers(-half, half, size=(T, C)).astype(np.int8)
+    alpha = rng.integers(0, 8, size=C).astype(np.uint8)
+    zp = int(rng.integers(-half, half))
+    zpo = int(rng.integers(-half, half))
+    over = dict(x_q=x, alpha=alpha, K=K, bits=bits, zp_in=zp, zp_out=zpo)
+    assert np.array_equal(_ln_gpu(fq, d, **over), _ln_ref(orc, d, **over))
+
+
+@pytest.mark.parametrize("C", [384, 96])
+def test_ln_edge_rows(fq, orc, C):
     """Constant rows (zero variance), rows at the zero point, gamma = 0, extreme
     affine values, tiny and huge s_out."""
-    say("ln edges")
-    d = W.ln_inputs(64, 384, seed=9)
+    say("ln edges", C)
+    d = W.ln_inputs(64, C, seed=9)
     x = d["x_q"].copy()
     x[0] = d["zp_in"]
     x[1] = (d["zp_in"] + (8 >> np.minimum(d["alpha"], 3))).astype(np.int8)
