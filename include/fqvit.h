@@ -9,7 +9,9 @@
  *     example allocated through torch).  The library allocates nothing, never
  *     synchronises, and enqueues its kernels on `stream` (a hipStream_t; NULL
  *     is the default stream).  It keeps no state between calls apart from the
- *     per-thread timing events of fq_time_next_call.  It is re-entrant.
+ *     per-thread timing events of fq_time_next_call and the fixed device array
+ *     of ptf_calibrate_noalloc.  It is re-entrant (ptf_calibrate_noalloc: see
+ *     its note on overlapping calls).
  *   - Scalars are passed by value.  Tensors are dense and row-major with the
  *     shapes given below; a tensor is read or written only inside the extent
  *     its shape gives.
