@@ -237,7 +237,10 @@ __device__ __forceinline__ void load_full(int (&dst)[8], const int32_t* row, con
 // readable elements inside their tensors, so the chunk is read with full
 // vectors and masked afterwards.  HALF: only the first four keys (the last
 // chunk holds at most 16 keys).
-template <bool HALF>
+// DEFER: keys past Lk read with full vectors are left as loaded, to be masked
+// by mask_last when the chunk is used; masking them here would make the
+// wavefront wait for the load (and every load before it) right away.
+template <bool HALF, bool DEFER = false>
 __device__ __forceinline__ void load_chunk(int (&dst)[8], const int32_t* row, const int32_t* brow,
                                            int c, int kg, int Lk, bool vec_ok) {
     const int k0 = 32 * c + 4 * kg;
@@ -250,9 +253,11 @@ __device__ __forceinline__ void load_chunk(int (&dst)[8], const int32_t* row, co
                 const i32x4a4 ba = *reinterpret_cast<const i32x4a4*>(brow + k0);
                 dst[0] += ba.x; dst[1] += ba.y; dst[2] += ba.z; dst[3] += ba.w;
             }
+            if (!DEFER) {
 #pragma unroll
-            for (int t = 0; t < 4; ++t)
-                if (k0 + t >= Lk) dst[t] = INT_MIN;
+                for (int t = 0; t < 4; ++t)
+                    if (k0 + t >= Lk) dst[t] = INT_MIN;
+            }
         } else {
 #pragma unroll
             for (int t = 0; t < 4; ++t)
@@ -264,10 +269,12 @@ __device__ __forceinline__ void load_chunk(int (&dst)[8], const int32_t* row, co
     }
     if (vec_ok || k1 + 4 <= Lk) {
         load_full(dst, row, brow, c, kg);
+        if (!DEFER) {
 #pragma unroll
-        for (int t = 0; t < 8; ++t) {
-            const int key = (t < 4 ? k0 : k1 - 4) + t;
-            if (key >= Lk) dst[t] = INT_MIN;
+            for (int t = 0; t < 8; ++t) {
+                const int key = (t < 4 ? k0 : k1 - 4) + t;
+                if (key >= Lk) dst[t] = INT_MIN;
+            }
         }
     } else {
 #pragma unroll
@@ -276,6 +283,27 @@ __device__ __forceinline__ void load_chunk(int (&dst)[8], const int32_t* row, co
             dst[t] = key < Lk ? row[key] + (brow ? brow[key] : 0) : INT_MIN;
         }
     }
+}
+
+// Valid keys of lane kg in the last chunk c = NC - 1, bit t for its key t.
+template <int NC>
+__device__ __forceinline__ uint32_t last_valid(int kg, int Lk) {
+    const int k0 = 32 * (NC - 1) + 4 * kg;
+    uint32_t m = 0;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+        const int key = (t < 4 ? k0 : k0 + 12) + t;
+        m |= key < Lk ? 1u << t : 0u;
+    }
+    return m;
+}
+
+// The masking deferred by load_chunk<HALF, true>: keys past Lk of the last
+// chunk become INT_MIN.
+template <int NC, int NT>
+__device__ __forceinline__ void mask_last(int (&lg)[NC][8], uint32_t valid) {
+#pragma unroll
+    for (int t = 0; t < NT; ++t) lg[NC - 1][t] = (valid >> t) & 1u ? lg[NC - 1][t] : INT_MIN;
 }
 
 // Store the 8 codes of lane (r, kg) in chunk c as nibbles (even key low).
@@ -750,12 +778,12 @@ __device__ __forceinline__ RowPtrs unit_row(const LisArgs& a, const LisLaunch& p
 }
 
 // Loads chunks [C0, C1) of a lane's keys.
-template <int NC, bool HALF, int C0 = 0, int C1 = NC>
+template <int NC, bool HALF, int C0 = 0, int C1 = NC, bool DEFER = false>
 __device__ __forceinline__ void tile_load(int (&lg)[NC][8], const RowPtrs& rp, int kg, int Lk) {
 #pragma unroll
     for (int c = C0; c < C1; ++c) {
         if (c < NC - 1) load_full(lg[c], rp.row, rp.brow, c, kg);
-        else load_chunk<HALF>(lg[NC - 1], rp.row, rp.brow, NC - 1, kg, Lk, rp.tail_vec);
+        else load_chunk<HALF, DEFER>(lg[NC - 1], rp.row, rp.brow, NC - 1, kg, Lk, rp.tail_vec);
     }
 }
 
@@ -771,26 +799,39 @@ __device__ __forceinline__ void tile_load(int (&lg)[NC][8], const RowPtrs& rp, i
 // the I-Exp pass of the current tile, and chunk PF + c right after chunk c of
 // the current tile has gone through its MFMA (its registers are free by then),
 // so the next tile is in flight without holding two tiles in registers.
-// Measured on the ViT-B/16 shapes with the current arithmetic: PF = 0 is the
-// fastest; PF = 1 to 3 (150 to 164 VGPRs) are 1 to 2 % slower, and PF = 7 (168
-// VGPRs and a few spilled) and requesting the whole next tile before the I-Exp
-// pass about 15 % slower.
-constexpr int unit_prefetch(int NC) { return NC < 0 ? NC : 0; }
+// Rows of five or more chunks also defer the masking of the last chunk's keys
+// past Lk to the chunk's use (mask_last): applied at the load, it made the
+// wavefront wait for the whole next tile right after requesting its last
+// chunk, before the current tile's output was stored.  Measured on the ViT-B/16
+// shapes (768 x 197 x 197, events over 96 launches, same box): deferred masking
+// with PF = 2 (156 VGPRs) 43.8-45.3 us against 45.4-46.9 us before; PF = 0 or 1
+// 44.5-45.3, PF = 3 45.6, PF = 4 48.1 (168 VGPRs, spills); requesting the last
+// chunk first no better than PF = 0.  The small-unit kernels keep the masking
+// at the load and PF = 0: deferred, they spill at their 80-register bound.
+// Both are taken by the fused kernels (the codes-only kernels of seven chunks
+// spill more with the deferred masking), PF = 2 where it fits the 168
+// registers of three wavefronts per SIMD: all but the widest (seven full
+// chunks and d > 32), which keeps PF = 0.
+constexpr bool unit_defer(int NC, bool FUSED) { return FUSED && NC >= 5; }
+constexpr int unit_prefetch(int NC, bool FUSED, int DTMAX, bool HALF) {
+    return unit_defer(NC, FUSED) && !(NC == 7 && DTMAX == 4 && !HALF) ? 2 : 0;
+}
 
-template <int NC, bool HALF>
+template <int NC, bool HALF, bool DEFER = false>
 __device__ __forceinline__ void load_one_chunk(int (&lg)[NC][8], const RowPtrs& rp, int c, int kg,
                                                int Lk) {
     if (c < NC - 1) load_full(lg[c], rp.row, rp.brow, c, kg);
-    else load_chunk<HALF>(lg[NC - 1], rp.row, rp.brow, NC - 1, kg, Lk, rp.tail_vec);
+    else load_chunk<HALF, DEFER>(lg[NC - 1], rp.row, rp.brow, NC - 1, kg, Lk, rp.tail_vec);
 }
 
 template <int NC, bool FUSED, int DTMAX, bool HALF, int WPU>
 __device__ __forceinline__ void unit_tile(int (&cur)[NC][8], int (&nxt)[NC][8], const LisArgs& a,
                                           const LisLaunch& p, const LisConsts& k, const uint16_t* vt,
                                           int32_t* ot, const UnitBase& ub, int64_t g, int tile,
-                                          int lane, int r, int kg) {
+                                          int lane, int r, int kg, uint32_t valid) {
     constexpr int NT = HALF ? 4 : 8;
-    constexpr int PF = unit_prefetch(NC);
+    constexpr int PF = unit_prefetch(NC, FUSED, DTMAX, HALF);
+    constexpr bool DF = unit_defer(NC, FUSED);
     const int i0 = 16 * tile;
     // Always prefetch (a conditional load would keep the stale buffer live
     // across the loop); past the last tile the current rows, still in cache,
@@ -798,8 +839,9 @@ __device__ __forceinline__ void unit_tile(int (&cur)[NC][8], int (&nxt)[NC][8], 
     const int nt = tile + WPU < p.ntiles ? tile + WPU : tile;
     const RowPtrs rn = unit_row<NC>(a, p, ub, min(16 * nt + r, a.Lq - 1));
     uint32_t zb[NC][2];
+    if (DF) mask_last<NC, NT>(cur, valid);
     const RowState st = tile_iexp<NC, true, NT>(cur, zb, k);
-    tile_load<NC, HALF, 0, PF>(nxt, rn, kg, a.Lk);
+    tile_load<NC, HALF, 0, PF, DF>(nxt, rn, kg, a.Lk);
     if constexpr (FUSED) {
         f32x4 acc[DTMAX];
 #pragma unroll
@@ -811,7 +853,7 @@ __device__ __forceinline__ void unit_tile(int (&cur)[NC][8], int (&nxt)[NC][8], 
                 chunk_mfma<DTMAX, true>(acc, pb, vt, p.ld, c, r, kg);
             else
                 chunk_mfma<DTMAX, false>(acc, pb, vt, p.ld, c, r, kg);
-            if (PF + c < NC) load_one_chunk<NC, HALF>(nxt, rn, PF + c, kg, a.Lk);
+            if (PF + c < NC) load_one_chunk<NC, HALF, DF>(nxt, rn, PF + c, kg, a.Lk);
             // keep each chunk's V^T reads next to its MFMAs (hoisting them all
             // would take 4 DTMAX registers per chunk)
             __builtin_amdgcn_sched_barrier(0);
@@ -834,7 +876,7 @@ __device__ __forceinline__ void unit_tile(int (&cur)[NC][8], int (&nxt)[NC][8], 
             int code[8];
             chunk_codes<NC, true, NT>(code, cur, zb, st, k, c);
             if (i < a.Lq) store_codes_row(cl + mis + r * nbr, a.Lk, k.top, c, kg, code);
-            if (PF + c < NC) load_one_chunk<NC, HALF>(nxt, rn, PF + c, kg, a.Lk);
+            if (PF + c < NC) load_one_chunk<NC, HALF, DF>(nxt, rn, PF + c, kg, a.Lk);
             __builtin_amdgcn_sched_barrier(0);
         }
         __builtin_amdgcn_wave_barrier();
@@ -858,7 +900,7 @@ __device__ __forceinline__ void unit_tile(int (&cur)[NC][8], int (&nxt)[NC][8], 
             int code[8];
             chunk_codes<NC, true, NT>(code, cur, zb, st, k, c);
             if (i < a.Lq) store_codes_row(crow, a.Lk, k.top, c, kg, code);
-            if (PF + c < NC) load_one_chunk<NC, HALF>(nxt, rn, PF + c, kg, a.Lk);
+            if (PF + c < NC) load_one_chunk<NC, HALF, DF>(nxt, rn, PF + c, kg, a.Lk);
             __builtin_amdgcn_sched_barrier(0);
         }
     }
@@ -902,7 +944,9 @@ __global__ __launch_bounds__(64 * WPU, unit_waves_per_simd(NC, FUSED, DTMAX, WPU
     int bufA[NC][8], bufB[NC][8];
     int tile = (wave + (int)(g % WPU)) % WPU;
     if (tile < p.ntiles)
-        tile_load<NC, HALF>(bufA, unit_row<NC>(a, p, ub, min(16 * tile + r, a.Lq - 1)), kg, a.Lk);
+        tile_load<NC, HALF, 0, NC, unit_defer(NC, FUSED)>(
+            bufA, unit_row<NC>(a, p, ub, min(16 * tile + r, a.Lq - 1)), kg, a.Lk);
+    const uint32_t valid = unit_defer(NC, FUSED) ? last_valid<NC>(kg, a.Lk) : 0xFFu;
     if constexpr (FUSED) {
         stage_store<64 * WPU>(sr, vt, p.ld, DTMAX, 32 * NC, a.zp_v);
         __syncthreads();
@@ -911,10 +955,12 @@ __global__ __launch_bounds__(64 * WPU, unit_waves_per_simd(NC, FUSED, DTMAX, WPU
     int32_t* ot = FUSED ? reinterpret_cast<int32_t*>(smem + p.vt_bytes) + wave * out_lds_dwords<DTMAX>()
                         : reinterpret_cast<int32_t*>(smem + wave * p.codes_ldw);
     while (tile < p.ntiles) {
-        unit_tile<NC, FUSED, DTMAX, HALF, WPU>(bufA, bufB, a, p, k, vt, ot, ub, g, tile, lane, r, kg);
+        unit_tile<NC, FUSED, DTMAX, HALF, WPU>(bufA, bufB, a, p, k, vt, ot, ub, g, tile, lane, r, kg,
+                                               valid);
         tile += WPU;
         if (tile >= p.ntiles) break;
-        unit_tile<NC, FUSED, DTMAX, HALF, WPU>(bufB, bufA, a, p, k, vt, ot, ub, g, tile, lane, r, kg);
+        unit_tile<NC, FUSED, DTMAX, HALF, WPU>(bufB, bufA, a, p, k, vt, ot, ub, g, tile, lane, r, kg,
+                                               valid);
         tile += WPU;
     }
 }

@@ -524,7 +524,10 @@ def test_head_long_rows_clamp_depth(fq, orc, n):
 # (d % 16 != 0) and the scalar output stores (d % 4 != 0).
 UNIT_SHAPES = [(1024, 17, 16, 64), (1024, 17, 17, 64), (1024, 20, 100, 64), (512, 70, 197, 64),
                (600, 49, 49, 32), (512, 65, 224, 64), (700, 33, 120, 48), (700, 33, 120, 20),
-               (2048, 2, 40, 17), (2048, 1, 5, 64)]
+               (2048, 2, 40, 17), (2048, 1, 5, 64),
+               # rows of five to seven chunks, whose fused kernels mask the last
+               # chunk at its use and prefetch two chunks ahead
+               (512, 50, 150, 32), (512, 64, 170, 64), (520, 49, 180, 20), (512, 70, 200, 16)]
 
 
 @pytest.mark.parametrize("G,Lq,Lk,d", UNIT_SHAPES)
