@@ -652,7 +652,13 @@ __device__ __forceinline__ u32x4 chunk_pbits(const int (&lg)[NC][8], const uint3
 }
 
 // acc[dt] += P x V^T for chunk c (cs: its index inside the current V^T stage).
-template <int DTMAX, bool HALFMMA>
+// TR = false: acc[dt] is the 16 x 16 output block (rows i0.., columns 16 dt..)
+// in the matrix cores' layout, lane (r, kg) holding rows 4 kg .. 4 kg + 3 of
+// column 16 dt + r.  TR = true: the operands swap roles, so the instruction
+// forms the transposed block V^T P^T from the same products and sums, and lane
+// (r, kg) holds columns 16 dt + 4 kg .. + 3 of row i0 + r: four consecutive
+// int32 of one output row, one 16-byte store.
+template <int DTMAX, bool HALFMMA, bool TR = false>
 __device__ __forceinline__ void chunk_mfma(f32x4 (&acc)[DTMAX], u32x4 pb, const uint16_t* vt,
                                            int ld, int cs, int r, int kg) {
     if constexpr (HALFMMA) {
@@ -660,16 +666,50 @@ __device__ __forceinline__ void chunk_mfma(f32x4 (&acc)[DTMAX], u32x4 pb, const 
 #pragma unroll
         for (int dt = 0; dt < DTMAX; ++dt) {
             const u32x2 bv = *reinterpret_cast<const u32x2*>(vt + (16 * dt + r) * ld + 32 * cs + 8 * kg);
-            acc[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(A, __builtin_bit_cast(i16x4, bv),
-                                                                acc[dt], 0, 0, 0);
+            const i16x4 B = __builtin_bit_cast(i16x4, bv);
+            if constexpr (TR)
+                acc[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(B, A, acc[dt], 0, 0, 0);
+            else
+                acc[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(A, B, acc[dt], 0, 0, 0);
         }
     } else {
         const bf16x8 A = __builtin_bit_cast(bf16x8, pb);
 #pragma unroll
         for (int dt = 0; dt < DTMAX; ++dt) {
             const u32x4 bv = *reinterpret_cast<const u32x4*>(vt + (16 * dt + r) * ld + 32 * cs + 8 * kg);
-            acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, __builtin_bit_cast(bf16x8, bv),
-                                                              acc[dt], 0, 0, 0);
+            const bf16x8 B = __builtin_bit_cast(bf16x8, bv);
+            if constexpr (TR)
+                acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(B, A, acc[dt], 0, 0, 0);
+            else
+                acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, B, acc[dt], 0, 0, 0);
+        }
+    }
+}
+
+// Output of transposed blocks (chunk_mfma with TR): lane (r, kg) writes
+// out[g][i0 + r][16 dt + 4 kg + q] = acc[dt][q].  vec (d % 4 == 0, 16-byte
+// aligned out): one 16-byte store per (row, dt), the four lanes of a row
+// covering 64 contiguous bytes.  Streaming stores: the output is not read
+// again here.
+template <int DTMAX>
+__device__ __forceinline__ void store_out_t(const f32x4 (&acc)[DTMAX], const LisArgs& a, int64_t g,
+                                            int i0, int r, int kg, bool vec) {
+    typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+    const int row = i0 + r;
+    if (row >= a.Lq) return;
+    int32_t* orow = a.out + (g * a.Lq + row) * (int64_t)a.d;
+#pragma unroll
+    for (int dt = 0; dt < DTMAX; ++dt) {
+        const int col = 16 * dt + 4 * kg;
+        if (col >= a.d) continue;
+        if (vec) {
+            const i32x4 v = {(int32_t)acc[dt][0], (int32_t)acc[dt][1], (int32_t)acc[dt][2],
+                             (int32_t)acc[dt][3]};
+            __builtin_nontemporal_store(v, reinterpret_cast<i32x4*>(orow + col));
+        } else {
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                if (col + q < a.d) orow[col + q] = (int32_t)acc[dt][q];
         }
     }
 }

@@ -18,7 +18,8 @@ hipError_t launch_lis_qk(const LisArgs& a, const QkInput& in, hipStream_t stream
     p.ld = p.kb + 8;
     p.vec_ok = (a.d % 16 == 0) && ((reinterpret_cast<uintptr_t>(a.v) & 15) == 0);
     p.vt_bytes = p.dpad * p.ld * (int)sizeof(uint16_t);
-    p.out_vec = 0;
+    // output rows as 16-byte units (d % 4 == 0 and a 16-byte aligned out)
+    p.out_vec = (a.d % 4 == 0) && ((reinterpret_cast<uintptr_t>(a.out) & 15) == 0);
     p.n_logits = 0;
     p.n_bias = a.bias ? (int64_t)a.Hb * a.Lq * a.Lk : 0;
     const size_t lds = (size_t)p.vt_bytes + (size_t)32 * nc * in.dk + (size_t)32 * nc * sizeof(int32_t);

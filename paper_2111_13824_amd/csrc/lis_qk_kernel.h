@@ -99,20 +99,24 @@ __global__ __launch_bounds__(kBlock, 3) void lis_qk_kernel(LisArgs a, QkArgs qa,
     const int8_t* q_base = qa.q + g * (int64_t)a.Lq * DK;
     const int32_t* bplane = a.bias ? a.bias + (g % a.Hb) * (int64_t)a.Lq * a.Lk : nullptr;
 
-    for (int tile = (wave + (int)(g & 3)) & 3; tile < p.ntiles; tile += 4) {
-        const int i0 = 16 * tile;
-        const int i = min(i0 + r, a.Lq - 1);
-        // B operand: this lane's bytes of query i (DK / 4 bytes)
-        const int8_t* qrow = q_base + (int64_t)i * DK;
-        i32x4v qb[DK >= 64 ? DK / 64 : 1];
-        int64_t qb8 = 0;
+    // B operand: this lane's bytes of query row i (DK / 4 bytes)
+    i32x4v qb[DK >= 64 ? DK / 64 : 1];
+    int64_t qb8 = 0;
+    auto load_q = [&](int t, i32x4v (&dst)[DK >= 64 ? DK / 64 : 1], int64_t& dst8) {
+        const int8_t* qrow = q_base + (int64_t)min(16 * t + r, a.Lq - 1) * DK;
         if constexpr (DK >= 64) {
 #pragma unroll
             for (int m = 0; m < DK / 64; ++m)
-                qb[m] = *reinterpret_cast<const i32x4v*>(qrow + 64 * m + 16 * kg);
+                dst[m] = *reinterpret_cast<const i32x4v*>(qrow + 64 * m + 16 * kg);
         } else {
-            qb8 = *reinterpret_cast<const int64_t*>(qrow + 8 * kg);
+            dst8 = *reinterpret_cast<const int64_t*>(qrow + 8 * kg);
         }
+    };
+    int tile = (wave + (int)(g & 3)) & 3;
+    if (tile < p.ntiles) load_q(tile, qb, qb8);
+    for (; tile < p.ntiles; tile += 4) {
+        const int i0 = 16 * tile;
+        const int i = min(i0 + r, a.Lq - 1);
 
         // logits of this tile in the Log-Int-Softmax lane layout
         int lg[NC][8];
@@ -152,6 +156,8 @@ __global__ __launch_bounds__(kBlock, 3) void lis_qk_kernel(LisArgs a, QkArgs qa,
                 }
             }
         }
+        // the next tile's query bytes, in flight during the rest of this tile
+        load_q(tile + 4 < p.ntiles ? tile + 4 : tile, qb, qb8);
         if (bplane) {   // uniform: the bias of the lane's row, in a pass of its own
             const int32_t* brow = bplane + (int64_t)i * a.Lk;
 #pragma unroll
@@ -172,12 +178,12 @@ __global__ __launch_bounds__(kBlock, 3) void lis_qk_kernel(LisArgs a, QkArgs qa,
         for (int c = 0; c < NC; ++c) {
             const u32x4 pb = chunk_pbits<NC, FP, NT>(lg, zb, st, k, c);
             if (HALF && c == NC - 1)
-                chunk_mfma<DTMAX, true>(acc, pb, vt, p.ld, c, r, kg);
+                chunk_mfma<DTMAX, true, true>(acc, pb, vt, p.ld, c, r, kg);
             else
-                chunk_mfma<DTMAX, false>(acc, pb, vt, p.ld, c, r, kg);
+                chunk_mfma<DTMAX, false, true>(acc, pb, vt, p.ld, c, r, kg);
             __builtin_amdgcn_sched_barrier(0);
         }
-        store_out<DTMAX>(acc, a, g, i0, r, kg);
+        store_out_t<DTMAX>(acc, a, g, i0, r, kg, p.out_vec);
     }
 }
 

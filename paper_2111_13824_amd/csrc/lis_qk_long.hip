@@ -192,9 +192,9 @@ __global__ __launch_bounds__(kQkLongBlock) void lis_qk_long_kernel(LisArgs a, Qk
             }
             const u32x4 pb = {pbits[0] | (pbits[1] << 16), pbits[2] | (pbits[3] << 16),
                               pbits[4] | (pbits[5] << 16), pbits[6] | (pbits[7] << 16)};
-            chunk_mfma<DTMAX, false>(acc, pb, vt, p.ld, c, r, kg);
+            chunk_mfma<DTMAX, false, true>(acc, pb, vt, p.ld, c, r, kg);
         }
-        store_out<DTMAX>(acc, a, g, i0, r, kg);
+        store_out_t<DTMAX>(acc, a, g, i0, r, kg, p.out_vec);
     }
 }
 

@@ -59,6 +59,8 @@ SHAPES = [  # G, Lq, Lk, dk, d
     (3, 50, 577, 64, 64),       # ViT-L/16 at 384 px
     (2, 33, 640, 32, 20),       # longest supported row
     (2, 17, 300, 64, 48),
+    (8, 33, 100, 32, 30),       # d % 4 != 0: output written element by element
+    (2, 20, 300, 64, 30),
 ]
 
 
