@@ -43,6 +43,20 @@ COPY_REPS = 3
 # sources matches the one recorded with it.
 def traffic_file(workload):
     return os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
+# The paper's own figures for the method, with their setting: model accuracy
+# only (it reports no timing or hardware), so context for this line, not a
+# target.  Table 1: ImageNet top-1 after post-training quantization with
+# 1,000 calibration images, bit-widths of weights / activations / attention
+# maps; Table 3: the BitOPs of ViT-B.
+PAPER_CONTEXT = {
+    "source": "FQ-ViT (arXiv 2111.13824), Table 1 and Table 3; accuracy, not throughput",
+    "imagenet_top1_pct": {
+        "ViT-L fp32": 85.81, "ViT-L FQ-ViT 8/8/8": 85.03, "ViT-L FQ-ViT 8/8/4": 84.89,
+        "ViT-B fp32": 84.53, "ViT-B FQ-ViT 8/8/8": 83.31, "ViT-B FQ-ViT 8/8/4": 82.68,
+        "ViT-B MinMax 8/8/8": 23.64,
+    },
+    "vit_b_gbitops_8_8_4_ptf_lis": 1117.76,
+}
 LIS_SOURCES = ["lis_device.h", "lis_attention.hip", "lis_inst_lo.hip", "lis_inst_hi.hip",
                "lis_inst_unit.hip", "fqvit_internal.h", "fqvit_launch.h"]
 
@@ -682,6 +696,7 @@ def main():
             "algorithmic_bytes_per_launch": head_bytes,
         },
         "wall_s_timed": wall,
+        "paper_context": PAPER_CONTEXT,
     }
     if not args.no_extras:
         result["extras"] = extras(cfg, inp, sets[0]["out"], fq, torch)
