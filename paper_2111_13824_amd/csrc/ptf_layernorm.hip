@@ -426,7 +426,9 @@ __device__ __forceinline__ void load_rows(uint32_t (&xv)[R][W],
 #pragma unroll
         for (int w = 0; w < W; ++w) {
             const int off = (j < nr && ok[w]) ? (int)(((r0 + j) * nd + lane + 64 * w) * 4) : INT_MIN;
-            xv[j][w] = __builtin_amdgcn_raw_buffer_load_b32(xr, off, 0, 2 /* nt */);
+            // default cache policy: streaming (non-temporal) loads measured
+            // 0.1-0.5 us slower on the ViT-B, ViT-L and Swin-S rows
+            xv[j][w] = __builtin_amdgcn_raw_buffer_load_b32(xr, off, 0, 0);
         }
     }
 }
@@ -741,7 +743,7 @@ __device__ __forceinline__ void load_seg(uint32_t (&xv)[P][W], __amdgpu_buffer_r
 #pragma unroll
         for (int w = 0; w < W; ++w) {
             const int off = (p * R + seg < nr && ok[w]) ? (dw0 + p * R * nd + L * w) * 4 : INT_MIN;
-            xv[p][w] = __builtin_amdgcn_raw_buffer_load_b32(xr, off, 0, 2 /* nt */);
+            xv[p][w] = __builtin_amdgcn_raw_buffer_load_b32(xr, off, 0, 0);
         }
     }
 }
