@@ -417,10 +417,35 @@ __device__ __forceinline__ double readlane_f64(double v, int lane) {
 // are not needed address past its end and return 0 without a memory access,
 // so every load is issued unconditionally and the compiler can count the
 // loads in flight across the batches.
-template <int W, int R>
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x3_t __attribute__((ext_vector_type(3)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+// CT: lane l holds dwords W l .. W l + W - 1 of a row (nd = 64 W): one load
+// of 4 W bytes per lane and row.
+template <int W, int R, bool CT>
 __device__ __forceinline__ void load_rows(uint32_t (&xv)[R][W],
                                           __amdgpu_buffer_rsrc_t xr, int64_t r0, int nr, int nd,
                                           int lane, const bool (&ok)[W]) {
+    if constexpr (CT) {
+#pragma unroll
+        for (int j = 0; j < R; ++j) {
+            const int off = j < nr ? (int)(((r0 + j) * nd + W * lane) * 4) : INT_MIN;
+            if constexpr (W == 1) {
+                xv[j][0] = __builtin_amdgcn_raw_buffer_load_b32(xr, off, 0, 0);
+            } else if constexpr (W == 2) {
+                const u32x2_t v = __builtin_amdgcn_raw_buffer_load_b64(xr, off, 0, 0);
+                xv[j][0] = v[0]; xv[j][1] = v[1];
+            } else if constexpr (W == 3) {
+                const u32x3_t v = __builtin_amdgcn_raw_buffer_load_b96(xr, off, 0, 0);
+                xv[j][0] = v[0]; xv[j][1] = v[1]; xv[j][2] = v[2];
+            } else {
+                const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0);
+                xv[j][0] = v[0]; xv[j][1] = v[1]; xv[j][2] = v[2]; xv[j][3] = v[3];
+            }
+        }
+        return;
+    }
 #pragma unroll
     for (int j = 0; j < R; ++j) {
 #pragma unroll
@@ -500,11 +525,11 @@ __device__ __forceinline__ void rows_stats(const LnArgs& a, const RowsCtx<W>& k,
 // into bytes and stored as soon as it is computed, so that the stores of a
 // wavefront spread over its arithmetic instead of leaving together at its end;
 // the other rows are written element by element (their bytes read again).
-template <int W, int R>
+template <int W, int R, bool CT>
 __device__ __forceinline__ void rows_output(const LnArgs& a, const RowsCtx<W>& k,
                                             const double2* s_gb, const RowsStats<W, R>& st,
                                             int64_t r0, int nr, int nd, int lane,
-                                            uint32_t* y32) {
+                                            uint32_t* y32, __amdgpu_buffer_rsrc_t yr_rsrc) {
 #pragma unroll
     for (int j = 0; j < R; ++j) {
         if (j >= nr) break;
@@ -532,17 +557,31 @@ __device__ __forceinline__ void rows_output(const LnArgs& a, const RowsCtx<W>& k
                 // elements would not fit the register budget
                 __builtin_amdgcn_sched_barrier(0);
             }
-            uint32_t* yr = y32 + (r0 + j) * nd + lane;
+            if constexpr (CT) {
+                const int off = (int)(((r0 + j) * nd + W * lane) * 4);
+                if constexpr (W == 1) {
+                    __builtin_amdgcn_raw_buffer_store_b32(yo[0], yr_rsrc, off, 0, 2);
+                } else if constexpr (W == 2) {
+                    __builtin_amdgcn_raw_buffer_store_b64(u32x2_t{yo[0], yo[1]}, yr_rsrc, off, 0, 2);
+                } else if constexpr (W == 3) {
+                    __builtin_amdgcn_raw_buffer_store_b96(u32x3_t{yo[0], yo[1], yo[2]}, yr_rsrc, off, 0, 2);
+                } else {
+                    __builtin_amdgcn_raw_buffer_store_b128(u32x4_t{yo[0], yo[1], yo[2], yo[3]}, yr_rsrc, off, 0, 2);
+                }
+            } else {
+                uint32_t* yr = y32 + (r0 + j) * nd + lane;
 #pragma unroll
-            for (int w = 0; w < W; ++w)
-                if (k.ok[w]) __builtin_nontemporal_store(yo[w], yr + 64 * w);
+                for (int w = 0; w < W; ++w)
+                    if (k.ok[w]) __builtin_nontemporal_store(yo[w], yr + 64 * w);
+            }
         } else {
             const int8_t* xrow = a.x + (r0 + j) * a.C;
             int8_t* yrow = a.y + (r0 + j) * a.C;
 #pragma unroll 1
             for (int c = lane; c < a.C; c += 64) {
                 const int xh = ((int)xrow[c] - a.zp_in) * (1 << min((int)a.alpha[c], a.K));
-                const double2 gb = s_gb[(c & 3) * nd + (c >> 2)];
+                const int dq = c >> 2;
+                const double2 gb = s_gb[(c & 3) * nd + (CT ? (dq % W) * 64 + dq / W : dq)];
                 const double A = gb.x * rj;
                 const double B = gb.y - gb.x * mj;
                 yrow[c] = (int8_t)ln_requant(A, B, xh, a.bits, a.zp_out, k.qlo, k.qhi);
@@ -557,7 +596,7 @@ __device__ __forceinline__ void rows_output(const LnArgs& a, const RowsCtx<W>& k
 // arithmetic of the earlier ones.  No load is in flight across the loop's
 // back edge (a wait there would cover every outstanding load).  BLOCK threads
 // per workgroup; the grid sets the number of wavefronts per CU.
-template <int W, int R, int BLOCK, int NB>
+template <int W, int R, int BLOCK, int NB, bool CT>
 __global__ __launch_bounds__(BLOCK) void ln_rows_kernel(LnArgs a) {
     extern __shared__ double smem[];
     double2* s_gb = reinterpret_cast<double2*>(smem);        // (gs, bs) at [b][dword]
@@ -576,12 +615,14 @@ __global__ __launch_bounds__(BLOCK) void ln_rows_kernel(LnArgs a) {
     // the whole input, a.T * a.C < 2^31 bytes (checked by the launcher)
     const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
         (void*)a.x, (short)0, (int)(a.T * a.C), 0x00020000);
+    const __amdgpu_buffer_rsrc_t yrs = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)a.y, (short)0, (int)(a.T * a.C), 0x00020000);
     const int64_t base = a.T / nw, rem = a.T % nw;
     int64_t ra = gw * base + min(gw, rem);
     const int64_t r1 = ra + base + (gw < rem ? 1 : 0);
     RowsCtx<W> k;
 #pragma unroll
-    for (int w = 0; w < W; ++w) k.ok[w] = lane + 64 * w < nd;
+    for (int w = 0; w < W; ++w) k.ok[w] = CT || lane + 64 * w < nd;
 
     // Set-up, one thread per dword (4 channels; nd <= 256 <= blockDim): its
     // loads go first, then the first two batches of rows, so that the
@@ -593,6 +634,9 @@ __global__ __launch_bounds__(BLOCK) void ln_rows_kernel(LnArgs a) {
     //   s_pk[2 dw + 1] = bytes of 2^alpha, sum of -u 2^alpha, and the largest
     //                    and smallest high word of |gs| over the 4 channels
     const int sdw = threadIdx.x;
+    // LDS position of dword sdw: CT keeps the constants of the dwords a lane
+    // holds (W l + w) at w 64 + l, so the reads stay lane-consecutive
+    const int spos = CT ? (sdw % W) * 64 + sdw / W : sdw;
     float sg[4], sb[4];
     int sa[4];
     if (sdw < nd) {
@@ -608,7 +652,7 @@ __global__ __launch_bounds__(BLOCK) void ln_rows_kernel(LnArgs a) {
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
         nr[i] = (int)max<int64_t>(0, min<int64_t>(R, r1 - ra - R * i));
-        load_rows<W, R>(xv[i], xr, ra + R * i, nr[i], nd, lane, k.ok);
+        load_rows<W, R, CT>(xv[i], xr, ra + R * i, nr[i], nd, lane, k.ok);
     }
 
     const int u = a.zp_in + 128;
@@ -617,7 +661,7 @@ __global__ __launch_bounds__(BLOCK) void ln_rows_kernel(LnArgs a) {
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
             const double gs = (double)sg[b] / (double)a.s_out;
-            s_gb[b * nd + sdw] = double2{gs, (double)sb[b] / (double)a.s_out};
+            s_gb[b * nd + spos] = double2{gs, (double)sb[b] / (double)a.s_out};
             const int sh = min(sa[b], a.K);
             const uint32_t zm = (uint32_t)(-u) << sh;
             mulb |= (1u << sh) << (8 * b);
@@ -628,8 +672,8 @@ __global__ __launch_bounds__(BLOCK) void ln_rows_kernel(LnArgs a) {
             ghi = max(ghi, h);
             glo = min(glo, h);
         }
-        s_pk[2 * sdw] = uint4{mulp[0], mulp[1], zmp[0], zmp[1]};
-        s_pk[2 * sdw + 1] = uint4{mulb, m1p, ghi, glo};
+        s_pk[2 * spos] = uint4{mulp[0], mulp[1], zmp[0], zmp[1]};
+        s_pk[2 * spos + 1] = uint4{mulb, m1p, ghi, glo};
     }
     __syncthreads();
     if (nr[0] <= 0) return;
@@ -681,14 +725,14 @@ __global__ __launch_bounds__(BLOCK) void ln_rows_kernel(LnArgs a) {
             if (nr[i] <= 0) break;
             RowsStats<W, R> st;
             rows_stats<W, R>(a, k, xv[i], st);
-            rows_output<W, R>(a, k, s_gb, st, ra + R * i, nr[i], nd, lane, y32);
+            rows_output<W, R, CT>(a, k, s_gb, st, ra + R * i, nr[i], nd, lane, y32, yrs);
         }
         ra += NB * R;
         if (ra >= r1) break;
 #pragma unroll
         for (int i = 0; i < NB; ++i) {
             nr[i] = (int)max<int64_t>(0, min<int64_t>(R, r1 - ra - R * i));
-            load_rows<W, R>(xv[i], xr, ra + R * i, nr[i], nd, lane, k.ok);
+            load_rows<W, R, CT>(xv[i], xr, ra + R * i, nr[i], nd, lane, k.ok);
         }
     }
 }
@@ -964,8 +1008,12 @@ hipError_t launch_rows_rb(const LnArgs& a, int wpc, hipStream_t stream) {
     const int64_t waves = std::max<int64_t>(1, std::min<int64_t>(want, 256 * (int64_t)wpc));
     const int64_t blocks = (waves + kWaves - 1) / kWaves;
     const size_t lds = (size_t)a.C * 2 * sizeof(double) + (size_t)(a.C / 4) * 2 * sizeof(uint4);
-    launch_kernel(ln_rows_kernel<W, R, BLOCK, NB>, dim3((unsigned)blocks), dim3(BLOCK),
-                  lds, stream, a);
+    if (a.C == 256 * W)
+        launch_kernel(ln_rows_kernel<W, R, BLOCK, NB, true>, dim3((unsigned)blocks), dim3(BLOCK),
+                      lds, stream, a);
+    else
+        launch_kernel(ln_rows_kernel<W, R, BLOCK, NB, false>, dim3((unsigned)blocks), dim3(BLOCK),
+                      lds, stream, a);
     return hipGetLastError();
 }
 

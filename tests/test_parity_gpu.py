@@ -125,7 +125,7 @@ def test_ln_params_small_rows(fq, orc, C, K, bits):
     assert np.array_equal(_ln_gpu(fq, d, **over), _ln_ref(orc, d, **over))
 
 
-@pytest.mark.parametrize("C", [384, 96])
+@pytest.mark.parametrize("C", [384, 96, 768, 1024])
 def test_ln_edge_rows(fq, orc, C):
     """Constant rows (zero variance), rows at the zero point, gamma = 0, extreme
     affine values, tiny and huge s_out."""
@@ -133,7 +133,7 @@ def test_ln_edge_rows(fq, orc, C):
     d = W.ln_inputs(64, C, seed=9)
     x = d["x_q"].copy()
     x[0] = d["zp_in"]
-    x[1] = (d["zp_in"] + (8 >> np.minimum(d["alpha"], 3))).astype(np.int8)
+    x[1] = (d["zp_in"] + (8 >> np.minimum(d["alpha"].astype(np.int32), 3))).astype(np.int8)
     x[2] = 127
     x[3] = -128
     gamma = d["gamma"].copy()
