@@ -777,11 +777,50 @@ __device__ __forceinline__ double seg_bcast_f64(double v, int p) {
 // zeros for rows past nr and lanes past the row), as buffer loads that
 // address past the input when not needed.  dw0 is the dword index of the
 // lane's first dword in the batch's first row group (T C < 2^31 bytes).
-template <int W, int L, int P>
+// Stores the W packed dwords of a lane: one 4W-byte store (CT) or W dword
+// stores L dwords apart.
+template <int W, int L, bool CT>
+__device__ __forceinline__ void store_seg(const uint32_t (&pk)[W], __amdgpu_buffer_rsrc_t yrs,
+                                          int yoff, const bool (&ok)[W]) {
+    if constexpr (CT) {
+        if constexpr (W == 1) __builtin_amdgcn_raw_buffer_store_b32(pk[0], yrs, yoff, 0, 2);
+        else if constexpr (W == 2) __builtin_amdgcn_raw_buffer_store_b64(u32x2_t{pk[0], pk[1]}, yrs, yoff, 0, 2);
+        else if constexpr (W == 3)
+            __builtin_amdgcn_raw_buffer_store_b96(u32x3_t{pk[0], pk[1], pk[2]}, yrs, yoff, 0, 2);
+        else
+            __builtin_amdgcn_raw_buffer_store_b128(u32x4_t{pk[0], pk[1], pk[2], pk[3]}, yrs, yoff, 0, 2);
+    } else {
+#pragma unroll
+        for (int w = 0; w < W; ++w)
+            if (ok[w]) __builtin_amdgcn_raw_buffer_store_b32(pk[w], yrs, yoff + 4 * L * w, 0, 2 /* nt */);
+    }
+}
+
+template <int W, int L, int P, bool CT>
 __device__ __forceinline__ void load_seg(uint32_t (&xv)[P][W], __amdgpu_buffer_rsrc_t xr,
                                          int dw0, int nr, int nd, int seg,
                                          const bool (&ok)[W]) {
     constexpr int R = 64 / L;
+    if constexpr (CT) {
+        // lane li holds dwords W li .. W li + W - 1 of its row (nd = L W)
+#pragma unroll
+        for (int p = 0; p < P; ++p) {
+            const int off = p * R + seg < nr ? (dw0 + p * R * nd) * 4 : INT_MIN;
+            if constexpr (W == 1) {
+                xv[p][0] = __builtin_amdgcn_raw_buffer_load_b32(xr, off, 0, 0);
+            } else if constexpr (W == 2) {
+                const u32x2_t v = __builtin_amdgcn_raw_buffer_load_b64(xr, off, 0, 0);
+                xv[p][0] = v[0]; xv[p][1] = v[1];
+            } else if constexpr (W == 3) {
+                const u32x3_t v = __builtin_amdgcn_raw_buffer_load_b96(xr, off, 0, 0);
+                xv[p][0] = v[0]; xv[p][1] = v[1]; xv[p][2] = v[2];
+            } else {
+                const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0);
+                xv[p][0] = v[0]; xv[p][1] = v[1]; xv[p][2] = v[2]; xv[p][3] = v[3];
+            }
+        }
+        return;
+    }
 #pragma unroll
     for (int p = 0; p < P; ++p) {
 #pragma unroll
@@ -792,7 +831,7 @@ __device__ __forceinline__ void load_seg(uint32_t (&xv)[P][W], __amdgpu_buffer_r
     }
 }
 
-template <int W, int L, int P, int BLOCK>
+template <int W, int L, int P, int BLOCK, bool CT>
 __global__ __launch_bounds__(BLOCK) void ln_seg_kernel(LnArgs a) {
     static_assert(P <= L && P <= 8, "lane li < P of a row group keeps pass li");
     constexpr int R = 64 / L;
@@ -824,12 +863,14 @@ __global__ __launch_bounds__(BLOCK) void ln_seg_kernel(LnArgs a) {
         (void*)a.y, (short)0, (int)(a.T * a.C), 0x00020000);
     RowsCtx<W> k;
 #pragma unroll
-    for (int w = 0; w < W; ++w) k.ok[w] = li + L * w < nd;
-    int dw0 = ((int)ra + seg) * nd + li;
+    for (int w = 0; w < W; ++w) k.ok[w] = CT || li + L * w < nd;
+    int dw0 = ((int)ra + seg) * nd + (CT ? W * li : li);
 
     // set-up as in ln_rows_kernel: one thread per dword (nd < 64), and the
     // bounds of |gs| over the whole row
     const int sdw = threadIdx.x;
+    // LDS position of dword sdw (CT: dword W li + w at w L + li)
+    const int spos = CT ? (sdw % W) * L + sdw / W : sdw;
     float sg[4], sb[4];
     int sa[4];
     if (sdw < nd) {
@@ -842,7 +883,7 @@ __global__ __launch_bounds__(BLOCK) void ln_seg_kernel(LnArgs a) {
     }
     uint32_t xv[P][W];
     int nr = (int)max<int64_t>(0, min<int64_t>(P * R, r1 - ra));
-    load_seg<W, L, P>(xv, xr, dw0, nr, nd, seg, k.ok);
+    load_seg<W, L, P, CT>(xv, xr, dw0, nr, nd, seg, k.ok);
 
     const int u = a.zp_in + 128;
     uint32_t dhi = 0, dlo = 0x7FF00000u;
@@ -851,7 +892,7 @@ __global__ __launch_bounds__(BLOCK) void ln_seg_kernel(LnArgs a) {
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
             const double gs = (double)sg[b] / (double)a.s_out;
-            s_gb[b * nd + sdw] = double2{gs, (double)sb[b] / (double)a.s_out};
+            s_gb[b * nd + spos] = double2{gs, (double)sb[b] / (double)a.s_out};
             const int sh = min(sa[b], a.K);
             const uint32_t zm = (uint32_t)(-u) << sh;
             mulb |= (1u << sh) << (8 * b);
@@ -862,8 +903,8 @@ __global__ __launch_bounds__(BLOCK) void ln_seg_kernel(LnArgs a) {
             dhi = max(dhi, h);
             dlo = min(dlo, h);
         }
-        s_pk[2 * sdw] = uint4{mulp[0], mulp[1], zmp[0], zmp[1]};
-        s_pk[2 * sdw + 1] = uint4{mulb, m1p, 0u, 0u};
+        s_pk[2 * spos] = uint4{mulp[0], mulp[1], zmp[0], zmp[1]};
+        s_pk[2 * spos + 1] = uint4{mulb, m1p, 0u, 0u};
     }
     if (threadIdx.x < 64) {   // wave 0 holds every dword (nd < 64)
 #pragma unroll
@@ -954,6 +995,7 @@ __global__ __launch_bounds__(BLOCK) void ln_seg_kernel(LnArgs a) {
             const int j = p * R + seg;
             const int yoff = (dw0 + p * R * nd) * 4;   // the lane's first dword of the row
             if (j < nr && fp) {
+                uint32_t packs[W];
 #pragma unroll
                 for (int w = 0; w < W; ++w) {
                     int q[4];
@@ -968,11 +1010,14 @@ __global__ __launch_bounds__(BLOCK) void ln_seg_kernel(LnArgs a) {
                     }
                     const uint32_t lo = __builtin_amdgcn_perm((uint32_t)q[1], (uint32_t)q[0], 0x0C0C0400u);
                     const uint32_t hi = __builtin_amdgcn_perm((uint32_t)q[3], (uint32_t)q[2], 0x0C0C0400u);
-                    const uint32_t pack = __builtin_amdgcn_perm(hi, lo, 0x05040100u);
-                    if (k.ok[w]) __builtin_amdgcn_raw_buffer_store_b32(pack, yrs, yoff + 4 * L * w, 0, 2 /* nt */);
+                    packs[w] = __builtin_amdgcn_perm(hi, lo, 0x05040100u);
+                    if (!CT && k.ok[w])
+                        __builtin_amdgcn_raw_buffer_store_b32(packs[w], yrs, yoff + 4 * L * w, 0, 2 /* nt */);
                     __builtin_amdgcn_sched_barrier(0);
                 }
+                if (CT) store_seg<W, L, true>(packs, yrs, yoff, k.ok);
             } else if (j < nr) {
+                uint32_t packs[W];
 #pragma unroll
                 for (int w = 0; w < W; ++w) {
                     uint32_t pack = 0;
@@ -986,15 +1031,16 @@ __global__ __launch_bounds__(BLOCK) void ln_seg_kernel(LnArgs a) {
                         const int q = ln_requant(A, B, xh, a.bits, a.zp_out, k.qlo, k.qhi);
                         pack |= ((uint32_t)q & 0xFFu) << (8 * b);
                     }
-                    if (k.ok[w]) __builtin_amdgcn_raw_buffer_store_b32(pack, yrs, yoff + 4 * L * w, 0, 2 /* nt */);
+                    packs[w] = pack;
                 }
+                store_seg<W, L, CT>(packs, yrs, yoff, k.ok);
             }
         }
         ra += P * R;
         dw0 += P * R * nd;
         if (ra >= r1) break;
         nr = (int)max<int64_t>(0, min<int64_t>(P * R, r1 - ra));
-        load_seg<W, L, P>(xv, xr, dw0, nr, nd, seg, k.ok);
+        load_seg<W, L, P, CT>(xv, xr, dw0, nr, nd, seg, k.ok);
     }
 }
 
@@ -1054,8 +1100,12 @@ hipError_t launch_seg_b(const LnArgs& a, int wpc, hipStream_t stream) {
     const int64_t blocks = (waves + kWaves - 1) / kWaves;
     const size_t lds =
         (size_t)a.C * 2 * sizeof(double) + (size_t)(a.C / 4) * 2 * sizeof(uint4) + sizeof(uint4);
-    launch_kernel(ln_seg_kernel<W, L, P, BLOCK>, dim3((unsigned)blocks), dim3(BLOCK), lds, stream,
-                  a);
+    if (a.C == 4 * L * W)
+        launch_kernel(ln_seg_kernel<W, L, P, BLOCK, true>, dim3((unsigned)blocks), dim3(BLOCK), lds,
+                      stream, a);
+    else
+        launch_kernel(ln_seg_kernel<W, L, P, BLOCK, false>, dim3((unsigned)blocks), dim3(BLOCK), lds,
+                      stream, a);
     return hipGetLastError();
 }
 
