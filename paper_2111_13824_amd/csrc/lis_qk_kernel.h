@@ -92,7 +92,7 @@ __global__ __launch_bounds__(kBlock, 3) void lis_qk_kernel(LisArgs a, QkArgs qa,
             s = __builtin_amdgcn_sdot4(v.z, 0x01010101, s, false);
             s = __builtin_amdgcn_sdot4(v.w, 0x01010101, s, false);
         }
-        ck[j] = -(qa.zq * s);        // stored negated: one three-operand add per logit
+        ck[j] = -(qa.zq * s);        // stored negated: the initial accumulator of the logits
     }
     __syncthreads();
 
@@ -131,7 +131,11 @@ __global__ __launch_bounds__(kBlock, 3) void lis_qk_kernel(LisArgs a, QkArgs qa,
                 }
                 const int kt = 2 * c + h;
                 const int key = 16 * kt + r;          // A operand row of this lane
-                i32x4v s = {0, 0, 0, 0};
+                const int j0 = 16 * kt + 4 * kg;      // keys of s[0..3]
+                // the per-key zero-point terms enter as the accumulator's
+                // initial value (same layout: lane (r, kg) holds keys j0 ..
+                // j0 + 3), so the sum needs no separate add
+                i32x4v s = *reinterpret_cast<const i32x4v*>(ck + j0);
                 if constexpr (DK >= 64) {
 #pragma unroll
                     for (int m = 0; m < DK / 64; ++m) {
@@ -143,14 +147,12 @@ __global__ __launch_bounds__(kBlock, 3) void lis_qk_kernel(LisArgs a, QkArgs qa,
                     const int64_t av = *reinterpret_cast<const int64_t*>(kst + key * DK + 8 * kg);
                     s = __builtin_amdgcn_mfma_i32_16x16x32_i8(av, qb8, s, 0, 0, 0);
                 }
-                const int j0 = 16 * kt + 4 * kg;      // keys of s[0..3]
-                const i32x4v cv = *reinterpret_cast<const i32x4v*>(ck + j0);
 #pragma unroll
                 for (int t = 0; t < 4; ++t) {
                     // the per-query term zp_q zp_k dk - zp_k sum_c q[i][c] is
                     // left out: the Log-Int-Softmax of a row depends only on
                     // the differences of its logits (u = max - v)
-                    const int v = s[t] + cv[t];
+                    const int v = s[t];
                     // only the last chunk can hold keys past Lk
                     lg[c][4 * h + t] = (c < NC - 1 || j0 + t < a.Lk) ? v : INT_MIN;
                 }

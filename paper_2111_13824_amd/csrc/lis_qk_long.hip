@@ -32,7 +32,9 @@ __device__ __forceinline__ void qk_long_chunk(int (&lg)[8], const int8_t* kst, c
     for (int h = 0; h < 2; ++h) {
         const int kt = 2 * c + h;
         const int key = 16 * kt + r;
-        i32x4v s = {0, 0, 0, 0};
+        const int j0 = 16 * kt + 4 * kg;
+        // the per-key zero-point terms as the initial accumulator
+        i32x4v s = *reinterpret_cast<const i32x4v*>(ck + j0);
         if constexpr (DK >= 64) {
 #pragma unroll
             for (int m = 0; m < DK / 64; ++m) {
@@ -43,10 +45,8 @@ __device__ __forceinline__ void qk_long_chunk(int (&lg)[8], const int8_t* kst, c
             const int64_t av = *reinterpret_cast<const int64_t*>(kst + key * DK + 8 * kg);
             s = __builtin_amdgcn_mfma_i32_16x16x32_i8(av, qb8, s, 0, 0, 0);
         }
-        const int j0 = 16 * kt + 4 * kg;
-        const i32x4v cv = *reinterpret_cast<const i32x4v*>(ck + j0);
 #pragma unroll
-        for (int t = 0; t < 4; ++t) lg[4 * h + t] = j0 + t < Lk ? s[t] + cv[t] : INT_MIN;
+        for (int t = 0; t < 4; ++t) lg[4 * h + t] = j0 + t < Lk ? s[t] : INT_MIN;
     }
     if (brow) {
 #pragma unroll
