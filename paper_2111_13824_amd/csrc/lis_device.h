@@ -410,9 +410,13 @@ __device__ __forceinline__ int lis_code(uint32_t qL, uint32_t z, const RowSum& r
 // multiply-adds), which cost less than binary32 arithmetic; the host accepts
 // only scales for which those steps are exact.  k.magic and the shifted u are
 // below 2^24, so the product maps to one v_mul_hi_u32_u24.
+// P0: the pre-shift is known to be 0 (|q_ln2| > 256, i.e. s below about
+// 2.7e-3), which saves the shift of every key.
+template <bool P0 = false>
 __device__ __forceinline__ float iexp_fu(uint32_t u, const LisConsts& k) {
+    const uint32_t us = P0 ? u : (u << k.pre);
     const uint32_t z =
-        (uint32_t)(((uint64_t)((u << k.pre) & 0xFFFFFFu) * (uint64_t)(k.magic & 0xFFFFFFu)) >> 32);
+        (uint32_t)(((uint64_t)(us & 0xFFFFFFu) * (uint64_t)(k.magic & 0xFFFFFFu)) >> 32);
     // q_p + q_b = z d + (q_b - u); written out because the compiler would
     // otherwise select a 64-bit multiply-add
     uint32_t w;
@@ -423,8 +427,9 @@ __device__ __forceinline__ float iexp_fu(uint32_t u, const LisConsts& k) {
 
 // The same for a logit v of a row with maximum mx: u = mx - v clamped at
 // n |q_ln2|.
+template <bool P0 = false>
 __device__ __forceinline__ float iexp_f(int v, int mx, const LisConsts& k) {
-    return iexp_fu(min((uint32_t)mx - (uint32_t)v, k.u_max), k);
+    return iexp_fu<P0>(min((uint32_t)mx - (uint32_t)v, k.u_max), k);
 }
 
 // Code of one key on the float path, from e (its binary32 bit pattern) and the
@@ -528,7 +533,7 @@ __device__ __forceinline__ int tile_max(const int (&lg)[NC][8]) {
     return row4_max(mx);
 }
 
-template <int NC, bool FP, int NT>
+template <int NC, bool FP, int NT, bool P0 = false>
 __device__ __forceinline__ RowState tile_iexp(int (&lg)[NC][8], uint32_t (&zb)[NC][2],
                                               const LisConsts& k) {
     const int mx = tile_max<NC>(lg);
@@ -543,7 +548,7 @@ __device__ __forceinline__ RowState tile_iexp(int (&lg)[NC][8], uint32_t (&zb)[N
 #pragma unroll
             for (int t = 0; t < (c < NC - 1 ? 8 : NT); ++t) {
                 const int v = lg[c][t];
-                float e = iexp_f(v, mx, k);
+                float e = iexp_f<P0>(v, mx, k);
                 if (c == NC - 1) e = v != INT_MIN ? e : 0.0f;
                 part[t & 3] += (double)e;
                 lg[c][t] = __float_as_int(e);

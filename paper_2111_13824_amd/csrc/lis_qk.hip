@@ -24,7 +24,9 @@ hipError_t launch_lis_qk(const LisArgs& a, const QkInput& in, hipStream_t stream
     p.n_bias = a.bias ? (int64_t)a.Hb * a.Lq * a.Lk : 0;
     const size_t lds = (size_t)p.vt_bytes + (size_t)32 * nc * in.dk + (size_t)32 * nc * sizeof(int32_t);
     const bool half = a.Lk - 32 * (nc - 1) <= 16;
-    const bool fp = a.k.fp_ok != 0;
+    // float path (and its I-Exp without the pre-shift where that is 0) or the
+    // integer path
+    const int fp = a.k.fp_ok != 0 ? (a.k.pre == 0 ? 2 : 1) : 0;
     const QkArgs qa{in.q, in.k, in.zp_q, in.zp_k};
     // rows beyond 7 chunks: logits recomputed per pass from K in LDS
     if (nc > 7) return launch_qk_long(in.dk, dt, fp, a, qa, p, lds, stream);

@@ -5,7 +5,7 @@
 namespace fqvit {
 namespace lis {
 
-hipError_t launch_qk_dk64(int nc, int dtm, bool half, bool fp, const LisArgs& a, const QkArgs& qa,
+hipError_t launch_qk_dk64(int nc, int dtm, bool half, int fp, const LisArgs& a, const QkArgs& qa,
                           const LisLaunch& p, size_t lds, hipStream_t stream) {
     return launch_qk_dk<64>(nc, dtm, half, fp, a, qa, p, lds, stream);
 }

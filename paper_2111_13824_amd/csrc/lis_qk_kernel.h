@@ -47,7 +47,7 @@ __device__ __forceinline__ int kst_off(int j, int u) {
     return j * DK + 16 * u;
 }
 
-template <int NC, int DTMAX, bool HALF, bool FP, int DK>
+template <int NC, int DTMAX, bool HALF, bool FP, int DK, bool P0 = false>
 __global__ __launch_bounds__(kBlock, 3) void lis_qk_kernel(LisArgs a, QkArgs qa, LisLaunch p) {
     constexpr int NT = HALF ? 4 : 8;
     constexpr int KP = 32 * NC;                 // staged keys (zero past Lk)
@@ -172,7 +172,7 @@ __global__ __launch_bounds__(kBlock, 3) void lis_qk_kernel(LisArgs a, QkArgs qa,
             }
         }
         uint32_t zb[NC][2];
-        const RowState st = tile_iexp<NC, FP, NT>(lg, zb, k);
+        const RowState st = tile_iexp<NC, FP, NT, P0>(lg, zb, k);
         f32x4 acc[DTMAX];
 #pragma unroll
         for (int dt = 0; dt < DTMAX; ++dt) acc[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -189,14 +189,17 @@ __global__ __launch_bounds__(kBlock, 3) void lis_qk_kernel(LisArgs a, QkArgs qa,
     }
 }
 
+// fpm: 0 the integer path, 1 the float path, 2 the float path with the
+// I-Exp pre-shift 0.
 template <int DK, int NC>
-hipError_t launch_qk_nc(int dtm, bool half, bool fp, const LisArgs& a, const QkArgs& qa,
+hipError_t launch_qk_nc(int dtm, bool half, int fpm, const LisArgs& a, const QkArgs& qa,
                         const LisLaunch& p, size_t lds, hipStream_t stream) {
     const dim3 grid((unsigned)a.G), block(kBlock);
-#define FQ_QK(DT, H, F) \
-    launch_kernel(lis_qk_kernel<NC, DT, H, F, DK>, grid, block, lds, stream, a, qa, p)
+#define FQ_QK(DT, H, F, P0) \
+    launch_kernel(lis_qk_kernel<NC, DT, H, F, DK, P0>, grid, block, lds, stream, a, qa, p)
 #define FQ_QK_F(DT, H) \
-    if (fp) FQ_QK(DT, H, true); else FQ_QK(DT, H, false)
+    if (fpm == 2) FQ_QK(DT, H, true, true); else if (fpm == 1) FQ_QK(DT, H, true, false); \
+    else FQ_QK(DT, H, false, false)
 #define FQ_QK_H(DT) \
     if (half) { FQ_QK_F(DT, true); } else { FQ_QK_F(DT, false); }
     if (dtm == 2) { FQ_QK_H(2) }
@@ -208,7 +211,7 @@ hipError_t launch_qk_nc(int dtm, bool half, bool fp, const LisArgs& a, const QkA
 }
 
 template <int DK>
-hipError_t launch_qk_dk(int nc, int dtm, bool half, bool fp, const LisArgs& a, const QkArgs& qa,
+hipError_t launch_qk_dk(int nc, int dtm, bool half, int fp, const LisArgs& a, const QkArgs& qa,
                         const LisLaunch& p, size_t lds, hipStream_t stream) {
     switch (nc) {
         case 1: return launch_qk_nc<DK, 1>(dtm, half, fp, a, qa, p, lds, stream);
@@ -222,13 +225,13 @@ hipError_t launch_qk_dk(int nc, int dtm, bool half, bool fp, const LisArgs& a, c
     }
 }
 
-hipError_t launch_qk_dk32(int nc, int dtm, bool half, bool fp, const LisArgs& a, const QkArgs& qa,
+hipError_t launch_qk_dk32(int nc, int dtm, bool half, int fp, const LisArgs& a, const QkArgs& qa,
                           const LisLaunch& p, size_t lds, hipStream_t stream);
 // Rows of 8 to 20 chunks (lis_qk_long.hip): one workgroup of 12 wavefronts per
 // unit, three passes over K in LDS per tile.
-hipError_t launch_qk_long(int dk, int dtm, bool fp, const LisArgs& a, const QkArgs& qa,
+hipError_t launch_qk_long(int dk, int dtm, int fp, const LisArgs& a, const QkArgs& qa,
                           const LisLaunch& p, size_t lds, hipStream_t stream);
-hipError_t launch_qk_dk64(int nc, int dtm, bool half, bool fp, const LisArgs& a, const QkArgs& qa,
+hipError_t launch_qk_dk64(int nc, int dtm, bool half, int fp, const LisArgs& a, const QkArgs& qa,
                           const LisLaunch& p, size_t lds, hipStream_t stream);
 
 }  // namespace lis

@@ -57,7 +57,7 @@ __device__ __forceinline__ void qk_long_chunk(int (&lg)[8], const int8_t* kst, c
     }
 }
 
-template <int DTMAX, bool FP, int DK>
+template <int DTMAX, bool FP, int DK, bool P0 = false>
 __global__ __launch_bounds__(kQkLongBlock) void lis_qk_long_kernel(LisArgs a, QkArgs qa,
                                                                    LisLaunch p) {
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
@@ -144,7 +144,7 @@ __global__ __launch_bounds__(kQkLongBlock) void lis_qk_long_kernel(LisArgs a, Qk
                 qk_long_chunk<DK>(lg, kst, ck, qb, qb8, brow, c, r, kg, Lk);
 #pragma unroll
                 for (int t = 0; t < 8; ++t) {
-                    const float e = iexp_f(lg[t], mx, k);
+                    const float e = iexp_f<P0>(lg[t], mx, k);
                     part[t & 1] += lg[t] != INT_MIN ? (double)e : 0.0;
                 }
             }
@@ -181,7 +181,7 @@ __global__ __launch_bounds__(kQkLongBlock) void lis_qk_long_kernel(LisArgs a, Qk
             for (int t = 0; t < 8; ++t) {
                 const bool valid = lg[t] != INT_MIN;
                 if constexpr (FP) {
-                    const int eb = __float_as_int(iexp_f(valid ? lg[t] : mx, mx, k));
+                    const int eb = __float_as_int(iexp_f<P0>(valid ? lg[t] : mx, mx, k));
                     pbits[t] = valid ? (127u + code_rev_f(eb, st, kr)) << 7 : 0u;
                 } else {
                     uint32_t z;
@@ -199,22 +199,25 @@ __global__ __launch_bounds__(kQkLongBlock) void lis_qk_long_kernel(LisArgs a, Qk
 }
 
 template <int DK>
-hipError_t launch_qk_long_dk(int dtm, bool fp, const LisArgs& a, const QkArgs& qa,
+hipError_t launch_qk_long_dk(int dtm, int fpm, const LisArgs& a, const QkArgs& qa,
                              const LisLaunch& p, size_t lds, hipStream_t stream) {
     const dim3 grid((unsigned)a.G), block(kQkLongBlock);
-#define FQ_QKL(DT, F) launch_kernel(lis_qk_long_kernel<DT, F, DK>, grid, block, lds, stream, a, qa, p)
+#define FQ_QKL(DT, F, P0) \
+    launch_kernel(lis_qk_long_kernel<DT, F, DK, P0>, grid, block, lds, stream, a, qa, p)
     if (dtm == 2) {
-        if (fp) FQ_QKL(2, true);
-        else FQ_QKL(2, false);
+        if (fpm == 2) FQ_QKL(2, true, true);
+        else if (fpm == 1) FQ_QKL(2, true, false);
+        else FQ_QKL(2, false, false);
     } else {
-        if (fp) FQ_QKL(4, true);
-        else FQ_QKL(4, false);
+        if (fpm == 2) FQ_QKL(4, true, true);
+        else if (fpm == 1) FQ_QKL(4, true, false);
+        else FQ_QKL(4, false, false);
     }
 #undef FQ_QKL
     return hipGetLastError();
 }
 
-hipError_t launch_qk_long(int dk, int dtm, bool fp, const LisArgs& a, const QkArgs& qa,
+hipError_t launch_qk_long(int dk, int dtm, int fp, const LisArgs& a, const QkArgs& qa,
                           const LisLaunch& p, size_t lds, hipStream_t stream) {
     return dk == 32 ? launch_qk_long_dk<32>(dtm, fp, a, qa, p, lds, stream)
                     : launch_qk_long_dk<64>(dtm, fp, a, qa, p, lds, stream);
