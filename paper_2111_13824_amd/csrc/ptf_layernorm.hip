@@ -405,6 +405,10 @@ __device__ __forceinline__ uint32_t row16_sum(uint32_t v) {
     return v;
 }
 
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x3_t __attribute__((ext_vector_type(3)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
 __device__ __forceinline__ double readlane_f64(double v, int lane) {
     const uint64_t b = (uint64_t)__double_as_longlong(v);
     const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)b, lane);
@@ -417,10 +421,6 @@ __device__ __forceinline__ double readlane_f64(double v, int lane) {
 // are not needed address past its end and return 0 without a memory access,
 // so every load is issued unconditionally and the compiler can count the
 // loads in flight across the batches.
-typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
-typedef uint32_t u32x3_t __attribute__((ext_vector_type(3)));
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
-
 // CT: lane l holds dwords W l .. W l + W - 1 of a row (nd = 64 W): one load
 // of 4 W bytes per lane and row.
 template <int W, int R, bool CT>
