@@ -1195,15 +1195,11 @@ hipError_t launch_ptf_layernorm(const LnArgs& a, hipStream_t stream) {
     }
     // Per-lane sums of squares: 4W values of at most (255 * 2^K)^2 each.
     const bool wide = (double)(4 * best_w) * 65025.0 * (double)(1 << (2 * a.K)) >= 2147483647.0;
-    if (!wide && best_l >= 3 && best_l <= 5 && best_w <= 4 &&
-        a.T * (int64_t)a.C < ((int64_t)1 << 31)) {
-        switch (best_w) {
-            case 1: return launch_seg<1>(a, best_l, stream);
-            case 2: return launch_seg<2>(a, best_l, stream);
-            case 3: return launch_seg<3>(a, best_l, stream);
-            default: return launch_seg<4>(a, best_l, stream);
-        }
-    }
+    // The choice above gives odd W wherever L < 64: an even W ties with twice
+    // the lanes and half the dwords, which the scan (most lanes first) keeps.
+    if (!wide && best_l >= 3 && best_l <= 5 && (best_w == 1 || best_w == 3) &&
+        a.T * (int64_t)a.C < ((int64_t)1 << 31))
+        return best_w == 1 ? launch_seg<1>(a, best_l, stream) : launch_seg<3>(a, best_l, stream);
     switch (best_w) {
         case 1: return launch_fast<1>(a, best_l, wide, stream);
         case 2: return launch_fast<2>(a, best_l, wide, stream);
