@@ -869,11 +869,88 @@ __device__ __forceinline__ void load_one_chunk(int (&lg)[NC][8], const RowPtrs& 
     else load_chunk<HALF, DEFER>(lg[NC - 1], rp.row, rp.brow, NC - 1, kg, Lk, rp.tail_vec);
 }
 
+// Maximum and sum over all 64 lanes: the four rows of sixteen lanes by the
+// lane swaps, then within each row by DPP rotations (every lane ends with the
+// total).  The sum is exact for integers below 2^53, in any order.
+__device__ __forceinline__ int wave_max(int v) {
+    v = row4_max(v);
+    v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x128, 0xF, 0xF, false));   // row_ror:8
+    v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x124, 0xF, 0xF, false));   // row_ror:4
+    v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x122, 0xF, 0xF, false));   // row_ror:2
+    return max(v, __builtin_amdgcn_update_dpp(0, v, 0x121, 0xF, 0xF, false)); // row_ror:1
+}
+
+__device__ __forceinline__ double wave_sum(double v) {
+    v = row4_sum(v);
+#pragma unroll
+    for (int s = 3; s >= 0; --s) {
+        const uint64_t b = (uint64_t)__double_as_longlong(v);
+        int lo = (int)(uint32_t)b, hi = (int)(uint32_t)(b >> 32);
+        switch (s) {
+            case 3: lo = __builtin_amdgcn_update_dpp(0, lo, 0x128, 0xF, 0xF, false);
+                    hi = __builtin_amdgcn_update_dpp(0, hi, 0x128, 0xF, 0xF, false); break;
+            case 2: lo = __builtin_amdgcn_update_dpp(0, lo, 0x124, 0xF, 0xF, false);
+                    hi = __builtin_amdgcn_update_dpp(0, hi, 0x124, 0xF, 0xF, false); break;
+            case 1: lo = __builtin_amdgcn_update_dpp(0, lo, 0x122, 0xF, 0xF, false);
+                    hi = __builtin_amdgcn_update_dpp(0, hi, 0x122, 0xF, 0xF, false); break;
+            default: lo = __builtin_amdgcn_update_dpp(0, lo, 0x121, 0xF, 0xF, false);
+                     hi = __builtin_amdgcn_update_dpp(0, hi, 0x121, 0xF, 0xF, false); break;
+        }
+        v += __longlong_as_double((int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo));
+    }
+    return v;
+}
+
+// A tile of one row (the last tile of units of 16 m + 1 rows, rows of at most
+// two chunks), at the cost of one key per lane instead of a 16-row tile's
+// eight per chunk: lane l takes key l (I-Exp, the wavefront's maximum and
+// sum, its code by the float path's threshold form), the bf16 bits of
+// 2^(N - code) go to LDS at the key's position in the matrix cores' order, and
+// the lanes of row 0 read them back as the A operand of the usual P x V^T
+// products (the other rows zero).  Same values as the 16-row tile: the row's
+// maximum, its exact sum and each key's code do not depend on the lane layout.
+template <int NC, int DTMAX>
+__device__ __forceinline__ void unit_row1(const LisArgs& a, const LisLaunch& p, const LisConsts& k,
+                                          const uint16_t* vt, int32_t* ot, const UnitBase& ub,
+                                          int64_t g, int i0, int lane, int r, int kg) {
+    static_assert(NC <= 2, "one key per lane");
+    const int j = lane;
+    const bool key = j < a.Lk && j < 32 * NC;
+    const int64_t off = (int64_t)i0 * a.Lk + j;
+    int v = INT_MIN;
+    if (key) v = a.logits[ub.loff + off] + (a.bias ? a.bias[ub.boff + off] : 0);
+    const int mx = wave_max(v);
+    const float e = key ? iexp_f(v, mx, k) : 0.0f;
+    const double S2 = 2.0 * wave_sum((double)e);
+    RowState st;
+    st.S2s = S2 * kCodeScale;
+    st.sc = kCodeScale;
+    asm volatile("" : "+s"(st.sc));
+    st.tau = third_floor_f32(S2);
+    const uint32_t kr = ((uint32_t)(k.top + 1) << 25) - 1u;
+    const uint32_t x = key ? (127u + code_rev_f(__float_as_int(e), st, kr)) << 7 : 0u;
+    uint16_t* pl = reinterpret_cast<uint16_t*>(ot);
+    if (j < 32 * NC) pl[32 * (j >> 5) + chunk_pos(j & 31)] = (uint16_t)x;
+    __builtin_amdgcn_wave_barrier();
+    f32x4 acc[DTMAX];
+#pragma unroll
+    for (int dt = 0; dt < DTMAX; ++dt) acc[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+        const u32x4 w = *reinterpret_cast<const u32x4*>(pl + 32 * c + 8 * kg);
+        const u32x4 pb = r == 0 ? w : u32x4{0u, 0u, 0u, 0u};
+        chunk_mfma<DTMAX, false>(acc, pb, vt, p.ld, c, r, kg);
+    }
+    __builtin_amdgcn_wave_barrier();
+    if (p.out_vec) store_out_rows<DTMAX>(acc, ot, a, g, i0, lane, r, kg);
+    else store_out<DTMAX>(acc, a, g, i0, r, kg);
+}
+
 template <int NC, bool FUSED, int DTMAX, bool HALF, int WPU>
 __device__ __forceinline__ void unit_tile(int (&cur)[NC][8], int (&nxt)[NC][8], const LisArgs& a,
                                           const LisLaunch& p, const LisConsts& k, const uint16_t* vt,
                                           int32_t* ot, const UnitBase& ub, int64_t g, int tile,
-                                          int lane, int r, int kg, uint32_t valid) {
+                                          int ntl, int lane, int r, int kg, uint32_t valid) {
     constexpr int NT = HALF ? 4 : 8;
     constexpr int PF = unit_prefetch(NC, FUSED, DTMAX, HALF);
     constexpr bool DF = unit_defer(NC, FUSED);
@@ -881,7 +958,7 @@ __device__ __forceinline__ void unit_tile(int (&cur)[NC][8], int (&nxt)[NC][8], 
     // Always prefetch (a conditional load would keep the stale buffer live
     // across the loop); past the last tile the current rows, still in cache,
     // are read again.
-    const int nt = tile + WPU < p.ntiles ? tile + WPU : tile;
+    const int nt = tile + WPU < ntl ? tile + WPU : tile;
     const RowPtrs rn = unit_row<NC>(a, p, ub, min(16 * nt + r, a.Lq - 1));
     uint32_t zb[NC][2];
     if (DF) mask_last<NC, NT>(cur, valid);
@@ -954,11 +1031,13 @@ __device__ __forceinline__ void unit_tile(int (&cur)[NC][8], int (&nxt)[NC][8], 
 // Minimum wavefronts per SIMD the register allocation is held to (the second
 // argument of __launch_bounds__): three for four wavefronts per unit (168
 // registers); for the small units that take one or two, six where the kernel
-// fits 80 registers (fused rows of up to two chunks with d <= 32, codes-only
-// rows of one chunk), so that as many units are in flight as the CU holds,
-// and four otherwise (128 registers: at 80 those spilled).
+// fits 80 registers (codes-only rows of one chunk), so that as many units are
+// in flight as the CU holds, five for fused rows of up to two chunks with
+// d <= 32 (96 registers: with the one-row tile path they spilled at 80; on
+// the Swin-S shapes five and six measured the same without it), and four
+// otherwise (128 registers).
 constexpr int unit_waves_per_simd(int NC, bool FUSED, int DTMAX, int WPU) {
-    return WPU == 4 ? 3 : ((FUSED ? (NC <= 2 && DTMAX <= 2) : NC <= 1) ? 6 : 4);
+    return WPU == 4 ? 3 : (FUSED && NC <= 2 && DTMAX <= 2 ? 5 : (!FUSED && NC <= 1) ? 6 : 4);
 }
 
 // WPU wavefronts per unit (4, or fewer for units of few tiles, so that each
@@ -986,9 +1065,14 @@ __global__ __launch_bounds__(64 * WPU, unit_waves_per_simd(NC, FUSED, DTMAX, WPU
     UnitBase ub;
     ub.loff = g * a.Lq * (int64_t)a.Lk;
     ub.boff = a.bias ? (g % a.Hb) * a.Lq * (int64_t)a.Lk : 0;
+    // Fused rows of at most two chunks: a last tile of one row (units of
+    // 16 m + 1 rows) is left out of the tile loop and taken by unit_row1 after
+    // it, where neither tile buffer is live.
+    constexpr bool kRow1 = FUSED && NC <= 2;
+    const int ntl = kRow1 && (a.Lq & 15) == 1 ? p.ntiles - 1 : p.ntiles;
     int bufA[NC][8], bufB[NC][8];
     int tile = (wave + (int)(g % WPU)) % WPU;
-    if (tile < p.ntiles)
+    if (tile < ntl)
         tile_load<NC, HALF, 0, NC, unit_defer(NC, FUSED)>(
             bufA, unit_row<NC>(a, p, ub, min(16 * tile + r, a.Lq - 1)), kg, a.Lk);
     const uint32_t valid = unit_defer(NC, FUSED) ? last_valid<NC>(kg, a.Lk) : 0xFFu;
@@ -999,14 +1083,18 @@ __global__ __launch_bounds__(64 * WPU, unit_waves_per_simd(NC, FUSED, DTMAX, WPU
     // LDS per wavefront: the output transpose (fused) or the tile's code rows
     int32_t* ot = FUSED ? reinterpret_cast<int32_t*>(smem + p.vt_bytes) + wave * out_lds_dwords<DTMAX>()
                         : reinterpret_cast<int32_t*>(smem + wave * p.codes_ldw);
-    while (tile < p.ntiles) {
-        unit_tile<NC, FUSED, DTMAX, HALF, WPU>(bufA, bufB, a, p, k, vt, ot, ub, g, tile, lane, r, kg,
-                                               valid);
+    while (tile < ntl) {
+        unit_tile<NC, FUSED, DTMAX, HALF, WPU>(bufA, bufB, a, p, k, vt, ot, ub, g, tile, ntl, lane, r,
+                                               kg, valid);
         tile += WPU;
-        if (tile >= p.ntiles) break;
-        unit_tile<NC, FUSED, DTMAX, HALF, WPU>(bufB, bufA, a, p, k, vt, ot, ub, g, tile, lane, r, kg,
-                                               valid);
+        if (tile >= ntl) break;
+        unit_tile<NC, FUSED, DTMAX, HALF, WPU>(bufB, bufA, a, p, k, vt, ot, ub, g, tile, ntl, lane, r,
+                                               kg, valid);
         tile += WPU;
+    }
+    if constexpr (kRow1) {
+        if (tile == ntl && ntl < p.ntiles)
+            unit_row1<NC, DTMAX>(a, p, k, vt, ot, ub, g, 16 * tile, lane, r, kg);
     }
 }
 
